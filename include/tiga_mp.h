@@ -1,0 +1,242 @@
+/*
+ * tiga_mp.h -- C ABI of the MI355X (gfx950) fused message-passing library.
+ *
+ * Fused message passing (Tiga, "Compiling Graph Message Passing at Scale"):
+ * for every destination entity the library traverses a relation, forms one
+ * message per (source, destination) pair and folds it into the reducer state
+ * immediately, so neither the edge list of a generated relation nor any
+ * per-edge message array is ever stored (Section 3.1 message/update equation;
+ * Section 4.2 on fused row traversal versus materialized E*F messages).
+ *
+ * Three relations are supported:
+ *   - a stored destination-major CSR graph (Sections 3.1 and 4.3),
+ *   - a radius relation generated from positions through a cell directory
+ *     (Section 4.9),
+ *   - the dense all-pairs relation, which needs no edge array (Section 1).
+ * Reverse mode (Section 5, vector-Jacobian products) is provided for the CSR
+ * and radius relations.
+ *
+ * Conventions shared by every entry point
+ *   - Arrays are DEVICE pointers unless a comment says otherwise.  The caller
+ *     owns every buffer, including the workspace `ws` of `ws_bytes` bytes
+ *     (size it with the matching *_workspace query; it must be 256-byte
+ *     aligned).  The library keeps no pointer after the call returns.
+ *   - Work is enqueued on `stream` (a hipStream_t passed as void*; NULL is the
+ *     null stream).  Calls return before the work completes; a device fault
+ *     surfaces at the caller's next synchronization.  Only
+ *     tiga_csr_validate(level 2) and tiga_radius_neighbors synchronize.
+ *   - Outputs are overwritten, never accumulated into.
+ *   - fp32 features are row-major [rows, feat].  A 16-byte aligned feature
+ *     array with feat % 4 == 0 takes the vector path; any other width works
+ *     through the scalar path.
+ *   - Arguments are checked on the host before anything is enqueued.  On
+ *     error the call returns a negative status, enqueues nothing, and
+ *     tiga_last_error() describes the problem.  There is no silent fallback:
+ *     unsupported combinations return TIGA_EUNSUPPORTED (the paper requires
+ *     explicit diagnosis rather than a substituted route, Sections 4.1 and 4.8).
+ *   - The library holds no global mutable state other than the per-thread
+ *     error string and the per-thread profiling events; calls are reentrant.
+ */
+#ifndef TIGA_MP_H
+#define TIGA_MP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TIGA_MP_ABI_VERSION 1
+
+/* Status codes. */
+enum tiga_status {
+    TIGA_OK = 0,
+    TIGA_EINVAL = -1,       /* bad argument (NULL, negative size, misaligned ws) */
+    TIGA_EGRAPH = -2,       /* the relation violates CSR invariants (validation) */
+    TIGA_EUNSUPPORTED = -3, /* valid request this library does not implement */
+    TIGA_EWORKSPACE = -4,   /* ws_bytes smaller than the workspace query */
+    TIGA_EDEVICE = -5       /* a HIP call failed */
+};
+
+/* Reducers (Section 3.1: identity, lift, combine, finalize).
+ *   SUM: identity 0; an empty row finalizes to 0.
+ *   MAX: identity -inf; ties keep the lowest edge position; an empty row
+ *        finalizes to value 0 with argmax -1. */
+enum tiga_reducer { TIGA_REDUCE_SUM = 0, TIGA_REDUCE_MAX = 1 };
+
+/* Messages over a stored CSR relation (edge function of Section 3.1). */
+enum tiga_csr_msg {
+    TIGA_MSG_SRC = 0,             /* m_e = x[s(e)]          (w_edge must be NULL) */
+    TIGA_MSG_EDGE_SCALED_SRC = 1  /* m_e = w[e] * x[s(e)]   (w_edge required)     */
+};
+
+/* Destination-major CSR relation (Sections 3.1, 4.3).  Destination row i owns
+ * edge positions [row_ptr[i], row_ptr[i+1]); the edge position indexes edge
+ * fields and col_idx[e] is the source id.  Duplicates and self edges are
+ * ordinary separate edges; num_src may differ from num_dst.
+ *   row_ptr: int64 [num_dst + 1], row_ptr[0] == 0, non-decreasing,
+ *            row_ptr[num_dst] == num_edges.
+ *   col_idx: int32 [num_edges], each in [0, num_src).
+ * The struct itself lives in HOST memory; the two arrays on the device. */
+typedef struct {
+    int64_t num_dst;
+    int64_t num_src;
+    int64_t num_edges;
+    const int64_t *row_ptr;
+    const int32_t *col_idx;
+} tiga_csr;
+
+/* Reverse incidence of a tiga_csr (the transposed relation; Section 4.6
+ * notes that source gradients accumulate over reverse incidence).
+ *   src_ptr: int64 [num_src + 1]; source j owns slots [src_ptr[j], src_ptr[j+1]).
+ *   edge_id: int32 [num_edges]; the forward edge position of each slot,
+ *            ascending within a source (a stable transpose).
+ *   dst_idx: int32 [num_edges]; the destination row of that edge.
+ * Built by tiga_csr_transpose; valid only for the unchanged topology (a
+ * topology snapshot is fixed for derivatives, Section 3.2). */
+typedef struct {
+    const int64_t *src_ptr;
+    const int32_t *edge_id;
+    const int32_t *dst_idx;
+} tiga_csr_t;
+
+/* ---------------------------------------------------------------- errors */
+
+/* Message describing the last failure on the calling thread ("" if none).
+ * Valid until the next library call on that thread.  Host pointer. */
+const char *tiga_last_error(void);
+
+/* TIGA_MP_ABI_VERSION of the built library. */
+int tiga_mp_abi_version(void);
+
+/* ------------------------------------------------------------ stored CSR */
+
+/* Workspace bytes for tiga_mp_csr_fwd on this relation shape (0 on error). */
+size_t tiga_mp_csr_fwd_workspace(const tiga_csr *rel, int32_t feat, int reducer);
+
+/* Forward fused aggregation over a stored CSR relation (Section 3.1 equation,
+ * Section 4.3 destination-major traversal, Section 4.4 bounded neighbour tiles
+ * with a degree guard and a split of high-degree rows into partial states
+ * merged afterwards):
+ *   SUM: y[i,f] = sum_{e in row i} m_e[f]
+ *   MAX: y[i,f] = max_{e in row i} m_e[f], argmax[i,f] = that e (lowest on ties)
+ * with m_e = x_src[col[e], :] or w_edge[e] * x_src[col[e], :] (one fp32
+ * multiply, so MAX values are exact products).
+ *   x_src:  fp32 [num_src, feat];  w_edge: fp32 [num_edges] or NULL (see msg)
+ *   y:      fp32 [num_dst, feat], overwritten
+ *   argmax: int32 [num_dst, feat] for MAX (required), NULL for SUM
+ * SUM results are deterministic (fixed reduction tree) but not bit-identical
+ * to a serial sum; MAX results are exact.  MAX requires num_edges < 2^31.
+ * Errors: TIGA_EINVAL, TIGA_EUNSUPPORTED, TIGA_EWORKSPACE, TIGA_EDEVICE. */
+int tiga_mp_csr_fwd(const tiga_csr *rel, int32_t feat, const float *x_src, int msg,
+                    const float *w_edge, int reducer, float *y, int32_t *argmax,
+                    void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes for tiga_mp_csr_bwd (0 on error). */
+size_t tiga_mp_csr_bwd_workspace(const tiga_csr *rel, int32_t feat, int reducer);
+
+/* Vector-Jacobian product of tiga_mp_csr_fwd (Section 5 weighted-sum adjoint):
+ *   SUM: dx[j,f] = sum_{e: col[e]=j} w[e] dy[d(e),f];  dw[e] = sum_f x[col[e],f] dy[d(e),f]
+ *   MAX: the same terms restricted to the selected edge e* = argmax[i,f] of
+ *        each (i,f); argmax is the forward's output (required for MAX).
+ * (w = 1 under TIGA_MSG_SRC.)  dx: fp32 [num_src, feat]; dw: fp32 [num_edges];
+ * either may be NULL (skipped) and each is overwritten.  dw requires
+ * TIGA_MSG_EDGE_SCALED_SRC.
+ * rev == NULL: dx accumulates with device atomics (fast, order not fixed).
+ * rev != NULL: dx is gathered over the reverse incidence (deterministic).
+ * Errors: as tiga_mp_csr_fwd. */
+int tiga_mp_csr_bwd(const tiga_csr *rel, const tiga_csr_t *rev, int32_t feat,
+                    const float *x_src, int msg, const float *w_edge, int reducer,
+                    const int32_t *argmax, const float *dy, float *dx, float *dw,
+                    void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes for tiga_csr_transpose (0 on error). */
+size_t tiga_csr_transpose_workspace(const tiga_csr *rel);
+
+/* Build the reverse incidence (see tiga_csr_t) with a stable sort by source:
+ * within a source, edge ids ascend.  Topology set-up: build once per
+ * unchanged topology.  src_ptr int64 [num_src+1], edge_id and dst_idx int32
+ * [num_edges], all overwritten.  Requires num_edges < 2^31. */
+int tiga_csr_transpose(const tiga_csr *rel, int64_t *src_ptr, int32_t *edge_id,
+                       int32_t *dst_idx, void *ws, size_t ws_bytes, void *stream);
+
+/* CSR validation (the paper's validate="full" and basic modes, Section 6.3):
+ *   level 1: host-only metadata checks (sizes, pointers); enqueues nothing.
+ *   level 2: additionally scans the device arrays: row_ptr[0] == 0,
+ *            non-decreasing, row_ptr[num_dst] == num_edges, every col_idx in
+ *            [0, num_src).  Synchronizes `stream`.
+ * Returns TIGA_OK or TIGA_EGRAPH (the first violation is described by
+ * tiga_last_error()). */
+int tiga_csr_validate(const tiga_csr *rel, int level, void *stream);
+
+/* -------------------------------------------------- generated radius relation */
+
+/* Workspace bytes for tiga_mp_radius_fwd / _bwd / tiga_radius_neighbors on n
+ * points with feat features (0 on error). */
+size_t tiga_mp_radius_workspace(int64_t n, int32_t feat);
+
+/* Forward over the radius relation generated from positions (Section 4.9:
+ * a cell directory restricts candidates, an exact distance predicate accepts,
+ * messages are consumed without storing accepted edges):
+ *   N(i) = { j != i : d2(i,j) < fl(radius*radius) },
+ *   d2   = fl(fl(fl(dx*dx) + fl(dy*dy)) + fl(dz*dz)), dx = fl(p_j.x - p_i.x), ...
+ *   y_i  = sum_{j in N(i)} exp(-|p_i - p_j|^2 / sigma^2) x_j
+ *   count_i = |N(i)|
+ * The cell directory is rebuilt on every call (stateless).
+ *   pos: fp32 [n, 3]; x: fp32 [n, feat]; y: fp32 [n, feat] (input order);
+ *   count: int32 [n] or NULL.  reducer must be TIGA_REDUCE_SUM.
+ * Requires n < 2^31, radius > 0, sigma > 0, finite positions. */
+int tiga_mp_radius_fwd(int64_t n, int32_t feat, const float *pos, const float *x,
+                       float radius, float sigma, int reducer, float *y, int32_t *count,
+                       void *ws, size_t ws_bytes, void *stream);
+
+/* VJP of tiga_mp_radius_fwd with membership held fixed (Section 5: radius
+ * cutoff membership is discrete and not differentiated):
+ *   dx_i = sum_{j in N(i)} k_ij dy_j
+ *   dpos_i = sum_{j in N(i)} (2 k_ij / sigma^2) (p_j - p_i) (<dy_i, x_j> + <dy_j, x_i>)
+ * with k_ij = exp(-|p_i - p_j|^2 / sigma^2).  dx: fp32 [n, feat] or NULL;
+ * dpos: fp32 [n, 3] or NULL (x is only read when dpos is requested). */
+int tiga_mp_radius_bwd(int64_t n, int32_t feat, const float *pos, const float *x,
+                       float radius, float sigma, const float *dy, float *dx, float *dpos,
+                       void *ws, size_t ws_bytes, void *stream);
+
+/* Accepted neighbour lists of the radius relation, ascending per point (the
+ * relation a fused call consumes, exported for exact checking).  Two phases:
+ *   nbr_idx == NULL: writes count int32 [n] and nbr_ptr int64 [n+1] (exclusive
+ *                    prefix of count); the caller then reads nbr_ptr[n].
+ *   nbr_idx != NULL: fills nbr_idx int32 [nbr_ptr[n]] using the nbr_ptr of
+ *                    phase one (count may be NULL).
+ * Synchronizes `stream`.  Not on the fused path: for tests and inspection. */
+int tiga_radius_neighbors(int64_t n, const float *pos, float radius, int32_t *count,
+                          int64_t *nbr_ptr, int32_t *nbr_idx, void *ws, size_t ws_bytes,
+                          void *stream);
+
+/* ---------------------------------------------------- dense all-pairs relation */
+
+/* Workspace bytes for tiga_mp_dense_fwd (0 on error). */
+size_t tiga_mp_dense_workspace(int64_t n);
+
+/* Dense all-pairs relation without an edge array (Section 1), softened
+ * inverse-square message, sum reducer:
+ *   y_i = sum_{j != i} q_j (p_j - p_i) / (|p_j - p_i|^2 + eps^2)^(3/2)
+ * pos: fp32 [n, 3]; q: fp32 [n]; y: fp32 [n, 3].  reducer must be SUM.
+ * Requires n < 2^31 and eps > 0. */
+int tiga_mp_dense_fwd(int64_t n, const float *pos, const float *q, float eps, int reducer,
+                      float *y, void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------- profiling */
+
+/* Profiling aid.  Arms the calling thread so that its next fused entry point
+ * records hipEvent `start` on its stream immediately before, and `stop`
+ * immediately after, the launch of that call's dominant kernel (the one that
+ * streams the edges or pairs).  The events (hipEvent_t passed as void*) stay
+ * owned by the caller; the arming is consumed by that one call.  Passing NULL
+ * for both disarms.  Returns TIGA_OK. */
+int tiga_mp_set_kernel_events(void *start, void *stop);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TIGA_MP_H */

@@ -1,0 +1,193 @@
+"""CPU oracle for fused message passing -- test infrastructure only.
+
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product path (the HIP library and
+its Python binding) never imports, links or runs it.
+
+The numerics live in ``tiga_oracle.c`` (plain C, OpenMP over independent
+outputs, fp64 accumulation); this module is argument marshalling with numpy.
+Every sum comes back as fp64 together with the per-output sum of absolute
+term values, so a caller can check an fp32 result of any summation order
+against ``|got - ref| <= rtol * sum|terms|``.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "tiga_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "libtiga_oracle.so")
+_lock = threading.Lock()
+_lib = None
+
+CFLAGS = ["-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-std=c11",
+          "-shared", "-fPIC", "-Wall"]
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (no contraction, no fast-math)."""
+    if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        tmp = _LIB_PATH + f".tmp{os.getpid()}"
+        subprocess.check_call(["gcc", *CFLAGS, _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is None:
+            lib = C.CDLL(build())
+            i64, i32, vp, f32 = C.c_int64, C.c_int32, C.c_void_p, C.c_float
+            sig = {
+                "tiga_oracle_threads": (C.c_int, []),
+                "tiga_oracle_csr_sum_fwd": (None, [i64, vp, i32, vp, vp, vp, vp, vp, vp]),
+                "tiga_oracle_csr_max_fwd": (None, [i64, vp, i32, vp, vp, vp, vp, vp, vp]),
+                "tiga_oracle_csr_sum_bwd": (None, [i64, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+                "tiga_oracle_csr_max_bwd": (None, [i64, i64, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+                "tiga_oracle_radius_fwd": (C.c_int, [i64, i32, vp, vp, f32, f32, i64, vp, vp, vp, vp]),
+                "tiga_oracle_radius_bwd": (C.c_int, [i64, i32, vp, vp, vp, f32, f32, i64, vp, vp, vp, vp, vp]),
+                "tiga_oracle_radius_neighbors": (C.c_int, [i64, vp, f32, i64, vp, vp, vp, vp]),
+                "tiga_oracle_dense_fwd": (None, [i64, vp, vp, f32, i64, vp, vp, vp]),
+            }
+            for name, (res, args) in sig.items():
+                fn = getattr(lib, name)
+                fn.restype = res
+                fn.argtypes = args
+            _lib = lib
+    return _lib
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data
+
+
+def _c(a, dtype):
+    return None if a is None else np.ascontiguousarray(a, dtype=dtype)
+
+
+def threads() -> int:
+    return int(_load().tiga_oracle_threads())
+
+
+def _rows(rows, n):
+    if rows is None:
+        return None, n
+    rows = _c(rows, np.int64).reshape(-1)
+    return rows, rows.shape[0]
+
+
+def csr_sum_fwd(row_ptr, col, x, w=None, rows=None):
+    """Weighted-sum forward; returns (y fp64 [nrows,F], sum|terms| fp64)."""
+    row_ptr, col, x, w = _c(row_ptr, np.int64), _c(col, np.int32), _c(x, np.float32), _c(w, np.float32)
+    F = x.shape[1]
+    rows, nrows = _rows(rows, row_ptr.shape[0] - 1)
+    y = np.empty((nrows, F), np.float64)
+    ya = np.empty((nrows, F), np.float64)
+    _load().tiga_oracle_csr_sum_fwd(nrows, _p(rows), F, _p(row_ptr), _p(col), _p(x), _p(w), _p(y), _p(ya))
+    return y, ya
+
+
+def csr_max_fwd(row_ptr, col, x, w=None, rows=None):
+    """Max forward; returns (y fp32 [nrows,F], argmax int32 [nrows,F])."""
+    row_ptr, col, x, w = _c(row_ptr, np.int64), _c(col, np.int32), _c(x, np.float32), _c(w, np.float32)
+    F = x.shape[1]
+    rows, nrows = _rows(rows, row_ptr.shape[0] - 1)
+    y = np.empty((nrows, F), np.float32)
+    arg = np.empty((nrows, F), np.int32)
+    _load().tiga_oracle_csr_max_fwd(nrows, _p(rows), F, _p(row_ptr), _p(col), _p(x), _p(w), _p(y), _p(arg))
+    return y, arg
+
+
+def csr_sum_bwd(row_ptr, col, x, w, dy, num_src, want_dx=True, want_dw=True):
+    """Weighted-sum VJP; returns (dx, dx_abs, dw, dw_abs), fp64 (None where not requested)."""
+    row_ptr, col, x, w, dy = (_c(row_ptr, np.int64), _c(col, np.int32), _c(x, np.float32),
+                              _c(w, np.float32), _c(dy, np.float32))
+    F = dy.shape[1]
+    E = col.shape[0]
+    dx = np.empty((num_src, F), np.float64) if want_dx else None
+    dxa = np.empty((num_src, F), np.float64) if want_dx else None
+    dw = np.empty(E, np.float64) if want_dw else None
+    dwa = np.empty(E, np.float64) if want_dw else None
+    _load().tiga_oracle_csr_sum_bwd(row_ptr.shape[0] - 1, num_src, F, _p(row_ptr), _p(col), _p(x),
+                                    _p(w), _p(dy), _p(dx), _p(dxa), _p(dw), _p(dwa))
+    return dx, dxa, dw, dwa
+
+
+def csr_max_bwd(row_ptr, col, x, w, arg, dy, num_src, want_dx=True, want_dw=True):
+    """Max VJP routed through argmax; returns (dx, dx_abs, dw, dw_abs), fp64."""
+    row_ptr, col, x, w, arg, dy = (_c(row_ptr, np.int64), _c(col, np.int32), _c(x, np.float32),
+                                   _c(w, np.float32), _c(arg, np.int32), _c(dy, np.float32))
+    F = dy.shape[1]
+    E = col.shape[0]
+    dx = np.empty((num_src, F), np.float64) if want_dx else None
+    dxa = np.empty((num_src, F), np.float64) if want_dx else None
+    dw = np.empty(E, np.float64) if want_dw else None
+    dwa = np.empty(E, np.float64) if want_dw else None
+    _load().tiga_oracle_csr_max_bwd(row_ptr.shape[0] - 1, num_src, E, F, _p(row_ptr), _p(col), _p(x),
+                                    _p(w), _p(arg), _p(dy), _p(dx), _p(dxa), _p(dw), _p(dwa))
+    return dx, dxa, dw, dwa
+
+
+def radius_fwd(pos, x, radius, sigma, pts=None):
+    """Radius forward; returns (y fp64 [npts,F], sum|terms|, count int32 [npts])."""
+    pos, x = _c(pos, np.float32), _c(x, np.float32)
+    n, F = x.shape
+    pts, npts = _rows(pts, n)
+    y = np.empty((npts, F), np.float64)
+    ya = np.empty((npts, F), np.float64)
+    cnt = np.empty(npts, np.int32)
+    rc = _load().tiga_oracle_radius_fwd(n, F, _p(pos), _p(x), float(radius), float(sigma), npts,
+                                        _p(pts), _p(y), _p(ya), _p(cnt))
+    if rc != 0:
+        raise MemoryError("oracle radius forward: allocation failed")
+    return y, ya, cnt
+
+
+def radius_bwd(pos, x, dy, radius, sigma, pts=None):
+    """Radius VJP; returns (dx, dx_abs, dpos, dpos_abs), fp64, for the requested points."""
+    pos, x, dy = _c(pos, np.float32), _c(x, np.float32), _c(dy, np.float32)
+    n, F = x.shape
+    pts, npts = _rows(pts, n)
+    dx = np.empty((npts, F), np.float64)
+    dxa = np.empty((npts, F), np.float64)
+    dp = np.empty((npts, 3), np.float64)
+    dpa = np.empty((npts, 3), np.float64)
+    rc = _load().tiga_oracle_radius_bwd(n, F, _p(pos), _p(x), _p(dy), float(radius), float(sigma),
+                                        npts, _p(pts), _p(dx), _p(dxa), _p(dp), _p(dpa))
+    if rc != 0:
+        raise MemoryError("oracle radius backward: allocation failed")
+    return dx, dxa, dp, dpa
+
+
+def radius_neighbors(pos, radius, pts=None):
+    """Accepted neighbour lists (ascending); returns (ptr int64 [npts+1], idx int32)."""
+    pos = _c(pos, np.float32)
+    n = pos.shape[0]
+    pts, npts = _rows(pts, n)
+    cnt = np.empty(npts, np.int32)
+    lib = _load()
+    if lib.tiga_oracle_radius_neighbors(n, _p(pos), float(radius), npts, _p(pts), _p(cnt), None, None):
+        raise MemoryError("oracle radius neighbours: allocation failed")
+    ptr = np.zeros(npts + 1, np.int64)
+    np.cumsum(cnt, out=ptr[1:])
+    idx = np.empty(int(ptr[-1]), np.int32)
+    if lib.tiga_oracle_radius_neighbors(n, _p(pos), float(radius), npts, _p(pts), None, _p(ptr), _p(idx)):
+        raise MemoryError("oracle radius neighbours: allocation failed")
+    return ptr, idx
+
+
+def dense_fwd(pos, q, eps, pts=None):
+    """Dense softened inverse-square sum; returns (y fp64 [npts,3], sum|terms|)."""
+    pos, q = _c(pos, np.float32), _c(q, np.float32)
+    n = pos.shape[0]
+    pts, npts = _rows(pts, n)
+    y = np.empty((npts, 3), np.float64)
+    ya = np.empty((npts, 3), np.float64)
+    _load().tiga_oracle_dense_fwd(n, _p(pos), _p(q), float(eps), npts, _p(pts), _p(y), _p(ya))
+    return y, ya

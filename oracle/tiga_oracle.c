@@ -1,0 +1,535 @@
+/*
+ * CPU oracle for fused message passing -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Only tests, the smoke check and the benchmark's CPU-baseline leg may load
+ * this library.  It shares no code, header, table or constant with the HIP
+ * library; the two only consume the same seeded inputs.
+ *
+ * Everything here is the plain definition of what fused message passing
+ * computes (Tiga, "Compiling Graph Message Passing at Scale"):
+ *
+ *   m_e = f(x_{s(e)}, z_{d(e)}, a_e),   y_i = finalize( combine_{d(e)=i} m_e )
+ *   (Section 3.1, the message/update equation)
+ *
+ * with the relation given as destination-major CSR (Section 3.1 and 4.3:
+ * row i owns edge positions [row_ptr[i], row_ptr[i+1]); the edge position
+ * indexes edge fields and col[e] is the source id), as a radius predicate over
+ * positions (Section 4.9, generated relations), or as all ordered pairs j != i.
+ *
+ * Floating point: inputs are fp32; every sum is accumulated in fp64 (fp32 x
+ * fp32 products are exact in fp64) and returned in fp64, together with the
+ * sum of absolute values of its terms, so a caller can bound the error of any
+ * fp32 summation order.  The max reducer and the radius membership test are
+ * decisions, so they are evaluated in fp32 exactly as the message is defined
+ * (one fp32 multiply; an fp32 squared distance without contraction).  Build
+ * with -ffp-contract=off.
+ *
+ * Parity pins for every function are in the CPU test suite (worked example of
+ * Section 3.1, library routines, brute force, invariants, finite differences).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+int tiga_oracle_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* ------------------------------------------------------------------------ */
+/* Stored CSR relation, weighted-sum message                                 */
+/* ------------------------------------------------------------------------ */
+
+/* Sum reducer (Section 3.1; identity 0, so an empty row finalizes to 0):
+ *   y[i,f] = sum_{e in row i} w[e] * x[col[e], f]     (w == NULL means w = 1)
+ * Rows are taken from `rows` (nrows entries) or, if rows == NULL, all rows
+ * 0..nrows-1.  Output k belongs to row rows[k]. */
+void tiga_oracle_csr_sum_fwd(int64_t nrows, const int64_t *rows, int32_t F,
+                             const int64_t *row_ptr, const int32_t *col,
+                             const float *x, const float *w,
+                             double *y, double *yabs) {
+    int64_t k;
+#pragma omp parallel for schedule(dynamic, 64)
+    for (k = 0; k < nrows; ++k) {
+        int64_t i = rows ? rows[k] : k;
+        for (int32_t f = 0; f < F; ++f) {
+            double acc = 0.0, mag = 0.0;
+            for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+                double term = (w ? (double)w[e] : 1.0) * (double)x[(int64_t)col[e] * F + f];
+                acc += term;
+                mag += fabs(term);
+            }
+            y[k * F + f] = acc;
+            if (yabs) yabs[k * F + f] = mag;
+        }
+    }
+}
+
+/* Max reducer.  The paper leaves max undefined beyond "an empty row starts
+ * from the identity and finalization fixes the empty-row convention"
+ * (Section 3.1).  Reading: identity -inf; the message is the fp32 product
+ * w[e]*x[col[e],f]; edges are visited in ascending CSR position and a later
+ * edge replaces the best only if strictly greater, so ties keep the lowest
+ * edge position (+0 and -0 compare equal); an empty row finalizes to value 0
+ * and argmax -1. */
+void tiga_oracle_csr_max_fwd(int64_t nrows, const int64_t *rows, int32_t F,
+                             const int64_t *row_ptr, const int32_t *col,
+                             const float *x, const float *w,
+                             float *y, int32_t *arg) {
+    int64_t k;
+#pragma omp parallel for schedule(dynamic, 64)
+    for (k = 0; k < nrows; ++k) {
+        int64_t i = rows ? rows[k] : k;
+        for (int32_t f = 0; f < F; ++f) {
+            int have = 0;
+            float best = 0.0f;
+            int64_t best_e = -1;
+            for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+                float xv = x[(int64_t)col[e] * F + f];
+                float v = w ? w[e] * xv : xv;
+                if (!have || v > best) {
+                    best = v;
+                    best_e = e;
+                    have = 1;
+                }
+            }
+            y[k * F + f] = have ? best : 0.0f;
+            arg[k * F + f] = (int32_t)best_e;
+        }
+    }
+}
+
+/* Vector-Jacobian product of the weighted sum (Section 5, adjoint equation):
+ *   dx[j,f] = sum_{e : col[e] = j} w[e] * dy[d(e), f]
+ *   dw[e]   = sum_f x[col[e], f] * dy[d(e), f]
+ * (the paper writes dw for one feature; a per-edge scalar weight broadcast
+ * over F features collects the sum over f).  Repeated sources accumulate,
+ * edges of empty rows do not exist.  dx is over all num_src sources, dw over
+ * all edges; either may be NULL.  A plain serial walk over rows and edges. */
+void tiga_oracle_csr_sum_bwd(int64_t num_dst, int64_t num_src, int32_t F,
+                             const int64_t *row_ptr, const int32_t *col,
+                             const float *x, const float *w, const float *dy,
+                             double *dx, double *dxabs, double *dw, double *dwabs) {
+    if (dx) {
+        memset(dx, 0, sizeof(double) * (size_t)num_src * F);
+        if (dxabs) memset(dxabs, 0, sizeof(double) * (size_t)num_src * F);
+        for (int64_t i = 0; i < num_dst; ++i)
+            for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e)
+                for (int32_t f = 0; f < F; ++f) {
+                    double term = (w ? (double)w[e] : 1.0) * (double)dy[i * F + f];
+                    dx[(int64_t)col[e] * F + f] += term;
+                    if (dxabs) dxabs[(int64_t)col[e] * F + f] += fabs(term);
+                }
+    }
+    if (dw) {
+        int64_t i;
+#pragma omp parallel for schedule(dynamic, 64)
+        for (i = 0; i < num_dst; ++i)
+            for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+                double acc = 0.0, mag = 0.0;
+                for (int32_t f = 0; f < F; ++f) {
+                    double term = (double)x[(int64_t)col[e] * F + f] * (double)dy[i * F + f];
+                    acc += term;
+                    mag += fabs(term);
+                }
+                dw[e] = acc;
+                if (dwabs) dwabs[e] = mag;
+            }
+    }
+}
+
+/* Vector-Jacobian product of the max reducer: y[i,f] depends only on the
+ * selected edge e* = arg[i,f] (the derivative of max with respect to the
+ * selected message is 1 and 0 for the others), so
+ *   dx[col[e*], f] += w[e*] * dy[i,f],   dw[e*] += x[col[e*], f] * dy[i,f]
+ * for every (i,f) with e* >= 0.  Empty rows contribute nothing. */
+void tiga_oracle_csr_max_bwd(int64_t num_dst, int64_t num_src, int64_t num_edges, int32_t F,
+                             const int64_t *row_ptr, const int32_t *col,
+                             const float *x, const float *w, const int32_t *arg,
+                             const float *dy,
+                             double *dx, double *dxabs, double *dw, double *dwabs) {
+    (void)row_ptr;
+    if (dx) {
+        memset(dx, 0, sizeof(double) * (size_t)num_src * F);
+        if (dxabs) memset(dxabs, 0, sizeof(double) * (size_t)num_src * F);
+    }
+    if (dw) {
+        memset(dw, 0, sizeof(double) * (size_t)num_edges);
+        if (dwabs) memset(dwabs, 0, sizeof(double) * (size_t)num_edges);
+    }
+    for (int64_t i = 0; i < num_dst; ++i)
+        for (int32_t f = 0; f < F; ++f) {
+            int64_t e = arg[i * F + f];
+            if (e < 0) continue;
+            int64_t j = col[e];
+            double g = (double)dy[i * F + f];
+            if (dx) {
+                double term = (w ? (double)w[e] : 1.0) * g;
+                dx[j * F + f] += term;
+                if (dxabs) dxabs[j * F + f] += fabs(term);
+            }
+            if (dw) {
+                double term = (double)x[j * F + f] * g;
+                dw[e] += term;
+                if (dwabs) dwabs[e] += fabs(term);
+            }
+        }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Generated radius relation (Section 4.9)                                   */
+/* ------------------------------------------------------------------------ */
+
+/* Membership: j != i and the fp32 squared distance, formed from direct
+ * coordinate differences (the evaluation protocol uses direct differences,
+ * not the |a|^2+|b|^2-2ab identity), is strictly below fp32(r*r).  Each
+ * operation is one fp32 rounding; nothing is contracted. */
+static int within(const float *pi, const float *pj, float r2) {
+    float dx = pj[0] - pi[0];
+    float dy = pj[1] - pi[1];
+    float dz = pj[2] - pi[2];
+    float sx = dx * dx;
+    float sy = dy * dy;
+    float sz = dz * dz;
+    float d2 = (sx + sy) + sz;
+    return d2 < r2;
+}
+
+/* A uniform cell directory: per axis, the box [lo, hi] is cut into cells no
+ * smaller than r (with a 1e-3 relative margin), so every accepted neighbour
+ * of a point lies in the 27 cells around the point's own cell.  Cells only
+ * restrict the candidates; the predicate alone decides membership. */
+typedef struct {
+    int64_t n;
+    double lo[3], h[3];
+    int64_t dim[3];
+    int64_t *start; /* ncell + 1 */
+    int64_t *items; /* point ids, grouped by cell, ascending within a cell */
+} grid_t;
+
+static int64_t cell_coord(const grid_t *g, int a, float p) {
+    int64_t c = (int64_t)floor(((double)p - g->lo[a]) / g->h[a]);
+    if (c < 0) c = 0;
+    if (c >= g->dim[a]) c = g->dim[a] - 1;
+    return c;
+}
+
+static int grid_build(grid_t *g, int64_t n, const float *pos, float radius) {
+    g->n = n;
+    for (int a = 0; a < 3; ++a) {
+        double lo = INFINITY, hi = -INFINITY;
+        for (int64_t i = 0; i < n; ++i) {
+            double v = pos[i * 3 + a];
+            if (v < lo) lo = v;
+            if (v > hi) hi = v;
+        }
+        if (n == 0) lo = hi = 0.0;
+        double ext = hi - lo;
+        double hmin = (double)radius * 1.001;
+        int64_t d = (hmin > 0.0) ? (int64_t)floor(ext / hmin) : 1;
+        if (d < 1) d = 1;
+        if (d > 1024) d = 1024;
+        g->lo[a] = lo;
+        g->h[a] = (ext > 0.0) ? ext / (double)d : 1.0;
+        g->dim[a] = d;
+    }
+    int64_t ncell = g->dim[0] * g->dim[1] * g->dim[2];
+    g->start = (int64_t *)calloc((size_t)ncell + 1, sizeof(int64_t));
+    g->items = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n ? n : 1));
+    int64_t *cell = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n ? n : 1));
+    if (!g->start || !g->items || !cell) return -1;
+    for (int64_t i = 0; i < n; ++i) {
+        const float *p = pos + i * 3;
+        cell[i] = (cell_coord(g, 2, p[2]) * g->dim[1] + cell_coord(g, 1, p[1])) * g->dim[0] +
+                  cell_coord(g, 0, p[0]);
+        g->start[cell[i] + 1]++;
+    }
+    for (int64_t c = 0; c < ncell; ++c) g->start[c + 1] += g->start[c];
+    int64_t *fill = (int64_t *)malloc(sizeof(int64_t) * (size_t)ncell);
+    if (!fill) return -1;
+    memcpy(fill, g->start, sizeof(int64_t) * (size_t)ncell);
+    for (int64_t i = 0; i < n; ++i) g->items[fill[cell[i]]++] = i;
+    free(fill);
+    free(cell);
+    return 0;
+}
+
+static void grid_free(grid_t *g) {
+    free(g->start);
+    free(g->items);
+}
+
+/* Visit the accepted neighbours of point i in ascending index order.  With
+ * use_grid == 0 this is the plain O(N) scan over all j. */
+typedef void (*visit_fn)(void *ctx, int64_t i, int64_t j);
+
+static int cmp_i64(const void *a, const void *b) {
+    int64_t x = *(const int64_t *)a, y = *(const int64_t *)b;
+    return (x > y) - (x < y);
+}
+
+static int64_t neighbours(const grid_t *g, int use_grid, int64_t n, const float *pos, float r2,
+                          int64_t i, int64_t *buf, int64_t cap) {
+    int64_t cnt = 0;
+    const float *pi = pos + i * 3;
+    if (!use_grid) {
+        for (int64_t j = 0; j < n; ++j)
+            if (j != i && within(pi, pos + j * 3, r2)) {
+                if (cnt < cap) buf[cnt] = j;
+                cnt++;
+            }
+        return cnt;
+    }
+    int64_t c[3];
+    for (int a = 0; a < 3; ++a) c[a] = cell_coord(g, a, pi[a]);
+    for (int64_t cz = c[2] - 1; cz <= c[2] + 1; ++cz) {
+        if (cz < 0 || cz >= g->dim[2]) continue;
+        for (int64_t cy = c[1] - 1; cy <= c[1] + 1; ++cy) {
+            if (cy < 0 || cy >= g->dim[1]) continue;
+            for (int64_t cx = c[0] - 1; cx <= c[0] + 1; ++cx) {
+                if (cx < 0 || cx >= g->dim[0]) continue;
+                int64_t cell = (cz * g->dim[1] + cy) * g->dim[0] + cx;
+                for (int64_t t = g->start[cell]; t < g->start[cell + 1]; ++t) {
+                    int64_t j = g->items[t];
+                    if (j != i && within(pi, pos + j * 3, r2)) {
+                        if (cnt < cap) buf[cnt] = j;
+                        cnt++;
+                    }
+                }
+            }
+        }
+    }
+    if (cnt <= cap) qsort(buf, (size_t)cnt, sizeof(int64_t), cmp_i64);
+    return cnt;
+}
+
+/* Shared driver: for each requested point, gather its sorted neighbour list
+ * and hand it to `body`. */
+typedef void (*point_body)(void *ctx, int64_t k, int64_t i, const int64_t *nb, int64_t cnt);
+
+static int for_each_point(int64_t n, const float *pos, float radius, int64_t npts,
+                          const int64_t *pts, point_body body, void *ctx) {
+    float r2 = radius * radius;
+    grid_t g;
+    memset(&g, 0, sizeof g);
+    int use_grid = n > 4096;
+    if (use_grid && grid_build(&g, n, pos, radius) != 0) return -1;
+    int err = 0;
+    int64_t k;
+#pragma omp parallel
+    {
+        int64_t cap = 256;
+        int64_t *buf = (int64_t *)malloc(sizeof(int64_t) * (size_t)cap);
+#pragma omp for schedule(dynamic, 64)
+        for (k = 0; k < npts; ++k) {
+            int64_t i = pts ? pts[k] : k;
+            int64_t cnt = neighbours(&g, use_grid, n, pos, r2, i, buf, cap);
+            if (cnt > cap) {
+                free(buf);
+                cap = cnt;
+                buf = (int64_t *)malloc(sizeof(int64_t) * (size_t)cap);
+                if (!buf) {
+#pragma omp atomic write
+                    err = 1;
+                    cap = 0;
+                    continue;
+                }
+                cnt = neighbours(&g, use_grid, n, pos, r2, i, buf, cap);
+            }
+            body(ctx, k, i, buf, cnt);
+        }
+        free(buf);
+    }
+    if (use_grid) grid_free(&g);
+    return err ? -1 : 0;
+}
+
+/* Gaussian weight of an accepted pair, from the fp64 displacement. */
+static double kernel_weight(const float *pi, const float *pj, double inv_s2, double d[3]) {
+    d[0] = (double)pj[0] - (double)pi[0];
+    d[1] = (double)pj[1] - (double)pi[1];
+    d[2] = (double)pj[2] - (double)pi[2];
+    return exp(-(d[0] * d[0] + d[1] * d[1] + d[2] * d[2]) * inv_s2);
+}
+
+typedef struct {
+    int32_t F;
+    const float *pos, *x, *dy;
+    double inv_s2;
+    double *y, *yabs, *dx, *dxabs, *dp, *dpabs;
+    int32_t *count;
+} radius_ctx;
+
+/* Forward: y_i = sum_{j in N(i)} exp(-|p_i - p_j|^2 / sigma^2) x_j, with
+ * N(i) = { j != i : |p_j - p_i|^2 < r^2 }; count_i = |N(i)|. */
+static void radius_fwd_body(void *vctx, int64_t k, int64_t i, const int64_t *nb, int64_t cnt) {
+    radius_ctx *c = (radius_ctx *)vctx;
+    const int32_t F = c->F;
+    double *y = c->y + k * F;
+    double *ya = c->yabs ? c->yabs + k * F : NULL;
+    for (int32_t f = 0; f < F; ++f) {
+        y[f] = 0.0;
+        if (ya) ya[f] = 0.0;
+    }
+    const float *pi = c->pos + i * 3;
+    for (int64_t t = 0; t < cnt; ++t) {
+        int64_t j = nb[t];
+        double d[3];
+        double kw = kernel_weight(pi, c->pos + j * 3, c->inv_s2, d);
+        for (int32_t f = 0; f < F; ++f) {
+            double term = kw * (double)c->x[j * F + f];
+            y[f] += term;
+            if (ya) ya[f] += fabs(term);
+        }
+    }
+    if (c->count) c->count[k] = (int32_t)cnt;
+}
+
+int tiga_oracle_radius_fwd(int64_t n, int32_t F, const float *pos, const float *x,
+                           float radius, float sigma, int64_t npts, const int64_t *pts,
+                           double *y, double *yabs, int32_t *count) {
+    radius_ctx c;
+    memset(&c, 0, sizeof c);
+    c.F = F;
+    c.pos = pos;
+    c.x = x;
+    c.inv_s2 = 1.0 / ((double)sigma * (double)sigma);
+    c.y = y;
+    c.yabs = yabs;
+    c.count = count;
+    return for_each_point(n, pos, radius, npts, pts, radius_fwd_body, &c);
+}
+
+/* Backward with membership held fixed (Section 5: radius cutoff membership is
+ * discrete and not differentiated).  With k_ij = exp(-|p_i-p_j|^2/sigma^2)
+ * and the loss L = sum_i <dy_i, y_i>:
+ *   dx_j = sum_{i : j in N(i)} k_ij dy_i = sum_{i in N(j)} k_ij dy_i
+ *          (the relation and the weight are symmetric in i, j),
+ *   dp_i = sum_{j in N(i)} (2 k_ij / sigma^2) (p_j - p_i) (<dy_i, x_j> + <dy_j, x_i>)
+ *          (p_i enters k_ij as destination and k_ji as source; dk/dp_i =
+ *          (2k/sigma^2)(p_j - p_i) in both). */
+static void radius_bwd_body(void *vctx, int64_t k, int64_t i, const int64_t *nb, int64_t cnt) {
+    radius_ctx *c = (radius_ctx *)vctx;
+    const int32_t F = c->F;
+    const float *pi = c->pos + i * 3;
+    if (c->dx) {
+        for (int32_t f = 0; f < F; ++f) {
+            c->dx[k * F + f] = 0.0;
+            if (c->dxabs) c->dxabs[k * F + f] = 0.0;
+        }
+    }
+    double gp[3] = {0, 0, 0}, ga[3] = {0, 0, 0};
+    for (int64_t t = 0; t < cnt; ++t) {
+        int64_t j = nb[t];
+        double d[3];
+        double kw = kernel_weight(pi, c->pos + j * 3, c->inv_s2, d);
+        if (c->dx) {
+            for (int32_t f = 0; f < F; ++f) {
+                double term = kw * (double)c->dy[j * F + f];
+                c->dx[k * F + f] += term;
+                if (c->dxabs) c->dxabs[k * F + f] += fabs(term);
+            }
+        }
+        if (c->dp) {
+            double s = 0.0, sa = 0.0;
+            for (int32_t f = 0; f < F; ++f) {
+                double a = (double)c->dy[i * F + f] * (double)c->x[j * F + f];
+                double b = (double)c->dy[j * F + f] * (double)c->x[i * F + f];
+                s += a + b;
+                sa += fabs(a) + fabs(b);
+            }
+            double coef = 2.0 * kw * c->inv_s2;
+            for (int a = 0; a < 3; ++a) {
+                gp[a] += coef * d[a] * s;
+                ga[a] += fabs(coef * d[a]) * sa;
+            }
+        }
+    }
+    if (c->dp)
+        for (int a = 0; a < 3; ++a) {
+            c->dp[k * 3 + a] = gp[a];
+            if (c->dpabs) c->dpabs[k * 3 + a] = ga[a];
+        }
+}
+
+int tiga_oracle_radius_bwd(int64_t n, int32_t F, const float *pos, const float *x,
+                           const float *dy, float radius, float sigma, int64_t npts,
+                           const int64_t *pts, double *dx, double *dxabs, double *dp,
+                           double *dpabs) {
+    radius_ctx c;
+    memset(&c, 0, sizeof c);
+    c.F = F;
+    c.pos = pos;
+    c.x = x;
+    c.dy = dy;
+    c.inv_s2 = 1.0 / ((double)sigma * (double)sigma);
+    c.dx = dx;
+    c.dxabs = dxabs;
+    c.dp = dp;
+    c.dpabs = dpabs;
+    return for_each_point(n, pos, radius, npts, pts, radius_bwd_body, &c);
+}
+
+typedef struct {
+    int64_t *ptr;
+    int32_t *idx;
+    int32_t *count;
+} nbr_ctx;
+
+static void nbr_body(void *vctx, int64_t k, int64_t i, const int64_t *nb, int64_t cnt) {
+    nbr_ctx *c = (nbr_ctx *)vctx;
+    (void)i;
+    if (c->count) c->count[k] = (int32_t)cnt;
+    if (c->idx)
+        for (int64_t t = 0; t < cnt; ++t) c->idx[c->ptr[k] + t] = (int32_t)nb[t];
+}
+
+/* Accepted neighbour lists, ascending per point.  Call once with idx == NULL
+ * to obtain counts, then with ptr (exclusive prefix of counts) and idx. */
+int tiga_oracle_radius_neighbors(int64_t n, const float *pos, float radius, int64_t npts,
+                                 const int64_t *pts, int32_t *count, const int64_t *ptr,
+                                 int32_t *idx) {
+    nbr_ctx c = {(int64_t *)ptr, idx, count};
+    return for_each_point(n, pos, radius, npts, pts, nbr_body, &c);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Dense all-pairs relation (no edge array; Section 1: a dense relation may  */
+/* need no edge array)                                                       */
+/* ------------------------------------------------------------------------ */
+
+/* Softened inverse-square message summed over all j != i:
+ *   y_i = sum_{j != i} q_j (p_j - p_i) / (|p_j - p_i|^2 + eps^2)^(3/2). */
+void tiga_oracle_dense_fwd(int64_t n, const float *pos, const float *q, float eps,
+                           int64_t npts, const int64_t *pts, double *y, double *yabs) {
+    double e2 = (double)eps * (double)eps;
+    int64_t k;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (k = 0; k < npts; ++k) {
+        int64_t i = pts ? pts[k] : k;
+        double acc[3] = {0, 0, 0}, mag[3] = {0, 0, 0};
+        for (int64_t j = 0; j < n; ++j) {
+            if (j == i) continue;
+            double d[3];
+            for (int a = 0; a < 3; ++a) d[a] = (double)pos[j * 3 + a] - (double)pos[i * 3 + a];
+            double s = d[0] * d[0] + d[1] * d[1] + d[2] * d[2] + e2;
+            double coef = (double)q[j] / (s * sqrt(s));
+            for (int a = 0; a < 3; ++a) {
+                acc[a] += coef * d[a];
+                mag[a] += fabs(coef * d[a]);
+            }
+        }
+        for (int a = 0; a < 3; ++a) {
+            y[k * 3 + a] = acc[a];
+            if (yabs) yabs[k * 3 + a] = mag[a];
+        }
+    }
+}

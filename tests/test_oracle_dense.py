@@ -1,0 +1,82 @@
+"""Pins for the dense all-pairs oracle (softened inverse-square message).
+
+y_i = sum_{j != i} q_j (p_j - p_i) / (|p_j - p_i|^2 + eps^2)^(3/2) is the field
+of point charges (attractive sign convention).  The pins are physical laws the
+definition must obey: Gauss's law through a sphere of zero-charge probes (sign
+and inverse-square exponent), the monopole far field, Newton's third law,
+exact symmetry cancellation, and the two-body softening.
+"""
+import numpy as np
+
+import oracle
+from paper_2609_24802_amd import synth
+
+
+def _fibonacci_sphere(m, radius):
+    k = np.arange(m) + 0.5
+    z = 1 - 2 * k / m
+    phi = np.pi * (1 + 5 ** 0.5) * k
+    rho = np.sqrt(1 - z * z)
+    return radius * np.stack([rho * np.cos(phi), rho * np.sin(phi), z], 1)
+
+
+def test_gauss_law_flux():
+    rng = np.random.default_rng(4)
+    nq, m, R = 40, 6000, 1.0
+    charges = rng.uniform(-0.35, 0.35, (nq, 3))
+    q = rng.uniform(0.5, 1.5, nq)
+    probes = _fibonacci_sphere(m, R)
+    pos = np.concatenate([charges, probes]).astype(np.float32)
+    qq = np.concatenate([q, np.zeros(m)]).astype(np.float32)
+    y, _ = oracle.dense_fwd(pos, qq, np.float32(1e-4))
+    normals = probes / R
+    flux = float((y[nq:] * normals).sum(1).sum() * (4 * np.pi * R * R / m))
+    # the field points toward positive charges: outward flux is -4 pi Q
+    np.testing.assert_allclose(flux, -4 * np.pi * float(qq[:nq].astype(np.float64).sum()), rtol=2e-3)
+
+
+def test_monopole_far_field():
+    rng = np.random.default_rng(5)
+    cluster = rng.normal(0, 0.01, (50, 3))
+    q = rng.uniform(0.5, 1.5, 50)
+    probe = np.array([[60.0, -30.0, 45.0]])
+    pos = np.concatenate([cluster, probe]).astype(np.float32)
+    qq = np.concatenate([q, [0.0]]).astype(np.float32)
+    y, _ = oracle.dense_fwd(pos, qq, np.float32(1e-2))
+    centre = (qq[:50, None].astype(np.float64) * pos[:50]).sum(0) / qq[:50].astype(np.float64).sum()
+    d = centre - pos[50].astype(np.float64)
+    expect = qq[:50].astype(np.float64).sum() * d / np.linalg.norm(d) ** 3
+    np.testing.assert_allclose(y[50], expect, rtol=1e-6)
+
+
+def test_third_law_and_symmetry():
+    g = synth.config4(n=3000)
+    y, ya = oracle.dense_fwd(g["pos"], g["q"], g["eps"])
+    q = g["q"].astype(np.float64)
+    total = (q[:, None] * y).sum(0)
+    assert np.all(np.abs(total) <= 1e-12 * (q[:, None] * ya).sum(0))
+    # eight equal charges on cube vertices: zero field at the centre probe
+    cube = np.array([[a, b, c] for a in (-1, 1) for b in (-1, 1) for c in (-1, 1)], np.float32)
+    pos = np.concatenate([cube, [[0, 0, 0]]]).astype(np.float32)
+    qq = np.array([1.0] * 8 + [2.0], np.float32)
+    y2, _ = oracle.dense_fwd(pos, qq, np.float32(1e-2))
+    assert np.all(np.abs(y2[8]) < 1e-15)
+
+
+def test_two_body_softening():
+    # separation equal to eps: |d|^2 + eps^2 = 2 eps^2, so |y_0| = q_1 eps / (2 eps^2)^(3/2)
+    eps = np.float32(2.0 ** -7)
+    pos = np.array([[0, 0, 0], [float(eps), 0, 0]], np.float32)
+    q = np.array([1.0, 3.0], np.float32)
+    y, _ = oracle.dense_fwd(pos, q, eps)
+    e = float(eps)
+    np.testing.assert_allclose(y[0], [3.0 * e / (2 * e * e) ** 1.5, 0, 0], rtol=1e-14)
+    np.testing.assert_allclose(y[1], [-1.0 * e / (2 * e * e) ** 1.5, 0, 0], rtol=1e-14)
+
+
+def test_subset_rows():
+    g = synth.config4(n=2000)
+    y, ya = oracle.dense_fwd(g["pos"], g["q"], g["eps"])
+    pts = np.array([1999, 0, 1000])
+    ys, yas = oracle.dense_fwd(g["pos"], g["q"], g["eps"], pts=pts)
+    assert np.array_equal(ys, y[pts]) and np.array_equal(yas, ya[pts])
