@@ -1,0 +1,264 @@
+"""Benchmark of fused message passing on one MI355X.
+
+Headline workload: the power-law CSR graph with 50M nodes and 1e9 edges
+(in-degrees Zipf(2.1) capped at 1e6, uniform sources, x fp32 [N, 16], edge
+weights fp32), weighted-sum forward.  One step = one call of
+tiga_mp_csr_fwd: the degree plan followed by the fused gather-reduce and the
+split-row merge, inputs resident in HBM.
+
+Printed: one JSON line with GEdges/s, the roofline of the dominant kernel
+(the gather-reduce, timed with HIP events on its own stream), the CPU oracle
+timed on a bounded sample of the same graph, and per-path figures for the
+other relations (power-law CSR sum/max forward and backward, radius forward
+and backward including the cell build, dense all-pairs).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+# FP32 vector issue: 256 CUs x 4 SIMDs x 16 lanes x 2 flops (FMA) x 2.4 GHz;
+# packed FP32 instructions are disabled in this build.
+VALU_PEAK_TFLOPS = 78.6
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--scale", type=float, default=1.0, help="shrink the headline graph (testing only)")
+    p.add_argument("--no-paths", action="store_true", help="skip the per-path figures")
+    p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--cpu-seconds", type=float, default=10.0)
+    p.add_argument("--check-rows", type=int, default=400)
+    return p.parse_args()
+
+
+class Timer:
+    """HIP events around the dominant kernel of each call, plus whole-step events."""
+
+    def __init__(self, torch, tb, steps):
+        self.torch, self.tb = torch, tb
+        self.k = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        s = torch.cuda.current_stream()
+        for a, b in self.k:  # materialize the underlying hipEvents
+            a.record(s)
+            b.record(s)
+        torch.cuda.synchronize()
+
+    def arm(self, i):
+        a, b = self.k[i]
+        self.tb.tiga_mp_set_kernel_events(a, b)
+
+    def kernel_ms(self):
+        return [a.elapsed_time(b) for a, b in self.k]
+
+
+def time_steps(torch, tb, fn, steps, warmup):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    tm = Timer(torch, tb, steps)
+    s0 = torch.cuda.Event(enable_timing=True)
+    s1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    s0.record()
+    for i in range(steps):
+        tm.arm(i)
+        fn()
+    s1.record()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3
+    return dict(step_ms=s0.elapsed_time(s1) / steps, wall_ms=wall / steps, kernel_ms=tm.kernel_ms())
+
+
+def headline(args, torch, tb, synth, oracle):
+    t = time.time()
+    g = synth.config5(scale=args.scale)
+    rp, col, x, w, n = g["row_ptr"], g["col"], g["x"], g["w"], g["num_dst"]
+    E, F = int(rp[-1]), x.shape[1]
+    log(f"generated {n} nodes / {E} edges in {time.time() - t:.1f} s")
+    dev = lambda a: torch.from_numpy(a).cuda()
+    rel = tb.Csr(dev(rp), dev(col), n)
+    xd, wd = dev(x), dev(w)
+    y = torch.empty(n, F, dtype=torch.float32, device="cuda")
+    ws = torch.empty(tb.load().tiga_mp_csr_fwd_workspace(rel.ref, F, tb.REDUCE_SUM), dtype=torch.uint8,
+                     device="cuda")
+    torch.cuda.synchronize()
+    log("inputs resident on the device")
+
+    fn = lambda: tb.tiga_mp_csr_fwd(rel, xd, wd, y=y, ws=ws)
+    r = time_steps(torch, tb, fn, args.steps, args.warmup)
+    log(f"step {r['step_ms']:.3f} ms, gather-reduce {np.mean(r['kernel_ms']):.3f} ms")
+
+    # sampled parity of what was timed
+    deg = np.diff(rp)
+    rows = np.unique(np.concatenate([np.argsort(-deg, kind="stable")[:4],
+                                     np.random.default_rng(1).integers(0, n, args.check_rows)]))
+    yh = y[torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
+    ref, mag = oracle.csr_sum_fwd(rp, col, x, w, rows=rows)
+    parity_ok = bool(np.all(np.abs(yh - ref) <= 1e-5 * mag))
+    log(f"sampled parity ({rows.size} rows): {'ok' if parity_ok else 'FAILED'}")
+
+    kernel_ms = float(np.mean(r["kernel_ms"]))
+    bytes_alg = E * (4 + 4 + 4 * F) + n * (8 + 4 * F)
+    achieved = bytes_alg / (kernel_ms * 1e-3) / 1e9
+    out = dict(E=E, n=n, F=F, step_ms=r["step_ms"], kernel_ms=kernel_ms, bytes_alg=bytes_alg,
+               achieved=achieved, parity_ok=parity_ok, kernel_ms_all=r["kernel_ms"])
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(args, oracle, rp, col, x, w)
+    del rel, xd, wd, y, ws
+    torch.cuda.empty_cache()
+    return out, cpu
+
+
+def cpu_baseline(args, oracle, rp, col, x, w):
+    """The oracle (untuned, fp64) on the first rows of the same graph."""
+    n = rp.size - 1
+    # calibrate on ~2M edges, then size the sample for about cpu_seconds
+    k = int(np.searchsorted(rp, 2_000_000))
+    k = max(1, min(k, n))
+    t = time.perf_counter()
+    oracle.csr_sum_fwd(rp, col, x, w, rows=np.arange(k))
+    rate = (rp[k] - rp[0]) / max(time.perf_counter() - t, 1e-6)
+    target = int(rate * args.cpu_seconds)
+    k = int(np.searchsorted(rp, target))
+    k = max(1, min(k, n))
+    rows = np.arange(k)
+    t = time.perf_counter()
+    oracle.csr_sum_fwd(rp, col, x, w, rows=rows)
+    dt = time.perf_counter() - t
+    edges = int(rp[k] - rp[0])
+    log(f"cpu oracle: {edges} edges in {dt:.2f} s on {oracle.threads()} threads")
+    return dict(value=edges / dt / 1e9, unit="GEdges/s", cores=oracle.threads(), kind="oracle",
+                sample=f"weighted-sum forward of rows [0, {k}) of the 1e9-edge graph ({edges} edges), "
+                       f"fp64 accumulation, {dt:.1f} s")
+
+
+def paths(args, torch, tb, synth):
+    """Per-path figures on the other workloads (each timed with HIP events)."""
+    res = {}
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    steps, warm = max(5, args.steps // 2), 2
+
+    g = synth.config2()
+    rp, col, n = g["row_ptr"], g["col"], g["num_dst"]
+    E = int(rp[-1])
+    rel = tb.Csr(dev(rp), dev(col), n)
+    xd, wd, dyd = dev(g["x"]), dev(g["w"]), dev(g["dy"])
+    F = xd.shape[1]
+    rev = tb.tiga_csr_transpose(rel)
+    _, am = tb.tiga_mp_csr_fwd(rel, xd, wd, reducer=tb.REDUCE_MAX)
+    cases = {
+        "csr_powerlaw_1m_16m_f64_sum_fwd": lambda: tb.tiga_mp_csr_fwd(rel, xd, wd),
+        "csr_powerlaw_1m_16m_f64_max_fwd": lambda: tb.tiga_mp_csr_fwd(rel, xd, wd, reducer=tb.REDUCE_MAX),
+        "csr_powerlaw_1m_16m_f64_sum_bwd_atomic": lambda: tb.tiga_mp_csr_bwd(rel, dyd, xd, wd),
+        "csr_powerlaw_1m_16m_f64_sum_bwd_gather": lambda: tb.tiga_mp_csr_bwd(rel, dyd, xd, wd, rev=rev),
+        "csr_powerlaw_1m_16m_f64_max_bwd_atomic": lambda: tb.tiga_mp_csr_bwd(rel, dyd, xd, wd,
+                                                                             reducer=tb.REDUCE_MAX, argmax=am),
+        "csr_powerlaw_1m_16m_f64_max_bwd_gather": lambda: tb.tiga_mp_csr_bwd(rel, dyd, xd, wd,
+                                                                             reducer=tb.REDUCE_MAX, argmax=am,
+                                                                             rev=rev),
+    }
+    fwd_bytes = E * (8 + 4 * F) + n * (8 + 4 * F)
+    for name, fn in cases.items():
+        r = time_steps(torch, tb, fn, steps, warm)
+        d = dict(ms=r["step_ms"], gedges_per_s=E / r["step_ms"] / 1e6)
+        if name.endswith("sum_fwd"):
+            k = float(np.mean(r["kernel_ms"]))
+            d.update(kernel_ms=k, alg_gbs=fwd_bytes / k / 1e6, frac_hbm=fwd_bytes / k / 1e6 / HBM_PEAK_GBS)
+        res[name] = d
+        log(f"{name}: {d['ms']:.3f} ms")
+    del rel, xd, wd, dyd, rev, am
+    torch.cuda.empty_cache()
+
+    g = synth.config3()
+    pd, xd, dyd = dev(g["pos"]), dev(g["x"]), dev(g["dy"])
+    r, s = g["radius"], g["sigma"]
+    _, cnt = tb.tiga_mp_radius_fwd(pd, xd, r, s)
+    pairs = int(cnt.long().sum().item())
+    for name, fn in {"radius_1m_f32_fwd_with_build": lambda: tb.tiga_mp_radius_fwd(pd, xd, r, s, want_count=False),
+                     "radius_1m_f32_bwd_with_build": lambda: tb.tiga_mp_radius_bwd(pd, xd, dyd, r, s)}.items():
+        rr = time_steps(torch, tb, fn, steps, warm)
+        res[name] = dict(ms=rr["step_ms"], gedges_per_s=pairs / rr["step_ms"] / 1e6, accepted_pairs=pairs,
+                         kernel_ms=float(np.mean(rr["kernel_ms"])))
+        log(f"{name}: {rr['step_ms']:.3f} ms")
+    del pd, xd, dyd
+    g = synth.config4()
+    pd, qd = dev(g["pos"]), dev(g["q"])
+    nn = pd.shape[0]
+    rr = time_steps(torch, tb, lambda: tb.tiga_mp_dense_fwd(pd, qd, g["eps"]), steps, warm)
+    k = float(np.mean(rr["kernel_ms"]))
+    tf = nn * (nn - 1) * 20 / (k * 1e-3) / 1e12
+    res["dense_65536_fwd"] = dict(ms=rr["step_ms"], gpairs_per_s=nn * (nn - 1) / rr["step_ms"] / 1e6, kernel_ms=k,
+                                  tflops_20_per_pair=tf, frac_valu=tf / VALU_PEAK_TFLOPS)
+    log(f"dense: {rr['step_ms']:.3f} ms ({tf:.1f} TFLOP/s)")
+    return res
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import oracle
+    from paper_2609_24802_amd import binding as tb
+    from paper_2609_24802_amd import synth
+
+    if not os.path.exists(tb.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    tb.load()
+    h, cpu = headline(args, torch, tb, synth, oracle)
+    extra = {} if args.no_paths else paths(args, torch, tb, synth)
+    value = h["E"] / (h["step_ms"] * 1e-3) / 1e9
+    line = {
+        "metric": "GEdges/s fused fwd(+bwd) and achieved HBM GB/s vs peak, 1 MI355X",
+        "value": value,
+        "unit": "GEdges/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": h["step_ms"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded power-law CSR, Zipf(2.1) in-degrees, uniform sources)",
+        "config": {"workload": f"csr_powerlaw_{h['n']}n_{h['E']}e_f{h['F']}_sum_fwd", "num_nodes": h["n"],
+                   "num_edges": h["E"], "feat": h["F"], "reducer": "sum", "message": "w_e * x_src",
+                   "scale": args.scale},
+        "roofline": {"bound": "hbm", "achieved": h["achieved"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": h["achieved"] / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "gather_reduce_kernel", "kernel_ms": h["kernel_ms"],
+                     "bytes_per_launch": h["bytes_alg"]},
+        "cpu_baseline": cpu,
+        "parity_sampled": h["parity_ok"],
+        "paths": extra,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,284 @@
+"""Python binding of the gfx950 fused message-passing library (ctypes).
+
+Argument marshalling only: every function below checks tensor shapes, dtypes
+and devices, allocates outputs and the workspace with torch (device memory and
+the current stream are the only things torch provides here), and calls the
+C entry point of the same name.  All computation happens in the HIP kernels of
+``libtiga_mp.so``; if that library is missing or cannot be loaded, every call
+raises instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import threading
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtiga_mp.so")
+
+TIGA_OK, TIGA_EINVAL, TIGA_EGRAPH, TIGA_EUNSUPPORTED, TIGA_EWORKSPACE, TIGA_EDEVICE = 0, -1, -2, -3, -4, -5
+REDUCE_SUM, REDUCE_MAX = 0, 1
+MSG_SRC, MSG_EDGE_SCALED_SRC = 0, 1
+_STATUS = {0: "TIGA_OK", -1: "TIGA_EINVAL", -2: "TIGA_EGRAPH", -3: "TIGA_EUNSUPPORTED",
+           -4: "TIGA_EWORKSPACE", -5: "TIGA_EDEVICE"}
+
+
+class TigaError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"{_STATUS.get(code, code)}: {message}")
+        self.code = code
+
+
+class _Csr(C.Structure):
+    _fields_ = [("num_dst", C.c_int64), ("num_src", C.c_int64), ("num_edges", C.c_int64),
+                ("row_ptr", C.c_void_p), ("col_idx", C.c_void_p)]
+
+
+class _CsrT(C.Structure):
+    _fields_ = [("src_ptr", C.c_void_p), ("edge_id", C.c_void_p), ("dst_idx", C.c_void_p)]
+
+
+_lib = None
+_lock = threading.Lock()
+
+_SIGS = {
+    "tiga_last_error": (C.c_char_p, []),
+    "tiga_mp_abi_version": (C.c_int, []),
+    "tiga_mp_csr_fwd_workspace": (C.c_size_t, [C.c_void_p, C.c_int32, C.c_int]),
+    "tiga_mp_csr_fwd": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_int, C.c_void_p, C.c_int, C.c_void_p,
+                                  C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tiga_mp_csr_bwd_workspace": (C.c_size_t, [C.c_void_p, C.c_int32, C.c_int]),
+    "tiga_mp_csr_bwd": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_int, C.c_void_p, C.c_int,
+                                  C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
+                                  C.c_void_p]),
+    "tiga_csr_transpose_workspace": (C.c_size_t, [C.c_void_p]),
+    "tiga_csr_transpose": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
+                                     C.c_void_p]),
+    "tiga_csr_validate": (C.c_int, [C.c_void_p, C.c_int, C.c_void_p]),
+    "tiga_mp_radius_workspace": (C.c_size_t, [C.c_int64, C.c_int32]),
+    "tiga_mp_radius_fwd": (C.c_int, [C.c_int64, C.c_int32, C.c_void_p, C.c_void_p, C.c_float, C.c_float, C.c_int,
+                                     C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tiga_mp_radius_bwd": (C.c_int, [C.c_int64, C.c_int32, C.c_void_p, C.c_void_p, C.c_float, C.c_float,
+                                     C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tiga_radius_neighbors": (C.c_int, [C.c_int64, C.c_void_p, C.c_float, C.c_void_p, C.c_void_p, C.c_void_p,
+                                        C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tiga_mp_dense_workspace": (C.c_size_t, [C.c_int64]),
+    "tiga_mp_dense_fwd": (C.c_int, [C.c_int64, C.c_void_p, C.c_void_p, C.c_float, C.c_int, C.c_void_p,
+                                    C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tiga_mp_set_kernel_events": (C.c_int, [C.c_void_p, C.c_void_p]),
+}
+
+
+def load(path: str = LIB_PATH):
+    """Load the HIP library (torch's HIP runtime is loaded first and shared)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(path):
+                raise RuntimeError(f"HIP library not built: {path} is missing (run __graft_entry__.build())")
+            lib = C.CDLL(path)
+            for name, (res, args) in _SIGS.items():
+                fn = getattr(lib, name)
+                fn.restype = res
+                fn.argtypes = args
+            _lib = lib
+    return _lib
+
+
+def _check(rc: int):
+    if rc != TIGA_OK:
+        raise TigaError(rc, load().tiga_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(t, dtype, name, shape=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t
+
+
+def _workspace(nbytes: int, device):
+    ws = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+    assert ws.data_ptr() % 256 == 0
+    return ws
+
+
+class Csr:
+    """A destination-major CSR relation on the device (row_ptr int64, col_idx int32)."""
+
+    def __init__(self, row_ptr: torch.Tensor, col_idx: torch.Tensor, num_src: int):
+        self.row_ptr = _dev(row_ptr, torch.int64, "row_ptr")
+        self.col_idx = _dev(col_idx, torch.int32, "col_idx")
+        self.num_dst = row_ptr.numel() - 1
+        self.num_src = int(num_src)
+        self.num_edges = col_idx.numel()
+        self._c = _Csr(self.num_dst, self.num_src, self.num_edges, self.row_ptr.data_ptr(),
+                       self.col_idx.data_ptr() if self.num_edges else None)
+
+    @property
+    def ref(self):
+        return C.byref(self._c)
+
+
+class CsrT:
+    """Reverse incidence built by :func:`tiga_csr_transpose`."""
+
+    def __init__(self, src_ptr, edge_id, dst_idx):
+        self.src_ptr, self.edge_id, self.dst_idx = src_ptr, edge_id, dst_idx
+        self._c = _CsrT(src_ptr.data_ptr(), edge_id.data_ptr() if edge_id.numel() else None,
+                        dst_idx.data_ptr() if dst_idx.numel() else None)
+
+    @property
+    def ref(self):
+        return C.byref(self._c)
+
+
+def tiga_mp_abi_version() -> int:
+    return int(load().tiga_mp_abi_version())
+
+
+def tiga_mp_set_kernel_events(start=None, stop=None):
+    """Arm hipEvents (torch.cuda.Event, already recorded once) around the next dominant kernel."""
+    lib = load()
+    s = C.c_void_p(start.cuda_event) if start is not None else None
+    e = C.c_void_p(stop.cuda_event) if stop is not None else None
+    _check(lib.tiga_mp_set_kernel_events(s, e))
+
+
+def tiga_mp_csr_fwd(rel: Csr, x: torch.Tensor, w: torch.Tensor | None = None, reducer: int = REDUCE_SUM,
+                    y: torch.Tensor | None = None, argmax: torch.Tensor | None = None, ws=None):
+    """Fused forward over a stored CSR relation; returns (y, argmax or None)."""
+    lib = load()
+    feat = x.shape[1]
+    _dev(x, torch.float32, "x", (rel.num_src, feat))
+    msg = MSG_SRC
+    if w is not None:
+        _dev(w, torch.float32, "w", (rel.num_edges,))
+        msg = MSG_EDGE_SCALED_SRC
+    if y is None:
+        y = torch.empty(rel.num_dst, feat, dtype=torch.float32, device=x.device)
+    if reducer == REDUCE_MAX and argmax is None:
+        argmax = torch.empty(rel.num_dst, feat, dtype=torch.int32, device=x.device)
+    need = lib.tiga_mp_csr_fwd_workspace(rel.ref, feat, reducer)
+    if ws is None:
+        ws = _workspace(need, x.device)
+    _check(lib.tiga_mp_csr_fwd(rel.ref, feat, _ptr(x), msg, _ptr(w), reducer, _ptr(y), _ptr(argmax),
+                               _ptr(ws), ws.numel(), _stream()))
+    return y, argmax
+
+
+def tiga_mp_csr_bwd(rel: Csr, dy: torch.Tensor, x: torch.Tensor | None = None, w: torch.Tensor | None = None,
+                    reducer: int = REDUCE_SUM, argmax: torch.Tensor | None = None, rev: CsrT | None = None,
+                    want_dx: bool = True, want_dw: bool = True, ws=None):
+    """VJP of tiga_mp_csr_fwd; returns (dx or None, dw or None)."""
+    lib = load()
+    feat = dy.shape[1]
+    _dev(dy, torch.float32, "dy", (rel.num_dst, feat))
+    msg = MSG_EDGE_SCALED_SRC if w is not None else MSG_SRC
+    want_dw = want_dw and w is not None
+    dx = torch.empty(rel.num_src, feat, dtype=torch.float32, device=dy.device) if want_dx else None
+    dw = torch.empty(rel.num_edges, dtype=torch.float32, device=dy.device) if want_dw else None
+    need = lib.tiga_mp_csr_bwd_workspace(rel.ref, feat, reducer)
+    if ws is None:
+        ws = _workspace(need, dy.device)
+    _check(lib.tiga_mp_csr_bwd(rel.ref, rev.ref if rev is not None else None, feat, _ptr(x), msg, _ptr(w),
+                               reducer, _ptr(argmax), _ptr(dy), _ptr(dx), _ptr(dw), _ptr(ws), ws.numel(),
+                               _stream()))
+    return dx, dw
+
+
+def tiga_csr_transpose(rel: Csr) -> CsrT:
+    lib = load()
+    dev = rel.row_ptr.device
+    src_ptr = torch.empty(rel.num_src + 1, dtype=torch.int64, device=dev)
+    edge_id = torch.empty(rel.num_edges, dtype=torch.int32, device=dev)
+    dst_idx = torch.empty(rel.num_edges, dtype=torch.int32, device=dev)
+    ws = _workspace(lib.tiga_csr_transpose_workspace(rel.ref), dev)
+    _check(lib.tiga_csr_transpose(rel.ref, _ptr(src_ptr), _ptr(edge_id) if rel.num_edges else None,
+                                  _ptr(dst_idx) if rel.num_edges else None, _ptr(ws), ws.numel(), _stream()))
+    return CsrT(src_ptr, edge_id, dst_idx)
+
+
+def tiga_csr_validate(rel: Csr, level: int = 2):
+    """Raise TigaError (TIGA_EGRAPH) on an invalid relation."""
+    _check(load().tiga_csr_validate(rel.ref, level, _stream()))
+
+
+def tiga_mp_radius_fwd(pos: torch.Tensor, x: torch.Tensor, radius: float, sigma: float, want_count: bool = True,
+                       y=None, count=None, ws=None):
+    lib = load()
+    n, feat = x.shape
+    _dev(pos, torch.float32, "pos", (n, 3))
+    _dev(x, torch.float32, "x", (n, feat))
+    if y is None:
+        y = torch.empty(n, feat, dtype=torch.float32, device=x.device)
+    if want_count and count is None:
+        count = torch.empty(n, dtype=torch.int32, device=x.device)
+    if ws is None:
+        ws = _workspace(lib.tiga_mp_radius_workspace(n, feat), x.device)
+    _check(lib.tiga_mp_radius_fwd(n, feat, _ptr(pos), _ptr(x), float(radius), float(sigma), REDUCE_SUM, _ptr(y),
+                                  _ptr(count), _ptr(ws), ws.numel(), _stream()))
+    return y, count
+
+
+def tiga_mp_radius_bwd(pos, x, dy, radius: float, sigma: float, want_dx: bool = True, want_dpos: bool = True,
+                       ws=None):
+    lib = load()
+    n, feat = dy.shape
+    _dev(pos, torch.float32, "pos", (n, 3))
+    _dev(dy, torch.float32, "dy", (n, feat))
+    if want_dpos:
+        _dev(x, torch.float32, "x", (n, feat))
+    dx = torch.empty(n, feat, dtype=torch.float32, device=dy.device) if want_dx else None
+    dpos = torch.empty(n, 3, dtype=torch.float32, device=dy.device) if want_dpos else None
+    if ws is None:
+        ws = _workspace(lib.tiga_mp_radius_workspace(n, feat), dy.device)
+    _check(lib.tiga_mp_radius_bwd(n, feat, _ptr(pos), _ptr(x) if want_dpos else None, float(radius), float(sigma),
+                                  _ptr(dy), _ptr(dx), _ptr(dpos), _ptr(ws), ws.numel(), _stream()))
+    return dx, dpos
+
+
+def tiga_radius_neighbors(pos: torch.Tensor, radius: float):
+    """Accepted neighbour lists; returns (count int32, ptr int64 [n+1], idx int32).  Synchronizes."""
+    lib = load()
+    n = pos.shape[0]
+    _dev(pos, torch.float32, "pos", (n, 3))
+    count = torch.empty(n, dtype=torch.int32, device=pos.device)
+    ptr = torch.empty(n + 1, dtype=torch.int64, device=pos.device)
+    ws = _workspace(lib.tiga_mp_radius_workspace(n, 0), pos.device)
+    _check(lib.tiga_radius_neighbors(n, _ptr(pos), float(radius), _ptr(count), _ptr(ptr), None, _ptr(ws),
+                                     ws.numel(), _stream()))
+    total = int(ptr[-1].item())
+    idx = torch.empty(max(total, 1), dtype=torch.int32, device=pos.device)
+    _check(lib.tiga_radius_neighbors(n, _ptr(pos), float(radius), None, _ptr(ptr), _ptr(idx), _ptr(ws), ws.numel(),
+                                     _stream()))
+    return count, ptr, idx[:total]
+
+
+def tiga_mp_dense_fwd(pos: torch.Tensor, q: torch.Tensor, eps: float, y=None, ws=None):
+    lib = load()
+    n = pos.shape[0]
+    _dev(pos, torch.float32, "pos", (n, 3))
+    _dev(q, torch.float32, "q", (n,))
+    if y is None:
+        y = torch.empty(n, 3, dtype=torch.float32, device=pos.device)
+    if ws is None:
+        ws = _workspace(lib.tiga_mp_dense_workspace(n), pos.device)
+    _check(lib.tiga_mp_dense_fwd(n, _ptr(pos), _ptr(q), float(eps), REDUCE_SUM, _ptr(y), _ptr(ws), ws.numel(),
+                                 _stream()))
+    return y

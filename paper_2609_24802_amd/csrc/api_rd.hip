@@ -1,0 +1,99 @@
+// C ABI of the generated radius relation and the dense all-pairs relation.
+#include "dense.hpp"
+#include "radius.hpp"
+
+using namespace tiga;
+
+namespace {
+
+int check_ws(void *ws, size_t ws_bytes, size_t need) {
+    if (ws_bytes < need)
+        return fail(TIGA_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, need);
+    if (need > 0 && !ws) return fail(TIGA_EINVAL, "ws is NULL");
+    if (ws && (reinterpret_cast<uintptr_t>(ws) & 255u)) return fail(TIGA_EINVAL, "ws must be 256-byte aligned");
+    return TIGA_OK;
+}
+
+int check_points(int64_t n, const float *pos) {
+    if (n < 0) return fail(TIGA_EINVAL, "n must be >= 0 (got %lld)", (long long)n);
+    if (n > INT32_MAX - 64) return fail(TIGA_EUNSUPPORTED, "n %lld exceeds the int32 point-id range", (long long)n);
+    if (n > 0 && !pos) return fail(TIGA_EINVAL, "pos is NULL");
+    return TIGA_OK;
+}
+
+int check_radius(float radius, float sigma) {
+    if (!(radius > 0.0f) || !(radius < 3.0e38f)) return fail(TIGA_EINVAL, "radius must be finite and > 0");
+    if (!(sigma > 0.0f) || !(sigma < 3.0e38f)) return fail(TIGA_EINVAL, "sigma must be finite and > 0");
+    return TIGA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t tiga_mp_radius_workspace(int64_t n, int32_t feat) {
+    if (n < 0 || feat < 0) return 0;
+    return radius::workspace_bytes(n, feat);
+}
+
+int tiga_mp_radius_fwd(int64_t n, int32_t feat, const float *pos, const float *x, float radius, float sigma,
+                       int reducer, float *y, int32_t *count, void *ws, size_t ws_bytes, void *stream) {
+    clear_error();
+    if (int rc = check_points(n, pos)) return rc;
+    if (feat < 1) return fail(TIGA_EINVAL, "feat must be >= 1 (got %d)", feat);
+    if (reducer == TIGA_REDUCE_MAX) return fail(TIGA_EUNSUPPORTED, "the radius relation supports the sum reducer only");
+    if (reducer != TIGA_REDUCE_SUM) return fail(TIGA_EINVAL, "unknown reducer %d", reducer);
+    if (int rc = check_radius(radius, sigma)) return rc;
+    if (n == 0) return TIGA_OK;
+    if (!x || !y) return fail(TIGA_EINVAL, "x and y are required");
+    if (int rc = check_ws(ws, ws_bytes, radius::workspace_bytes(n, feat))) return rc;
+    return radius::forward(n, feat, pos, x, radius, sigma, y, count, ws, static_cast<hipStream_t>(stream));
+}
+
+int tiga_mp_radius_bwd(int64_t n, int32_t feat, const float *pos, const float *x, float radius, float sigma,
+                       const float *dy, float *dx, float *dpos, void *ws, size_t ws_bytes, void *stream) {
+    clear_error();
+    if (int rc = check_points(n, pos)) return rc;
+    if (feat < 1) return fail(TIGA_EINVAL, "feat must be >= 1 (got %d)", feat);
+    if (int rc = check_radius(radius, sigma)) return rc;
+    if (n == 0 || (!dx && !dpos)) return TIGA_OK;
+    if (!dy) return fail(TIGA_EINVAL, "dy is NULL");
+    if (dpos && !x) return fail(TIGA_EINVAL, "x is required for dpos");
+    if (int rc = check_ws(ws, ws_bytes, radius::workspace_bytes(n, feat))) return rc;
+    return radius::backward(n, feat, pos, x, radius, sigma, dy, dx, dpos, ws, static_cast<hipStream_t>(stream));
+}
+
+int tiga_radius_neighbors(int64_t n, const float *pos, float radius, int32_t *count, int64_t *nbr_ptr,
+                          int32_t *nbr_idx, void *ws, size_t ws_bytes, void *stream) {
+    clear_error();
+    if (int rc = check_points(n, pos)) return rc;
+    if (int rc = check_radius(radius, 1.0f)) return rc;
+    if (!nbr_ptr) return fail(TIGA_EINVAL, "nbr_ptr is NULL");
+    if (n == 0) {
+        if (nbr_idx) return TIGA_OK;
+        if (int rc = fill_u32(nbr_ptr, 0u, 2, static_cast<hipStream_t>(stream))) return rc;
+        return check_hip(hipStreamSynchronize(static_cast<hipStream_t>(stream)), "neighbours: synchronize");
+    }
+    if (int rc = check_ws(ws, ws_bytes, radius::workspace_bytes(n, 0))) return rc;
+    return radius::neighbors(n, pos, radius, count, nbr_ptr, nbr_idx, ws, static_cast<hipStream_t>(stream));
+}
+
+size_t tiga_mp_dense_workspace(int64_t n) {
+    if (n < 0) return 0;
+    return dense::workspace_bytes(n);
+}
+
+int tiga_mp_dense_fwd(int64_t n, const float *pos, const float *q, float eps, int reducer, float *y, void *ws,
+                      size_t ws_bytes, void *stream) {
+    clear_error();
+    if (int rc = check_points(n, pos)) return rc;
+    if (reducer == TIGA_REDUCE_MAX) return fail(TIGA_EUNSUPPORTED, "the dense relation supports the sum reducer only");
+    if (reducer != TIGA_REDUCE_SUM) return fail(TIGA_EINVAL, "unknown reducer %d", reducer);
+    if (!(eps > 0.0f) || !(eps < 3.0e38f)) return fail(TIGA_EINVAL, "eps must be finite and > 0");
+    if (n == 0) return TIGA_OK;
+    if (!q || !y) return fail(TIGA_EINVAL, "q and y are required");
+    if (int rc = check_ws(ws, ws_bytes, dense::workspace_bytes(n))) return rc;
+    return dense::forward(n, pos, q, eps, y, ws, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,37 @@
+// Host interface of the CSR vector-Jacobian products, the stable transpose and
+// full validation.
+#pragma once
+
+#include "csr_fwd.hpp"
+
+namespace tiga {
+namespace csr {
+
+struct BwdArgs {
+    const tiga_csr *rel;
+    const tiga_csr_t *rev;  // null: atomic dx
+    int32_t feat;
+    const float *x;         // [num_src, feat]
+    const float *w;         // [num_edges] or null (unweighted message)
+    int red;
+    const int32_t *arg;     // [num_dst, feat] (max)
+    const float *dy;        // [num_dst, feat]
+    float *dx;              // [num_src, feat] or null
+    float *dw;              // [num_edges] or null
+};
+
+size_t bwd_ws_bytes(int64_t num_dst, int64_t num_src, int64_t num_edges, int64_t feat);
+int launch_bwd(const BwdArgs &a, void *ws, hipStream_t stream);
+
+size_t transpose_ws_bytes(int64_t num_dst, int64_t num_src, int64_t num_edges);
+int launch_transpose(const tiga_csr *rel, int64_t *src_ptr, int32_t *edge_id, int32_t *dst_idx, void *ws,
+                     hipStream_t stream);
+
+int launch_validate(const tiga_csr *rel, hipStream_t stream);
+
+// Device-wide exclusive prefix sum of n int64 values (in may equal out).
+size_t scan_ws_bytes(int64_t n);
+int launch_excl_scan(const int64_t *in, int64_t *out, int64_t n, void *ws, hipStream_t stream);
+
+}  // namespace csr
+}  // namespace tiga

@@ -1,0 +1,332 @@
+// Topology utilities: device exclusive scan, the stable CSR transpose (an LSD
+// radix sort of edge positions keyed by source id) and full validation.
+#include "csr_bwd.hpp"
+
+namespace tiga {
+namespace csr {
+
+namespace {
+
+constexpr int kScanItems = 8;
+constexpr int kScanTile = kBlock * kScanItems;
+
+// Block-wide exclusive scan of one int64 per thread; returns the block total.
+__device__ __forceinline__ int64_t block_excl_scan(int64_t v, int64_t &excl) {
+    __shared__ int64_t sh[kWavesPerBlock];
+    const int lane = lane_id();
+    const int wave = threadIdx.x / kWave;
+    const int64_t inc = wave_incl_scan(v);
+    if (lane == kWave - 1) sh[wave] = inc;
+    __syncthreads();
+    int64_t off = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) {
+        if (w < wave) off += sh[w];
+        tot += sh[w];
+    }
+    __syncthreads();
+    excl = off + inc - v;
+    return tot;
+}
+
+__global__ __launch_bounds__(kBlock) void scan_reduce_kernel(const int64_t *__restrict__ in, int64_t n,
+                                                             int64_t *__restrict__ partial) {
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanTile;
+    int64_t s = 0;
+#pragma unroll
+    for (int r = 0; r < kScanItems; ++r) {
+        const int64_t i = base + r * kBlock + threadIdx.x;
+        if (i < n) s += in[i];
+    }
+    int64_t excl;
+    const int64_t tot = block_excl_scan(s, excl);
+    if (threadIdx.x == 0) partial[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(kBlock) void scan_partials_kernel(int64_t *__restrict__ partial, int64_t n) {
+    int64_t carry = 0;
+    for (int64_t b = 0; b < n; b += kBlock) {
+        const int64_t i = b + threadIdx.x;
+        const int64_t v = i < n ? partial[i] : 0;
+        int64_t excl;
+        const int64_t tot = block_excl_scan(v, excl);
+        if (i < n) partial[i] = carry + excl;
+        carry += tot;
+    }
+}
+
+// Each thread scans kScanItems consecutive elements of the tile.
+__global__ __launch_bounds__(kBlock) void scan_down_kernel(const int64_t *in, int64_t *out, int64_t n,
+                                                           const int64_t *__restrict__ partial) {
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanTile + threadIdx.x * kScanItems;
+    int64_t v[kScanItems];
+    int64_t s = 0;
+#pragma unroll
+    for (int r = 0; r < kScanItems; ++r) {
+        v[r] = (base + r < n) ? in[base + r] : 0;
+        s += v[r];
+    }
+    int64_t excl;
+    block_excl_scan(s, excl);
+    int64_t run = partial[blockIdx.x] + excl;
+#pragma unroll
+    for (int r = 0; r < kScanItems; ++r) {
+        if (base + r < n) out[base + r] = run;
+        run += v[r];
+    }
+}
+
+// ---------------------------------------------------------------- radix sort
+
+constexpr int kRadixBits = 8;
+constexpr int kRadix = 1 << kRadixBits;
+constexpr int kSortItems = 8;
+constexpr int kSortTile = kBlock * kSortItems;
+
+__global__ __launch_bounds__(kBlock) void radix_hist_kernel(const int32_t *__restrict__ keys, int64_t n, int shift,
+                                                            int64_t nblocks, int64_t *__restrict__ counts) {
+    __shared__ int hist[kRadix];
+    hist[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kSortTile;
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+        const int64_t i = base + r * kBlock + threadIdx.x;
+        if (i < n) atomicAdd(&hist[(static_cast<uint32_t>(keys[i]) >> shift) & (kRadix - 1)], 1);
+    }
+    __syncthreads();
+    // digit-major layout: all blocks of digit 0, then digit 1, ...
+    counts[static_cast<int64_t>(threadIdx.x) * nblocks + blockIdx.x] = hist[threadIdx.x];
+}
+
+// Stable scatter.  Elements of a tile are ranked in (round, wave, lane) order,
+// which is their input order; equal digits keep that order.
+__global__ __launch_bounds__(kBlock) void radix_scatter_kernel(
+    const int32_t *__restrict__ keys_in, const int32_t *__restrict__ v0_in, const int32_t *__restrict__ v1_in,
+    int32_t *__restrict__ keys_out, int32_t *__restrict__ v0_out, int32_t *__restrict__ v1_out, int64_t n,
+    int shift, int64_t nblocks, const int64_t *__restrict__ offsets, int iota_v0) {
+    __shared__ int64_t run[kRadix];
+    __shared__ int wcnt[kWavesPerBlock][kRadix];
+    run[threadIdx.x] = offsets[static_cast<int64_t>(threadIdx.x) * nblocks + blockIdx.x];
+    const int lane = lane_id();
+    const int wave = threadIdx.x / kWave;
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kSortTile;
+    for (int r = 0; r < kSortItems; ++r) {
+#pragma unroll
+        for (int w = 0; w < kWavesPerBlock; ++w) wcnt[w][threadIdx.x] = 0;
+        __syncthreads();
+        const int64_t i = base + r * kBlock + threadIdx.x;
+        const bool valid = i < n;
+        int32_t key = 0, a = 0, b = 0;
+        int digit = 0;
+        if (valid) {
+            key = keys_in[i];
+            a = iota_v0 ? static_cast<int32_t>(i) : v0_in[i];
+            b = v1_in[i];
+            digit = (static_cast<uint32_t>(key) >> shift) & (kRadix - 1);
+        }
+        uint64_t peers = __ballot(valid);
+#pragma unroll
+        for (int bit = 0; bit < kRadixBits; ++bit) {
+            const uint64_t m = __ballot((digit >> bit) & 1);
+            peers &= ((digit >> bit) & 1) ? m : ~m;
+        }
+        const int rank = __popcll(peers & lt_mask);
+        if (valid && rank == 0) wcnt[wave][digit] = __popcll(peers);
+        __syncthreads();
+        if (valid) {
+            int64_t pos = run[digit] + rank;
+            for (int w = 0; w < wave; ++w) pos += wcnt[w][digit];
+            keys_out[pos] = key;
+            v0_out[pos] = a;
+            v1_out[pos] = b;
+        }
+        __syncthreads();
+        int64_t add = 0;
+#pragma unroll
+        for (int w = 0; w < kWavesPerBlock; ++w) add += wcnt[w][threadIdx.x];
+        run[threadIdx.x] += add;
+        __syncthreads();
+    }
+}
+
+// dst id of every edge position (row expansion of row_ptr).
+__global__ __launch_bounds__(kBlock) void expand_rows_kernel(const int64_t *__restrict__ row_ptr, int64_t nrows,
+                                                             int32_t *__restrict__ dst) {
+    const int64_t wave = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
+    const int64_t nwaves = static_cast<int64_t>(gridDim.x) * kWavesPerBlock;
+    for (int64_t row = wave; row < nrows; row += nwaves) {
+        const int64_t e1 = row_ptr[row + 1];
+        for (int64_t e = row_ptr[row] + lane_id(); e < e1; e += kWave) dst[e] = static_cast<int32_t>(row);
+    }
+}
+
+// src_ptr[j] = first sorted position with key >= j.
+__global__ __launch_bounds__(kBlock) void ptr_from_sorted_kernel(const int32_t *__restrict__ sorted, int64_t n,
+                                                                 int64_t nkeys, int64_t *__restrict__ ptr) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t k = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; k <= n; k += stride) {
+        const int64_t lo = (k == 0) ? -1 : static_cast<int64_t>(sorted[k - 1]);
+        const int64_t hi = (k == n) ? nkeys : static_cast<int64_t>(sorted[k]);
+        for (int64_t j = lo + 1; j <= hi; ++j) ptr[j] = k;
+    }
+}
+
+// ---------------------------------------------------------------- validation
+
+struct Violations {
+    unsigned long long first_row;    // first i with row_ptr[i] > row_ptr[i+1]
+    unsigned long long first_col;    // first e with col out of range
+    long long rp0, rpn;              // row_ptr[0], row_ptr[num_dst]
+};
+
+__global__ __launch_bounds__(kBlock) void validate_kernel(const int64_t *__restrict__ row_ptr,
+                                                          const int32_t *__restrict__ col, int64_t nrows,
+                                                          int64_t nedges, int64_t nsrc, Violations *v) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    const int64_t tid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (tid == 0) {
+        v->rp0 = row_ptr[0];
+        v->rpn = row_ptr[nrows];
+    }
+    for (int64_t i = tid; i < nrows; i += stride)
+        if (row_ptr[i] > row_ptr[i + 1]) atomicMin(&v->first_row, static_cast<unsigned long long>(i));
+    for (int64_t e = tid; e < nedges; e += stride) {
+        const int32_t c = col[e];
+        if (c < 0 || c >= nsrc) atomicMin(&v->first_col, static_cast<unsigned long long>(e));
+    }
+}
+
+__global__ void validate_init_kernel(Violations *v) {
+    v->first_row = ~0ull;
+    v->first_col = ~0ull;
+    v->rp0 = 0;
+    v->rpn = 0;
+}
+
+}  // namespace
+
+size_t scan_ws_bytes(int64_t n) {
+    Carve c(nullptr);
+    c.take<int64_t>(ceil_div(n > 0 ? n : 1, kScanTile));
+    return c.bytes();
+}
+
+int launch_excl_scan(const int64_t *in, int64_t *out, int64_t n, void *ws, hipStream_t stream) {
+    if (n <= 0) return TIGA_OK;
+    const int64_t blocks = ceil_div(n, kScanTile);
+    Carve c(ws);
+    int64_t *partial = c.take<int64_t>(blocks);
+    hipLaunchKernelGGL(scan_reduce_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kBlock), 0, stream, in, n, partial);
+    if (int rc = check_launch("scan reduce")) return rc;
+    hipLaunchKernelGGL(scan_partials_kernel, dim3(1), dim3(kBlock), 0, stream, partial, blocks);
+    if (int rc = check_launch("scan partials")) return rc;
+    hipLaunchKernelGGL(scan_down_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kBlock), 0, stream, in, out, n,
+                       partial);
+    return check_launch("scan down");
+}
+
+namespace {
+struct SortWs {
+    int32_t *k[2], *a[2], *b[2];
+    int64_t *counts;
+    void *scan;
+};
+
+SortWs carve_sort(Carve &c, int64_t n) {
+    SortWs s;
+    const int64_t nb = ceil_div(n > 0 ? n : 1, kSortTile);
+    for (int i = 0; i < 2; ++i) {
+        s.k[i] = c.take<int32_t>(n);
+        s.a[i] = c.take<int32_t>(n);
+        s.b[i] = c.take<int32_t>(n);
+    }
+    s.counts = c.take<int64_t>(nb * kRadix);
+    s.scan = c.take<char>(scan_ws_bytes(nb * kRadix));
+    return s;
+}
+}  // namespace
+
+size_t transpose_ws_bytes(int64_t num_dst, int64_t num_src, int64_t num_edges) {
+    (void)num_dst;
+    (void)num_src;
+    Carve c(nullptr);
+    carve_sort(c, num_edges);
+    return c.bytes();
+}
+
+int launch_transpose(const tiga_csr *rel, int64_t *src_ptr, int32_t *edge_id, int32_t *dst_idx, void *ws,
+                     hipStream_t stream) {
+    const int64_t n = rel->num_edges;
+    Carve c(ws);
+    SortWs s = carve_sort(c, n);
+    if (n > 0) {
+        const int eb = persistent_blocks(rel->num_dst, 8);
+        hipLaunchKernelGGL(expand_rows_kernel, dim3(eb), dim3(kBlock), 0, stream, rel->row_ptr, rel->num_dst, s.b[0]);
+        if (int rc = check_launch("expand rows")) return rc;
+        int bits = 1;
+        while (bits < 31 && (int64_t{1} << bits) < rel->num_src) ++bits;
+        const int passes = (bits + kRadixBits - 1) / kRadixBits;
+        const int64_t nb = ceil_div(n, kSortTile);
+        const int32_t *kin = rel->col_idx;
+        int cur = 0;
+        for (int p = 0; p < passes; ++p) {
+            const int shift = p * kRadixBits;
+            hipLaunchKernelGGL(radix_hist_kernel, dim3(static_cast<unsigned>(nb)), dim3(kBlock), 0, stream, kin, n,
+                               shift, nb, s.counts);
+            if (int rc = check_launch("radix histogram")) return rc;
+            if (int rc = launch_excl_scan(s.counts, s.counts, nb * kRadix, s.scan, stream)) return rc;
+            // the last pass writes straight into the caller's arrays
+            const bool last = p == passes - 1;
+            int32_t *ko = s.k[cur ^ 1];
+            int32_t *ao = last ? edge_id : s.a[cur ^ 1];
+            int32_t *bo = last ? dst_idx : s.b[cur ^ 1];
+            const int32_t *ai = s.a[cur];
+            const int32_t *bi = s.b[cur];
+            hipLaunchKernelGGL(radix_scatter_kernel, dim3(static_cast<unsigned>(nb)), dim3(kBlock), 0, stream, kin,
+                               ai, bi, ko, ao, bo, n, shift, nb, s.counts, p == 0 ? 1 : 0);
+            if (int rc = check_launch("radix scatter")) return rc;
+            kin = ko;
+            cur ^= 1;
+            if (!last) {
+                // the payloads of the next pass come from the buffers just written
+            }
+        }
+        const int pb = persistent_blocks(ceil_div(n + 1, kWave), 8);
+        hipLaunchKernelGGL(ptr_from_sorted_kernel, dim3(pb), dim3(kBlock), 0, stream, kin, n, rel->num_src, src_ptr);
+        return check_launch("source pointers");
+    }
+    return fill_u32(src_ptr, 0u, 2 * (rel->num_src + 1), stream);
+}
+
+int launch_validate(const tiga_csr *rel, hipStream_t stream) {
+    Violations *dv = nullptr;
+    if (int rc = check_hip(hipMalloc(&dv, sizeof(Violations)), "validate: hipMalloc")) return rc;
+    Violations hv{};
+    int rc = TIGA_OK;
+    hipLaunchKernelGGL(validate_init_kernel, dim3(1), dim3(1), 0, stream, dv);
+    rc = check_launch("validate init");
+    if (!rc) {
+        const int blocks = persistent_blocks(ceil_div(rel->num_dst + rel->num_edges, kWave), 8);
+        hipLaunchKernelGGL(validate_kernel, dim3(blocks), dim3(kBlock), 0, stream, rel->row_ptr, rel->col_idx,
+                           rel->num_dst, rel->num_edges, rel->num_src, dv);
+        rc = check_launch("validate");
+    }
+    if (!rc) rc = check_hip(hipMemcpyAsync(&hv, dv, sizeof hv, hipMemcpyDeviceToHost, stream), "validate: copy");
+    if (!rc) rc = check_hip(hipStreamSynchronize(stream), "validate: synchronize");
+    (void)hipFree(dv);
+    if (rc) return rc;
+    if (hv.rp0 != 0) return fail(TIGA_EGRAPH, "row_ptr[0] = %lld, expected 0", hv.rp0);
+    if (hv.first_row != ~0ull)
+        return fail(TIGA_EGRAPH, "row_ptr decreases at row %llu (row_ptr[i] > row_ptr[i+1])", hv.first_row);
+    if (hv.rpn != rel->num_edges)
+        return fail(TIGA_EGRAPH, "row_ptr[num_dst] = %lld, expected num_edges = %lld", hv.rpn,
+                    (long long)rel->num_edges);
+    if (hv.first_col != ~0ull)
+        return fail(TIGA_EGRAPH, "col_idx[%llu] is outside [0, %lld)", hv.first_col, (long long)rel->num_src);
+    return TIGA_OK;
+}
+
+}  // namespace csr
+}  // namespace tiga

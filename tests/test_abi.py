@@ -1,0 +1,126 @@
+"""The C-ABI library loads and exports every declared entry point, and its
+host-side argument checks reject bad calls before anything reaches a device.
+
+No compute call is made here: every call below returns from the host checks.
+"""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tiga_mp.h")
+LIB = os.path.join(ROOT, "paper_2609_24802_amd", "libtiga_mp.so")
+
+
+def declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b((?:tiga)_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def clib():
+    if not os.path.exists(LIB):
+        import __graft_entry__
+        __graft_entry__.build()
+    from paper_2609_24802_amd import binding
+    return binding.load(LIB)
+
+
+def test_exports_every_declared_symbol(clib):
+    names = declared()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(clib, n), n
+
+
+def test_abi_version(clib):
+    assert clib.tiga_mp_abi_version() == 1
+
+
+def _csr(num_dst, num_src, num_edges, rp=0x1000, col=0x2000):
+    from paper_2609_24802_amd.binding import _Csr
+    return _Csr(num_dst, num_src, num_edges, rp, col)
+
+
+def test_csr_forward_argument_errors(clib):
+    from paper_2609_24802_amd import binding as b
+    fake = C.c_void_p(0x10000)
+    rel = _csr(4, 4, 10)
+    ws_need = clib.tiga_mp_csr_fwd_workspace(C.byref(rel), 16, b.REDUCE_SUM)
+    assert ws_need > 0
+    cases = [
+        (dict(rel=None), b.TIGA_EINVAL),
+        (dict(feat=0), b.TIGA_EINVAL),
+        (dict(reducer=7), b.TIGA_EINVAL),
+        (dict(msg=b.MSG_SRC), b.TIGA_EINVAL),  # weights given with an unweighted message
+        (dict(w=None), b.TIGA_EINVAL),  # weighted message without weights
+        (dict(y=None), b.TIGA_EINVAL),
+        (dict(reducer=b.REDUCE_MAX), b.TIGA_EINVAL),  # max without argmax
+        (dict(argmax=fake), b.TIGA_EINVAL),  # argmax with sum
+        (dict(ws_bytes=16), b.TIGA_EWORKSPACE),
+        (dict(ws=C.c_void_p(0x10010)), b.TIGA_EINVAL),  # misaligned workspace
+        (dict(rel=_csr(4, 4, 3 << 30), reducer=b.REDUCE_MAX, argmax=fake), b.TIGA_EUNSUPPORTED),
+        (dict(rel=_csr(-1, 4, 10)), b.TIGA_EINVAL),
+        (dict(rel=_csr(4, 0, 10)), b.TIGA_EINVAL),
+        (dict(rel=_csr(4, 4, 10, rp=0)), b.TIGA_EINVAL),
+    ]
+    for over, code in cases:
+        a = dict(rel=rel, feat=16, x=fake, msg=b.MSG_EDGE_SCALED_SRC, w=fake, reducer=b.REDUCE_SUM, y=fake,
+                 argmax=None, ws=fake, ws_bytes=1 << 40)
+        a.update(over)
+        relp = C.byref(a["rel"]) if a["rel"] is not None else None
+        rc = clib.tiga_mp_csr_fwd(relp, a["feat"], a["x"], a["msg"], a["w"], a["reducer"], a["y"], a["argmax"],
+                                  a["ws"], a["ws_bytes"], None)
+        assert rc == code, (over, rc, clib.tiga_last_error())
+        assert clib.tiga_last_error()
+
+
+def test_csr_backward_and_transpose_errors(clib):
+    from paper_2609_24802_amd import binding as b
+    fake = C.c_void_p(0x10000)
+    rel = _csr(4, 4, 10)
+    rc = clib.tiga_mp_csr_bwd(C.byref(rel), None, 8, fake, b.MSG_SRC, None, b.REDUCE_SUM, None, fake, fake, fake,
+                              fake, 1 << 40, None)
+    assert rc == b.TIGA_EINVAL  # dw needs the weighted message
+    rc = clib.tiga_mp_csr_bwd(C.byref(rel), None, 8, fake, b.MSG_EDGE_SCALED_SRC, fake, b.REDUCE_MAX, None, fake,
+                              fake, None, fake, 1 << 40, None)
+    assert rc == b.TIGA_EINVAL  # max without argmax
+    big = _csr(4, 4, 3 << 30)
+    rc = clib.tiga_csr_transpose(C.byref(big), fake, fake, fake, fake, 1 << 40, None)
+    assert rc == b.TIGA_EUNSUPPORTED
+    rc = clib.tiga_csr_validate(C.byref(rel), 3, None)
+    assert rc == b.TIGA_EINVAL
+    assert clib.tiga_csr_validate(C.byref(rel), 1, None) == b.TIGA_OK
+    assert clib.tiga_csr_validate(C.byref(_csr(4, 0, 10)), 1, None) == b.TIGA_EGRAPH
+
+
+def test_radius_dense_errors(clib):
+    from paper_2609_24802_amd import binding as b
+    fake = C.c_void_p(0x10000)
+    rc = clib.tiga_mp_radius_fwd(100, 8, fake, fake, 0.1, 0.05, b.REDUCE_MAX, fake, None, fake, 1 << 40, None)
+    assert rc == b.TIGA_EUNSUPPORTED
+    rc = clib.tiga_mp_radius_fwd(100, 8, fake, fake, -0.1, 0.05, b.REDUCE_SUM, fake, None, fake, 1 << 40, None)
+    assert rc == b.TIGA_EINVAL
+    rc = clib.tiga_mp_radius_fwd(100, 8, fake, fake, 0.1, 0.05, b.REDUCE_SUM, fake, None, fake, 8, None)
+    assert rc == b.TIGA_EWORKSPACE
+    rc = clib.tiga_mp_radius_bwd(100, 8, fake, None, 0.1, 0.05, fake, fake, fake, fake, 1 << 40, None)
+    assert rc == b.TIGA_EINVAL  # dpos needs x
+    rc = clib.tiga_mp_dense_fwd(100, fake, fake, 0.0, b.REDUCE_SUM, fake, fake, 1 << 40, None)
+    assert rc == b.TIGA_EINVAL
+    rc = clib.tiga_mp_dense_fwd(100, fake, fake, 0.01, b.REDUCE_MAX, fake, fake, 1 << 40, None)
+    assert rc == b.TIGA_EUNSUPPORTED
+    # empty inputs are valid no-ops
+    assert clib.tiga_mp_dense_fwd(0, None, None, 0.01, b.REDUCE_SUM, None, None, 0, None) == b.TIGA_OK
+    assert clib.tiga_mp_radius_fwd(0, 8, None, None, 0.1, 0.05, b.REDUCE_SUM, None, None, None, 0, None) == b.TIGA_OK
+
+
+def test_workspace_queries_monotone(clib):
+    from paper_2609_24802_amd import binding as b
+    small = clib.tiga_mp_csr_fwd_workspace(C.byref(_csr(1000, 1000, 16000)), 64, b.REDUCE_MAX)
+    large = clib.tiga_mp_csr_fwd_workspace(C.byref(_csr(1_000_000, 1_000_000, 16_000_000)), 64, b.REDUCE_MAX)
+    assert 0 < small < large
+    assert clib.tiga_mp_radius_workspace(1000, 32) < clib.tiga_mp_radius_workspace(100000, 32)
+    assert clib.tiga_mp_dense_workspace(65536) > 65536 * 16

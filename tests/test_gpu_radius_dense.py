@@ -1,0 +1,137 @@
+"""GPU parity of the radius and dense relations against the oracle.
+
+Radius counts and neighbour lists are bit-exact (the predicate is a frozen
+fp32 recipe on both sides); values and gradients are within 1e-5 * sum|terms|.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_24802_amd import synth
+from tests.parity import assert_terms_close
+
+pytestmark = pytest.mark.gpu
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    return t.cpu().numpy()
+
+
+def cloud(kind, n, seed):
+    rng = np.random.default_rng(seed)
+    if kind == "uniform":
+        return synth.uniform_f32(n * 3, 0.0, 1.0, (80, seed)).reshape(n, 3)
+    if kind == "grid":  # binary-grid coordinates: many points exactly on cell boundaries
+        return synth.binary_grid_points(n, 5, (81, seed), span=24)
+    if kind == "cluster":  # a dense clump plus a sparse background, coincident points
+        p = rng.random((n, 3)).astype(np.float32)
+        p[: n // 4] = (0.5 + 0.01 * rng.random((n // 4, 3))).astype(np.float32)
+        p[n // 4: n // 4 + 20] = p[:20]
+        return p
+    if kind == "flat":  # a plane: zero extent in z
+        p = rng.random((n, 3)).astype(np.float32)
+        p[:, 2] = 0.25
+        return p
+    raise ValueError(kind)
+
+
+@pytest.mark.parametrize("kind,n,r,F", [("uniform", 3000, 0.07, 16), ("grid", 2500, 0.1, 4),
+                                        ("cluster", 2000, 0.05, 3), ("flat", 1500, 0.06, 32),
+                                        ("uniform", 777, 0.2, 1), ("uniform", 5000, 0.04, 64)])
+def test_radius_forward_backward(lib, kind, n, r, F):
+    pos = cloud(kind, n, n + F)
+    x = synth.normal_f32(n * F, (82, n, F)).reshape(n, F)
+    dy = synth.normal_f32(n * F, (83, n, F)).reshape(n, F)
+    r = np.float32(r)
+    s = np.float32(r / 2)
+    y, cnt = lib.tiga_mp_radius_fwd(dev(pos), dev(x), r, s)
+    ry, rya, rcnt = oracle.radius_fwd(pos, x, r, s)
+    assert np.array_equal(host(cnt), rcnt)
+    assert_terms_close(host(y), ry, rya, what=f"radius y {kind}")
+    dx, dp = lib.tiga_mp_radius_bwd(dev(pos), dev(x), dev(dy), r, s)
+    rdx, rdxa, rdp, rdpa = oracle.radius_bwd(pos, x, dy, r, s)
+    assert_terms_close(host(dx), rdx, rdxa, what=f"radius dx {kind}")
+    assert_terms_close(host(dp), rdp, rdpa, what=f"radius dpos {kind}")
+    # partial requests
+    dx2, none = lib.tiga_mp_radius_bwd(dev(pos), dev(x), dev(dy), r, s, want_dpos=False)
+    assert none is None and np.array_equal(host(dx2), host(dx))
+
+
+@pytest.mark.parametrize("kind,n,r", [("uniform", 4000, 0.06), ("grid", 3000, 0.09), ("cluster", 2500, 0.03)])
+def test_radius_neighbour_lists_exact(lib, kind, n, r):
+    pos = cloud(kind, n, 7)
+    cnt, ptr, idx = lib.tiga_radius_neighbors(dev(pos), r)
+    rptr, ridx = oracle.radius_neighbors(pos, r)
+    assert np.array_equal(host(ptr), rptr)
+    assert np.array_equal(host(idx), ridx)
+    assert np.array_equal(host(cnt), np.diff(rptr))
+
+
+def test_radius_deterministic(lib):
+    pos = cloud("uniform", 20000, 3)
+    x = synth.normal_f32(20000 * 8, (84,)).reshape(20000, 8)
+    a, _ = lib.tiga_mp_radius_fwd(dev(pos), dev(x), 0.03, 0.015)
+    b, _ = lib.tiga_mp_radius_fwd(dev(pos), dev(x), 0.03, 0.015)
+    assert torch.equal(a, b)
+
+
+def test_radius_rejects_max(lib):
+    pos = dev(cloud("uniform", 10, 1))
+    x = dev(np.ones((10, 4), np.float32))
+    with pytest.raises(lib.TigaError) as e:
+        y = torch.empty(10, 4, device="cuda")
+        ws = torch.empty(lib.load().tiga_mp_radius_workspace(10, 4), dtype=torch.uint8, device="cuda")
+        lib._check(lib.load().tiga_mp_radius_fwd(10, 4, lib._ptr(pos), lib._ptr(x), 0.1, 0.05, lib.REDUCE_MAX,
+                                                 lib._ptr(y), None, lib._ptr(ws), ws.numel(), lib._stream()))
+    assert e.value.code == lib.TIGA_EUNSUPPORTED
+
+
+def test_config3_full_size_sampled(lib):
+    g = synth.config3()
+    pos, x, dy, r, s = g["pos"], g["x"], g["dy"], g["radius"], g["sigma"]
+    pd, xd, dyd = dev(pos), dev(x), dev(dy)
+    y, cnt = lib.tiga_mp_radius_fwd(pd, xd, r, s)
+    pts = np.unique(np.random.default_rng(4).integers(0, pos.shape[0], 4000))
+    ry, rya, rcnt = oracle.radius_fwd(pos, x, r, s, pts=pts)
+    assert np.array_equal(host(cnt)[pts], rcnt)
+    assert_terms_close(host(y)[pts], ry, rya, what="config 3 y")
+    dx, dp = lib.tiga_mp_radius_bwd(pd, xd, dyd, r, s)
+    rdx, rdxa, rdp, rdpa = oracle.radius_bwd(pos, x, dy, r, s, pts=pts)
+    assert_terms_close(host(dx)[pts], rdx, rdxa, what="config 3 dx")
+    assert_terms_close(host(dp)[pts], rdp, rdpa, what="config 3 dpos")
+    # symmetric relation: the directed pair count is even; mean degree near 32
+    total = int(host(cnt).astype(np.int64).sum())
+    assert total % 2 == 0 and abs(total / pos.shape[0] - 31.3) < 0.3
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 255, 256, 257, 1000, 5003])
+def test_dense_small(lib, n):
+    g = synth.config4(n=n)
+    y = lib.tiga_mp_dense_fwd(dev(g["pos"]), dev(g["q"]), g["eps"])
+    ry, rya = oracle.dense_fwd(g["pos"], g["q"], g["eps"])
+    assert_terms_close(host(y), ry, rya, what=f"dense n={n}")
+
+
+def test_dense_same_sign_adversarial(lib):
+    # a far particle sees nearly parallel, same-sign terms from all others
+    n = 20000
+    rng = np.random.default_rng(8)
+    pos = rng.normal(0, 0.1, (n, 3)).astype(np.float32)
+    pos[0] = [50.0, 0.0, 0.0]
+    q = rng.uniform(0.5, 1.5, n).astype(np.float32)
+    y = lib.tiga_mp_dense_fwd(dev(pos), dev(q), np.float32(1e-2))
+    ry, rya = oracle.dense_fwd(pos, q, np.float32(1e-2), pts=np.array([0, 1, n - 1]))
+    assert_terms_close(host(y)[[0, 1, n - 1]], ry, rya, what="dense same-sign")
+
+
+def test_config4_full_size_sampled(lib):
+    g = synth.config4()
+    y = lib.tiga_mp_dense_fwd(dev(g["pos"]), dev(g["q"]), g["eps"])
+    pts = np.unique(np.random.default_rng(6).integers(0, 65536, 1500))
+    ry, rya = oracle.dense_fwd(g["pos"], g["q"], g["eps"], pts=pts)
+    assert_terms_close(host(y)[pts], ry, rya, what="config 4 y")
