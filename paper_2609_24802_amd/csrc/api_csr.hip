@@ -72,9 +72,9 @@ int tiga_mp_csr_fwd(const tiga_csr *rel, int32_t feat, const float *x_src, int m
     if (int rc = check_ws(ws, ws_bytes, need)) return rc;
     const bool vec = feat % 4 == 0 && aligned16(x_src) && aligned16(y) && (!argmax || aligned16(argmax));
     const Layout lay = layout_for(feat, vec);
-    Trav t{rel->row_ptr, rel->col_idx, w_edge, nullptr, x_src, rel->num_dst, lay.fu};
+    Trav t{rel->row_ptr, rel->col_idx, w_edge, nullptr, x_src, rel->num_dst, lay.fu, nullptr, 0u, rel->num_edges};
     const int wm = msg == TIGA_MSG_EDGE_SCALED_SRC ? W_DIRECT : W_NONE;
-    return launch_traversal(t, rel->num_edges, lay, reducer == TIGA_REDUCE_MAX ? RED_MAX : RED_SUM, wm, ws, y,
+    return launch_traversal(t, rel->num_src, rel->num_edges, lay, reducer == TIGA_REDUCE_MAX ? RED_MAX : RED_SUM, wm, ws, y,
                             argmax, static_cast<hipStream_t>(stream));
 }
 

@@ -36,6 +36,9 @@ inline int check_launch(const char *what) { return check_hip(hipGetLastError(), 
 // Number of compute units of the current device (cached per device).
 int device_cus();
 
+// Blocks of `block` threads of `kernel` that fit on one compute unit (>= 1).
+int resident_blocks(const void *kernel, int block);
+
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 

@@ -85,40 +85,26 @@ __device__ __forceinline__ void edge_pass(const EdgeT &t, int64_t row, int64_t e
 }
 
 template <int K, int L, int RED, bool DW, bool DX>
-__global__ __launch_bounds__(kBlock) void edge_kernel(EdgeT t, int64_t n_groups, const Desc *__restrict__ chunks,
-                                                      const PlanCounts *__restrict__ counts) {
-    constexpr Geom g = make_geom(L);
-    const int lane = lane_id();
-    const int64_t wave = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
-    const int64_t nwaves = static_cast<int64_t>(gridDim.x) * kWavesPerBlock;
-    const int64_t n_chunks = static_cast<int64_t>(counts->chunks);
-    const int64_t total = n_chunks + n_groups;
-    const int l = lane % L;
-    for (int64_t it = wave; it < total; it += nwaves) {
-        if (it < n_chunks) {
-            const Desc d = chunks[it];
-            const int64_t row = d.x;
-            const int64_t re = t.ptr[row + 1];
-            const int64_t e0 = t.ptr[row] + static_cast<int64_t>(d.y) * g.CH;
-            const int64_t e1 = (re < e0 + g.CH) ? re : e0 + g.CH;
-            for (int64_t fb = 0; fb < t.fu; fb += L) {
-                const int64_t u = fb + l;
-                edge_pass<K, L, RED, DW, DX, g.S>(t, row, e0, e1, lane / L, l, u, u < t.fu, fb == 0);
-            }
-        } else {
-            const int64_t row = (it - n_chunks) * g.RPW + lane / g.G;
-            int64_t e0 = 0, e1 = 0;
-            if (row < t.nrows) {
-                e0 = t.ptr[row];
-                e1 = t.ptr[row + 1];
-                if (e1 - e0 > g.DS) e1 = e0;
-            }
-            for (int64_t fb = 0; fb < t.fu; fb += L) {
-                const int64_t u = fb + l;
-                edge_pass<K, L, RED, DW, DX, g.P>(t, row, e0, e1, (lane % g.G) / L, l, u, u < t.fu, fb == 0);
-            }
+struct EdgeBody {
+    const EdgeT &t;
+
+    template <int GL>
+    __device__ __forceinline__ void run(const Meta &m, int glane) {
+        const int l = glane % L;
+        for (int64_t fb = 0; fb < t.fu; fb += L) {
+            const int64_t u = fb + l;
+            edge_pass<K, L, RED, DW, DX, GL / L>(t, m.row, m.e0, m.e0 + m.n, glane / L, l, u, u < t.fu, fb == 0);
         }
     }
+
+};
+
+template <int K, int L, int RED, bool DW, bool DX>
+__global__ __launch_bounds__(kBlock) void edge_kernel(EdgeT t, int64_t n_groups, const Desc *__restrict__ chunks,
+                                                      const PlanCounts *__restrict__ counts) {
+    EdgeBody<K, L, RED, DW, DX> body{t};
+    const Items items = make_items(counts, n_groups);
+    for_each_item<L>(items, chunks, t.ptr, t.nrows, body);
 }
 
 template <int K, int L, int RED, bool DW, bool DX>
@@ -129,10 +115,11 @@ int launch_edge_t(const EdgeT &t, int64_t nedges, void *ws, hipStream_t stream) 
     const PlanWs w = carve_plan(c, b, t.fu * K, false);
     if (int rc = launch_plan(t.ptr, t.nrows, g, b, w, stream)) return rc;
     const int64_t n_groups = ceil_div(t.nrows, g.RPW);
-    const int blocks = persistent_blocks(n_groups + b.max_chunks);
+    auto kern = edge_kernel<K, L, RED, DW, DX>;
+    static const int per_cu = resident_blocks(reinterpret_cast<const void *>(kern), kBlock);
+    const int blocks = persistent_blocks(n_groups + b.max_chunks, per_cu);
     prof_before(stream);
-    hipLaunchKernelGGL((edge_kernel<K, L, RED, DW, DX>), dim3(blocks), dim3(kBlock), 0, stream, t, n_groups,
-                       w.chunks, w.counts);
+    hipLaunchKernelGGL(kern, dim3(blocks), dim3(kBlock), 0, stream, t, n_groups, w.chunks, w.counts);
     prof_after(stream);
     return check_launch("edge backward");
 }
@@ -191,9 +178,11 @@ int launch_bwd(const BwdArgs &a, void *ws, hipStream_t stream) {
         if (rc) return rc;
     }
     if (a.dx && a.rev && rel->num_src > 0) {
-        Trav t{a.rev->src_ptr, a.rev->dst_idx, a.w, a.rev->edge_id, a.dy, rel->num_src, lay.fu, a.arg};
+        Trav t{a.rev->src_ptr, a.rev->dst_idx, a.w, a.rev->edge_id, a.dy, rel->num_src, lay.fu, a.arg, 0u,
+               rel->num_edges};
         const int wm = a.red == RED_MAX ? W_ROUTE : W_INDIRECT;
-        if (int rc = launch_traversal(t, rel->num_edges, lay, RED_SUM, wm, ws, a.dx, nullptr, stream)) return rc;
+        if (int rc = launch_traversal(t, rel->num_dst, rel->num_edges, lay, RED_SUM, wm, ws, a.dx, nullptr, stream))
+            return rc;
     }
     return TIGA_OK;
 }

@@ -1,22 +1,25 @@
 // Degree-aware traversal of a destination-major CSR relation on gfx950.
 //
-// The relation's rows are split into three classes by degree (Section 4.4 of
-// the paper: a bounded neighbour tile needs a degree guard; a high-degree row
-// needs explicit partial states and a legal merge):
-//   short rows  (deg <= DS): one group of G lanes per row, rows taken in their
-//                            natural order, RPW rows per wavefront;
-//   medium rows (DS < deg <= CH): one wavefront per row;
-//   long rows   (deg > CH): split into chunks of CH edges, one wavefront per
-//                           chunk, each producing a partial state that a
-//                           merge kernel combines in a fixed order.
-// Medium and long rows are both described by chunk descriptors, produced by a
-// deterministic plan (count per tile, scan, write) without global atomics.
+// Rows are split by degree (Section 4.4 of the paper: a bounded neighbour
+// tile needs a degree guard; a high-degree row needs explicit partial states
+// and a legal merge):
+//   short rows (deg <= DS): taken in their natural order, one group of G lanes
+//                           per row, RPW rows per wavefront (no plan entry);
+//   other rows:             cut into chunks of at most CH edges.  A chunk is
+//                           processed by a group of 64, 32 or 16 lanes chosen
+//                           by its length (its "class"), so a wavefront holds
+//                           one long chunk or several short ones.  A row of
+//                           several chunks writes partial states that a merge
+//                           kernel combines in chunk order.
+// Chunk descriptors come from a deterministic plan (count per tile, scan,
+// write) without global atomics; each carries its edge range, so a work item
+// needs no dependent row-pointer load.
 //
 // Lane layout: a feature row is FU "units" (float4 when the vector path
 // applies, else float).  L lanes (a power of two >= FU, at most 64) cover one
-// edge's units, so a wavefront holds S = 64 / L edge slots.  Each lane
+// edge's units, so a group of GL lanes holds GL / L edge slots.  Each lane
 // accumulates its slot's edges serially (kUnroll edges in flight), then the
-// slots of a row are reduced with cross-lane shuffles.
+// slots of a group are reduced with cross-lane shuffles.
 #pragma once
 
 #include "common.hpp"
@@ -34,6 +37,10 @@ constexpr int kBlock = 256;        // threads per block of the traversal kernels
 constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kPlanRowsPerThread = 8;
 constexpr int kPlanTile = kBlock * kPlanRowsPerThread;
+constexpr int kClasses = 3;        // chunk groups of 64, 32 and 16 lanes
+constexpr int kPlanVals = kClasses + 2;  // per tile: chunks of each class, partial slots, split rows
+
+__host__ __device__ constexpr int class_lanes(int c) { return c == 0 ? 64 : (c == 1 ? 32 : 16); }
 
 struct Geom {
     int L;    // lanes per edge
@@ -42,27 +49,59 @@ struct Geom {
     int G;    // lanes per short-row group
     int RPW;  // short rows per wavefront
     int DS;   // short-row degree bound
-    int CH;   // chunk length (edges) for medium and long rows
+    int CH;   // chunk length (edges)
+    int nclass;           // chunk classes whose group holds at least one edge
+    int cap[kClasses];    // longest chunk of each class (about four steps of its group)
 };
 
 __host__ __device__ constexpr Geom make_geom(int L) {
+    const int P = L >= 8 ? 1 : 8 / L;
+    const int nclass = L <= 16 ? 3 : (L <= 32 ? 2 : 1);
     return Geom{L,
                 kWave / L,
-                L >= 8 ? 1 : 8 / L,
+                P,
                 L >= 8 ? L : 8,
                 kWave / (L >= 8 ? L : 8),
-                2 * (L >= 8 ? 1 : 8 / L) * kUnroll,
-                (kWave / L) * kUnroll * 16};
+                2 * P * kUnroll,
+                (kWave / L) * kUnroll * 16,
+                nclass,
+                {(kWave / L) * kUnroll * 16, 4 * (32 / L > 0 ? 32 / L : 1) * kUnroll,
+                 4 * (16 / L > 0 ? 16 / L : 1) * kUnroll}};
 }
 
-// Chunk descriptor: row, chunk index within the row, partial slot (-1 when
-// the row is a single chunk and writes its output directly), chunks in row.
-// Split descriptor: row, first partial slot, chunk count, unused.
-using Desc = int4;
+// Class of a chunk of n edges: the narrowest group that finishes it in about
+// four steps.
+__host__ __device__ constexpr int chunk_class(const Geom &g, int64_t n) {
+    return (g.nclass > 2 && n <= g.cap[2]) ? 2 : ((g.nclass > 1 && n <= g.cap[1]) ? 1 : 0);
+}
 
-// Counters written by the plan: [0] chunks, [1] partial slots, [2] split rows.
+// Chunk descriptor: destination row, partial slot (-1 when the row is one
+// chunk and writes its output directly) and the edge range packed as
+// (first edge << 24) | length.
+struct alignas(16) Desc {
+    int32_t row;
+    int32_t slot;
+    uint64_t range;
+};
+constexpr int kRangeBits = 24;
+__host__ __device__ inline uint64_t pack_range(int64_t e0, int64_t n) {
+    return (static_cast<uint64_t>(e0) << kRangeBits) | static_cast<uint64_t>(n);
+}
+
+// Split row: row, first partial slot, chunk count.
+struct alignas(16) Split {
+    int32_t row;
+    int32_t slot0;
+    int32_t nch;
+    int32_t pad;
+};
+
+// Written by the plan: chunks of each class (stored class after class),
+// partial slots, split rows.
 struct PlanCounts {
-    unsigned long long chunks, slots, splits, pad;
+    unsigned long long cls[kClasses];
+    unsigned long long slots, splits;
+    unsigned long long pad[3];
 };
 
 struct PlanBounds {
@@ -84,9 +123,9 @@ inline PlanBounds plan_bounds(int64_t nrows, int64_t nedges, const Geom &g) {
 // max) per slot.
 struct PlanWs {
     PlanCounts *counts;
-    int64_t *tile_vals;  // 3 per tile: chunks, slots, splits (count, then offset)
+    int64_t *tile_vals;  // kPlanVals per tile (counts, then offsets)
     Desc *chunks;
-    Desc *splits;
+    Split *splits;
     float *part_v;
     int32_t *part_e;
 };
@@ -94,9 +133,9 @@ struct PlanWs {
 inline PlanWs carve_plan(Carve &c, const PlanBounds &b, int64_t feat, bool with_arg) {
     PlanWs w;
     w.counts = c.take<PlanCounts>(1);
-    w.tile_vals = c.take<int64_t>(3 * b.tiles);
+    w.tile_vals = c.take<int64_t>(kPlanVals * b.tiles);
     w.chunks = c.take<Desc>(b.max_chunks);
-    w.splits = c.take<Desc>(b.max_splits);
+    w.splits = c.take<Split>(b.max_splits);
     w.part_v = c.take<float>(b.max_slots * feat);
     w.part_e = with_arg ? c.take<int32_t>(b.max_slots * feat) : nullptr;
     return w;
@@ -216,14 +255,12 @@ struct Acc<K, RED_MAX> {
     }
     // message = one fp32 product; strict '>' keeps the earliest edge of a lane
     __device__ __forceinline__ void add(float w, const Vec<K> &x, int64_t edge, bool ok) {
-        if (!ok) return;
 #pragma unroll
         for (int k = 0; k < K; ++k) {
-            float m = w * x.v[k];
-            if (m > v[k] || e[k] == kNoEdge) {
-                v[k] = m;
-                e[k] = static_cast<int>(edge);
-            }
+            const float m = w * x.v[k];
+            const bool take = ok && (m > v[k] || e[k] == kNoEdge);
+            v[k] = take ? m : v[k];
+            e[k] = take ? static_cast<int>(edge) : e[k];
         }
     }
     __device__ __forceinline__ void take(float ov, int oe, int k) {
@@ -273,45 +310,122 @@ struct Trav {
     int64_t nrows;
     int64_t fu;                        // feature units per row
     const int32_t *__restrict__ arg;   // [*, feat] selected edges (W_ROUTE only)
+    uint32_t table_bytes;              // byte size of `table` (and `arg`) when below 4 GiB, else 0
+    int64_t nedges;                    // edges of the relation (idx, w and eid have this many)
+};
+
+// Row gathers from the feature table.  Tables below 4 GiB go through a buffer
+// resource: 32-bit byte offsets (fewer address registers) and a load outside
+// the table returns zero rather than faulting.  Larger tables use 64-bit
+// global loads.  Either way the load carries the non-temporal hint: a
+// random row is rarely reused before it would be evicted.
+constexpr int kBufWord3 = 0x00020000;  // raw buffer, 32-bit data format (gfx9)
+constexpr int kPolicyNT = 2;
+// Tables above this size are streamed with the non-temporal hint; smaller ones
+// stay eligible for the caches (a table that fits the 256 MB last-level cache
+// is re-read from it).
+constexpr int64_t kStreamTableBytes = int64_t{1} << 30;
+
+template <int K, bool BUF, bool NT = true>
+struct Table {
+    __amdgpu_buffer_rsrc_t rs;
+    const float *base;
+    uint32_t row_bytes;
+    __device__ __forceinline__ Table(const float *p, int64_t fu, uint32_t bytes) : base(p) {
+        row_bytes = static_cast<uint32_t>(fu * K * 4);
+        if constexpr (BUF) rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(p), 0, bytes, kBufWord3);
+    }
+    __device__ __forceinline__ Vec<K> load(int32_t row, int64_t u, int64_t fu) const {
+        Vec<K> r;
+        if constexpr (BUF) {
+            const int off = static_cast<int>(static_cast<uint32_t>(row) * row_bytes + static_cast<uint32_t>(u) * (K * 4));
+            if constexpr (K == 4) {
+                const f32x4 t =
+                    __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, NT ? kPolicyNT : 0));
+                r.v[0] = t.x;
+                r.v[1] = t.y;
+                r.v[2] = t.z;
+                r.v[3] = t.w;
+            } else {
+                r.v[0] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, NT ? kPolicyNT : 0));
+            }
+        } else {
+            // callers pass a valid row; padding units read the row's first unit
+            const int64_t unit = static_cast<int64_t>(row) * fu + (u < fu ? u : 0);
+            if constexpr (K == 4) {
+                const f32x4 t = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(base) + unit);
+                r.v[0] = t.x;
+                r.v[1] = t.y;
+                r.v[2] = t.z;
+                r.v[3] = t.w;
+            } else {
+                r.v[0] = __builtin_nontemporal_load(base + unit);
+            }
+        }
+        return r;
+    }
+    // the same row of an int32 table with identical shape (argmax)
+    __device__ __forceinline__ void load_i(const int32_t *ib, const __amdgpu_buffer_rsrc_t &irs, int32_t row,
+                                           int64_t u, int64_t fu, int (&out)[K]) const {
+        if constexpr (BUF) {
+            const int off = static_cast<int>(static_cast<uint32_t>(row) * row_bytes + static_cast<uint32_t>(u) * (K * 4));
+            if constexpr (K == 4) {
+                const i32x4 t = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(irs, off, 0, 0));
+                out[0] = t.x;
+                out[1] = t.y;
+                out[2] = t.z;
+                out[3] = t.w;
+            } else {
+                out[0] = __builtin_bit_cast(int, __builtin_amdgcn_raw_buffer_load_b32(irs, off, 0, 0));
+            }
+        } else {
+            load_unit_i<K>(ib, static_cast<int64_t>(row) * fu + (u < fu ? u : 0), out);
+        }
+    }
 };
 
 // Fold the edges [e0, e1) of one row into `acc`; this lane is slot `s` of SL
-// slots and covers feature unit `u` (`uok` false for padding lanes).
-template <int K, int RED, int WM, int SL, class A>
-__device__ __forceinline__ void run_edges(const Trav &t, int64_t e0, int64_t e1, int s, int64_t u,
-                                          bool uok, A &acc) {
+// slots and covers feature unit `u` (`uok` false for padding lanes).  The
+// lane issues kUnroll independent row gathers per step; latency is hidden by
+// the other resident wavefronts.  Offsets inside the row are 32-bit (a row
+// piece is at most one chunk of edges).  Lanes past the row's end issue no
+// loads at all (their exec bit is off).
+template <int K, int RED, int WM, int SL, bool BUF, bool NT, class A>
+__device__ __forceinline__ void run_edges(const Trav &t, const Table<K, BUF, NT> &tab,
+                                          const __amdgpu_buffer_rsrc_t &ars, int64_t e0, int64_t e1, int s,
+                                          int64_t u, bool uok, A &acc) {
     constexpr int STEP = SL * kUnroll;
-    int32_t c[kUnroll];
-    int32_t ee[kUnroll];
-    float wv[kUnroll];
-    auto fetch = [&](int64_t b, int32_t(&cc)[kUnroll], int32_t(&ei)[kUnroll], float(&ww)[kUnroll]) {
+    const int n = static_cast<int>(e1 - e0);
+    const int32_t *__restrict__ colr = t.idx + e0;
+    const float *__restrict__ wr = t.w + e0;
+    const int32_t *__restrict__ er = t.eid + e0;
+    for (int k0 = 0; k0 < n; k0 += STEP) {
+        int32_t c[kUnroll];
+        int32_t ee[kUnroll];
+        float wv[kUnroll];
+        bool ok[kUnroll];
 #pragma unroll
         for (int r = 0; r < kUnroll; ++r) {
-            const int64_t e = b + static_cast<int64_t>(r) * SL + s;
-            const bool ok = e < e1;
-            cc[r] = ok ? ldg_stream(t.idx + e) : -1;
-            ei[r] = 0;
+            const int k = k0 + r * SL + s;
+            ok[r] = k < n;
+            c[r] = ok[r] ? ldg_stream(colr + k) : 0;
+            ee[r] = 0;
             if constexpr (WM == W_DIRECT) {
-                ww[r] = ok ? ldg_stream(t.w + e) : 0.0f;
+                wv[r] = ok[r] ? ldg_stream(wr + k) : 0.0f;
             } else if constexpr (WM == W_INDIRECT || WM == W_ROUTE) {
-                ei[r] = ok ? ldg_stream(t.eid + e) : 0;
-                ww[r] = ok ? (t.w ? t.w[ei[r]] : 1.0f) : 0.0f;
+                ee[r] = ok[r] ? ldg_stream(er + k) : 0;
+                wv[r] = ok[r] ? (t.w ? t.w[ee[r]] : 1.0f) : 0.0f;
             } else {
-                ww[r] = ok ? 1.0f : 0.0f;
+                wv[r] = ok[r] ? 1.0f : 0.0f;
             }
         }
-    };
-    int64_t base = e0;
-    if (base < e1) fetch(base, c, ee, wv);
-    for (; base < e1; base += STEP) {
         Vec<K> xv[kUnroll];
         int sel[kUnroll][K];
 #pragma unroll
         for (int r = 0; r < kUnroll; ++r) {
-            if (c[r] >= 0 && uok) {
-                const int64_t unit = static_cast<int64_t>(c[r]) * t.fu + u;
-                xv[r] = load_unit<K>(t.table, unit);
-                if constexpr (WM == W_ROUTE) load_unit_i<K>(t.arg, unit, sel[r]);
+            if (ok[r] && uok) {
+                xv[r] = tab.load(c[r], u, t.fu);
+                if constexpr (WM == W_ROUTE) tab.load_i(t.arg, ars, c[r], u, t.fu, sel[r]);
             } else {
 #pragma unroll
                 for (int k = 0; k < K; ++k) {
@@ -320,37 +434,125 @@ __device__ __forceinline__ void run_edges(const Trav &t, int64_t e0, int64_t e1,
                 }
             }
         }
-        int32_t cn[kUnroll];
-        int32_t en[kUnroll];
-        float wn[kUnroll];
-        const int64_t nb = base + STEP;
-        if (nb < e1) {
-            fetch(nb, cn, en, wn);
-        } else {
-#pragma unroll
-            for (int r = 0; r < kUnroll; ++r) {
-                cn[r] = -1;
-                en[r] = 0;
-                wn[r] = 0.0f;
-            }
-        }
-        if constexpr (WM == W_ROUTE) {
-            // only the (row, feature) entries whose argmax is this edge receive its message
-#pragma unroll
-            for (int r = 0; r < kUnroll; ++r)
-#pragma unroll
-                for (int k = 0; k < K; ++k)
-                    if (sel[r][k] != ee[r]) xv[r].v[k] = 0.0f;
-        }
-#pragma unroll
-        for (int r = 0; r < kUnroll; ++r)
-            acc.add(wv[r], xv[r], base + static_cast<int64_t>(r) * SL + s, c[r] >= 0);
 #pragma unroll
         for (int r = 0; r < kUnroll; ++r) {
-            c[r] = cn[r];
-            ee[r] = en[r];
-            wv[r] = wn[r];
+            const bool live = ok[r] && uok;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                bool keep = live;
+                if constexpr (WM == W_ROUTE) keep = keep && sel[r][k] == ee[r];
+                xv[r].v[k] = keep ? xv[r].v[k] : 0.0f;
+            }
+            acc.add(wv[r], xv[r], e0 + k0 + r * SL + s, live);
         }
+    }
+}
+
+// Work items of one traversal, in this order: class-0 chunks (one per
+// wavefront), pairs of class-1 chunks, quadruples of class-2 chunks, then
+// groups of RPW short rows in natural order.
+struct Items {
+    int64_t n0, n1, n2;      // chunks of each class
+    int64_t b1, b2;          // first descriptor of classes 1 and 2 (class 0 starts at 0)
+    int64_t s1, s2, s3;      // first item of classes 1, 2 and of the short-row groups
+    int64_t total;
+};
+
+__device__ __forceinline__ Items make_items(const PlanCounts *__restrict__ pc, int64_t n_groups) {
+    Items it;
+    it.n0 = static_cast<int64_t>(pc->cls[0]);
+    it.n1 = static_cast<int64_t>(pc->cls[1]);
+    it.n2 = static_cast<int64_t>(pc->cls[2]);
+    it.b1 = it.n0;
+    it.b2 = it.n0 + it.n1;
+    it.s1 = it.n0;
+    it.s2 = it.s1 + (it.n1 + 1) / 2;
+    it.s3 = it.s2 + (it.n2 + 3) / 4;
+    it.total = it.s3 + n_groups;
+    return it;
+}
+
+// What one group needs to process its part of a work item: the edge range,
+// the output row, the partial slot (-1: write the output row) and whether it
+// writes at all (padding groups and skipped rows do not).
+struct Meta {
+    int64_t e0;
+    int32_t n;
+    int32_t row;
+    int32_t slot;
+    int32_t write;
+};
+
+// Metadata of item `it` for this lane (class-c chunk items and short-row
+// groups; see Items).  Geometry: L lanes per edge.
+template <int L>
+__device__ __forceinline__ Meta load_meta(const Items &items, const Desc *__restrict__ chunks,
+                                          const int64_t *__restrict__ ptr, int64_t nrows, int64_t it, int lane) {
+    constexpr Geom g = make_geom(L);
+    Meta m{0, 0, 0, -1, 0};
+    if (it >= items.total) return m;
+    int64_t j = -1, nj = 0;
+    if (it < items.s1) {
+        j = it;
+        nj = items.n0;
+    } else if (it < items.s2) {
+        const int64_t k = (it - items.s1) * 2 + lane / 32;
+        j = items.b1 + k;
+        nj = items.b1 + items.n1;
+    } else if (it < items.s3) {
+        const int64_t k = (it - items.s2) * 4 + lane / 16;
+        j = items.b2 + k;
+        nj = items.b2 + items.n2;
+    } else {
+        const int64_t row = (it - items.s3) * g.RPW + lane / g.G;
+        if (row < nrows) {
+            const int64_t e0 = ptr[row];
+            const int64_t d = ptr[row + 1] - e0;
+            if (d <= g.DS) {
+                m.e0 = e0;
+                m.n = static_cast<int32_t>(d);
+                m.row = static_cast<int32_t>(row);
+                m.write = 1;
+            }
+        }
+        return m;
+    }
+    if (j < nj) {
+        const Desc d = chunks[j];
+        m.e0 = static_cast<int64_t>(d.range >> kRangeBits);
+        m.n = static_cast<int32_t>(d.range & ((1u << kRangeBits) - 1));
+        m.row = d.row;
+        m.slot = d.slot;
+        m.write = 1;
+    }
+    return m;
+}
+
+// Persistent loop: wavefront w takes items w, w + nwaves, ...; every
+// wavefront leaves once it passes the item count, so the grid drains.  The
+// next item's metadata is loaded before the current item is processed, so its
+// latency hides behind the current item's gathers.
+// Body provides  template <int GL> run(const Meta&, int lane_in_group).
+template <int L, class Body>
+__device__ __forceinline__ void for_each_item(const Items &items, const Desc *__restrict__ chunks,
+                                              const int64_t *__restrict__ ptr, int64_t nrows, Body &body) {
+    constexpr Geom g = make_geom(L);
+    const int lane = lane_id();
+    const int64_t wave = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
+    const int64_t nwaves = static_cast<int64_t>(gridDim.x) * kWavesPerBlock;
+    Meta cur = load_meta<L>(items, chunks, ptr, nrows, wave, lane);
+    for (int64_t it = wave; it < items.total; it += nwaves) {
+        const Meta nxt = load_meta<L>(items, chunks, ptr, nrows, it + nwaves, lane);
+        if (it < items.s1) {
+            body.template run<64>(cur, lane);
+        } else if (it < items.s2) {
+            if constexpr (32 >= L) body.template run<32>(cur, lane % 32);
+        } else if (it < items.s3) {
+            if constexpr (16 >= L) body.template run<16>(cur, lane % 16);
+        } else {
+            body.template run<g.G>(cur, lane % g.G);
+        }
+        cur = nxt;
     }
 }
 

@@ -7,10 +7,47 @@ namespace csr {
 
 namespace {
 
-// Persistent traversal: work items are [chunk descriptors | short-row groups];
-// each wavefront takes items it, it + nwaves, ...  Every wavefront leaves the
-// loop once `it` passes the item count, so the grid always drains.
-template <int K, int L, int RED, int WM>
+// Fold one chunk (or short row) per group, reduce the group's slots, and
+// write the finalized output row or the chunk's partial state.
+template <int K, int L, int RED, int WM, bool BUF, bool NT>
+struct GatherBody {
+    const Trav &t;
+    const Table<K, BUF, NT> &tab;
+    const __amdgpu_buffer_rsrc_t &ars;
+    float *__restrict__ out;
+    int32_t *__restrict__ out_arg;
+    float *__restrict__ part_v;
+    int32_t *__restrict__ part_e;
+
+    template <int GL>
+    __device__ __forceinline__ void run(const Meta &m, int glane) {
+        using A = Acc<K, RED>;
+        const int s = glane / L;
+        const int l = glane % L;
+        for (int64_t fb = 0; fb < t.fu; fb += L) {
+            const int64_t u = fb + l;
+            const bool uok = u < t.fu;
+            A acc;
+            acc.init();
+            run_edges<K, RED, WM, GL / L, BUF, NT>(t, tab, ars, m.e0, m.e0 + m.n, s, u, uok, acc);
+            reduce_lanes<L, GL>(acc);
+            if (m.write && s == 0 && uok) {
+                if (m.slot < 0) {
+                    acc.finalize();
+                    const int64_t unit = static_cast<int64_t>(m.row) * t.fu + u;
+                    store_unit<K>(out, unit, acc.v);
+                    if constexpr (RED == RED_MAX) store_unit_i<K>(out_arg, unit, acc.e);
+                } else {
+                    const int64_t unit = static_cast<int64_t>(m.slot) * t.fu + u;
+                    store_unit<K>(part_v, unit, acc.v);
+                    if constexpr (RED == RED_MAX) store_unit_i<K>(part_e, unit, acc.e);
+                }
+            }
+        }
+    }
+};
+
+template <int K, int L, int RED, int WM, bool BUF, bool NT>
 __global__ __launch_bounds__(kBlock) void gather_reduce_kernel(Trav t, int64_t n_groups,
                                                                const Desc *__restrict__ chunks,
                                                                const PlanCounts *__restrict__ counts,
@@ -18,79 +55,19 @@ __global__ __launch_bounds__(kBlock) void gather_reduce_kernel(Trav t, int64_t n
                                                                int32_t *__restrict__ out_arg,
                                                                float *__restrict__ part_v,
                                                                int32_t *__restrict__ part_e) {
-    constexpr Geom g = make_geom(L);
-    using A = Acc<K, RED>;
-    const int lane = lane_id();
-    const int64_t wave = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
-    const int64_t nwaves = static_cast<int64_t>(gridDim.x) * kWavesPerBlock;
-    const int64_t n_chunks = static_cast<int64_t>(counts->chunks);
-    const int64_t total = n_chunks + n_groups;
-    const int l = lane % L;
-
-    for (int64_t it = wave; it < total; it += nwaves) {
-        if (it < n_chunks) {
-            // one wavefront over up to CH edges of a medium or long row
-            const Desc d = chunks[it];
-            const int64_t row = d.x;
-            const int64_t rb = t.ptr[row];
-            const int64_t re = t.ptr[row + 1];
-            const int64_t e0 = rb + static_cast<int64_t>(d.y) * g.CH;
-            const int64_t e1 = (re < e0 + g.CH) ? re : e0 + g.CH;
-            const int s = lane / L;
-            for (int64_t fb = 0; fb < t.fu; fb += L) {
-                const int64_t u = fb + l;
-                const bool uok = u < t.fu;
-                A acc;
-                acc.init();
-                run_edges<K, RED, WM, g.S>(t, e0, e1, s, u, uok, acc);
-                reduce_lanes<L, kWave>(acc);
-                if (s == 0 && uok) {
-                    if (d.z < 0) {
-                        acc.finalize();
-                        store_unit<K>(out, row * t.fu + u, acc.v);
-                        if constexpr (RED == RED_MAX) store_unit_i<K>(out_arg, row * t.fu + u, acc.e);
-                    } else {
-                        const int64_t slot = d.z;
-                        store_unit<K>(part_v, slot * t.fu + u, acc.v);
-                        if constexpr (RED == RED_MAX) store_unit_i<K>(part_e, slot * t.fu + u, acc.e);
-                    }
-                }
-            }
-        } else {
-            // RPW short rows in natural order, one group of G lanes each
-            const int64_t gi = it - n_chunks;
-            const int grp = lane / g.G;
-            const int s = (lane % g.G) / L;
-            const int64_t row = gi * g.RPW + grp;
-            int64_t e0 = 0, e1 = 0;
-            bool mine = false;
-            if (row < t.nrows) {
-                e0 = t.ptr[row];
-                e1 = t.ptr[row + 1];
-                mine = (e1 - e0) <= g.DS;
-            }
-            if (!mine) e1 = e0;  // medium and long rows belong to chunk items
-            for (int64_t fb = 0; fb < t.fu; fb += L) {
-                const int64_t u = fb + l;
-                const bool uok = u < t.fu;
-                A acc;
-                acc.init();
-                run_edges<K, RED, WM, g.P>(t, e0, e1, s, u, uok, acc);
-                reduce_lanes<L, g.G>(acc);
-                if (mine && s == 0 && uok) {
-                    acc.finalize();
-                    store_unit<K>(out, row * t.fu + u, acc.v);
-                    if constexpr (RED == RED_MAX) store_unit_i<K>(out_arg, row * t.fu + u, acc.e);
-                }
-            }
-        }
-    }
+    const Table<K, BUF, NT> tab(t.table, t.fu, t.table_bytes);
+    // argmax table (max-routing gather only; otherwise an unused empty resource)
+    const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t *>(t.arg), 0, (BUF && WM == W_ROUTE) ? t.table_bytes : 0u, kBufWord3);
+    GatherBody<K, L, RED, WM, BUF, NT> body{t, tab, ars, out, out_arg, part_v, part_e};
+    const Items items = make_items(counts, n_groups);
+    for_each_item<L>(items, chunks, t.ptr, t.nrows, body);
 }
 
 // Merge the partial states of split rows in chunk order: lane slot s folds
 // chunks s, s + S, ..., then the slots are combined by a fixed shuffle tree.
 template <int K, int L, int RED>
-__global__ __launch_bounds__(kBlock) void merge_kernel(const Desc *__restrict__ splits,
+__global__ __launch_bounds__(kBlock) void merge_kernel(const Split *__restrict__ splits,
                                                        const PlanCounts *__restrict__ counts, int64_t fu,
                                                        const float *__restrict__ part_v,
                                                        const int32_t *__restrict__ part_e,
@@ -104,16 +81,16 @@ __global__ __launch_bounds__(kBlock) void merge_kernel(const Desc *__restrict__ 
     const int s = lane / L;
     const int l = lane % L;
     for (int64_t it = wave; it < n_split; it += nwaves) {
-        const Desc d = splits[it];
-        const int64_t row = d.x;
+        const Split d = splits[it];
+        const int64_t row = d.row;
         for (int64_t fb = 0; fb < fu; fb += L) {
             const int64_t u = fb + l;
             const bool uok = u < fu;
             A acc;
             acc.init();
             if (uok) {
-                for (int c = s; c < d.z; c += g.S) {
-                    const int64_t unit = (static_cast<int64_t>(d.y) + c) * fu + u;
+                for (int c = s; c < d.nch; c += g.S) {
+                    const int64_t unit = (static_cast<int64_t>(d.slot0) + c) * fu + u;
                     Vec<K> p = load_unit<K>(part_v, unit);
                     int pe[K];
                     if constexpr (RED == RED_MAX) {
@@ -135,18 +112,33 @@ __global__ __launch_bounds__(kBlock) void merge_kernel(const Desc *__restrict__ 
     }
 }
 
+template <int K, int L, int RED, int WM, bool BUF, bool NT>
+int launch_gather_reduce(const Trav &t, int64_t n_groups, const PlanWs &w, const PlanBounds &b, float *out,
+                         int32_t *out_arg, hipStream_t stream) {
+    auto kern = gather_reduce_kernel<K, L, RED, WM, BUF, NT>;
+    static const int per_cu = resident_blocks(reinterpret_cast<const void *>(kern), kBlock);
+    const int blocks = persistent_blocks(n_groups + b.max_chunks, per_cu);
+    prof_before(stream);
+    hipLaunchKernelGGL(kern, dim3(blocks), dim3(kBlock), 0, stream, t, n_groups, w.chunks, w.counts, out, out_arg,
+                       w.part_v, w.part_e);
+    prof_after(stream);
+    return check_launch("gather-reduce");
+}
+
 template <int K, int L, int RED, int WM>
 int launch_traversal_t(const Trav &t, int64_t nedges, const PlanWs &w, const PlanBounds &b, float *out,
                        int32_t *out_arg, hipStream_t stream) {
     constexpr Geom g = make_geom(L);
     if (int rc = launch_plan(t.ptr, t.nrows, g, b, w, stream)) return rc;
     const int64_t n_groups = ceil_div(t.nrows, g.RPW);
-    const int blocks = persistent_blocks(n_groups + b.max_chunks);
-    prof_before(stream);
-    hipLaunchKernelGGL((gather_reduce_kernel<K, L, RED, WM>), dim3(blocks), dim3(kBlock), 0, stream, t,
-                       n_groups, w.chunks, w.counts, out, out_arg, w.part_v, w.part_e);
-    prof_after(stream);
-    if (int rc = check_launch("gather-reduce")) return rc;
+    int rc;
+    if (!t.table_bytes)
+        rc = launch_gather_reduce<K, L, RED, WM, false, true>(t, n_groups, w, b, out, out_arg, stream);
+    else if (t.table_bytes > kStreamTableBytes)
+        rc = launch_gather_reduce<K, L, RED, WM, true, true>(t, n_groups, w, b, out, out_arg, stream);
+    else
+        rc = launch_gather_reduce<K, L, RED, WM, true, false>(t, n_groups, w, b, out, out_arg, stream);
+    if (rc) return rc;
     const int mblocks = persistent_blocks(b.max_splits, 4);
     hipLaunchKernelGGL((merge_kernel<K, L, RED>), dim3(mblocks), dim3(kBlock), 0, stream, w.splits, w.counts,
                        t.fu, w.part_v, w.part_e, out, out_arg);
@@ -191,9 +183,12 @@ size_t traversal_ws_bytes(int64_t nrows, int64_t nedges, int64_t feat, bool with
     return best;
 }
 
-int launch_traversal(const Trav &t, int64_t nedges, const Layout &lay, int red, int wm, void *ws, float *out,
-                     int32_t *out_arg, hipStream_t stream) {
-    if (t.nrows == 0) return TIGA_OK;
+int launch_traversal(const Trav &t0, int64_t table_rows, int64_t nedges, const Layout &lay, int red, int wm, void *ws,
+                     float *out, int32_t *out_arg, hipStream_t stream) {
+    if (t0.nrows == 0) return TIGA_OK;
+    Trav t = t0;
+    const int64_t tb = table_rows * lay.fu * lay.K * 4;
+    t.table_bytes = (tb > 0 && tb < (int64_t{1} << 32)) ? static_cast<uint32_t>(tb) : 0u;
     const PlanBounds b = plan_bounds(t.nrows, nedges, lay.g);
     Carve c(ws);
     const PlanWs w = carve_plan(c, b, lay.fu * lay.K, red == RED_MAX);

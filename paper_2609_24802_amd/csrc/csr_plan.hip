@@ -1,11 +1,11 @@
 // Degree-aware row plan (deterministic; no global atomics).
 //
-// count: per tile of kPlanTile rows, the number of chunk descriptors, partial
-//        slots and split rows its medium/long rows need;
+// count: per tile of kPlanTile rows, the chunks of each class, partial slots
+//        and split rows its non-short rows need;
 // scan:  exclusive prefix over tiles (one block), totals to PlanCounts;
-// write: each tile recomputes its rows and writes descriptors at its offset.
-// Within a tile, row (r, t) = tile_base + r * kBlock + t is visited in
-// (r, t) order, so the descriptor order depends only on the topology.
+// write: each tile recomputes its rows and writes descriptors at its offsets;
+//        class c's descriptors follow those of classes 0..c-1.
+// Descriptor positions depend only on the topology.
 #include "csr_common.hpp"
 
 namespace tiga {
@@ -13,136 +13,169 @@ namespace csr {
 
 namespace {
 
-struct RowNeed {
-    int64_t chunks, slots, splits;
+struct Need {
+    int64_t v[kPlanVals];  // chunks per class, partial slots, split rows
 };
 
-__device__ __forceinline__ RowNeed row_need(const int64_t *__restrict__ ptr, int64_t row, int64_t nrows,
-                                            int DS, int CH) {
-    RowNeed r{0, 0, 0};
+__device__ __forceinline__ Need row_need(const Geom &g, const int64_t *__restrict__ ptr, int64_t row, int64_t nrows,
+                                         int64_t &e0, int64_t &deg) {
+    Need r;
+#pragma unroll
+    for (int k = 0; k < kPlanVals; ++k) r.v[k] = 0;
+    e0 = 0;
+    deg = 0;
     if (row < nrows) {
-        const int64_t d = ptr[row + 1] - ptr[row];
-        if (d > DS) {
-            r.chunks = (d + CH - 1) / CH;
-            if (r.chunks > 1) {
-                r.slots = r.chunks;
-                r.splits = 1;
+        e0 = ptr[row];
+        deg = ptr[row + 1] - e0;
+        if (deg > g.DS) {
+            const int64_t nch = (deg + g.CH - 1) / g.CH;
+            const int64_t last = deg - (nch - 1) * g.CH;
+            const int c = chunk_class(g, last);
+            r.v[0] += nch - 1 + (c == 0);
+            r.v[1] += (c == 1);
+            r.v[2] += (c == 2);
+            if (nch > 1) {
+                r.v[kClasses] = nch;
+                r.v[kClasses + 1] = 1;
             }
         }
     }
     return r;
 }
 
-// Block-wide exclusive scan of three counters; returns block totals.
-__device__ __forceinline__ RowNeed block_excl_scan3(RowNeed v, RowNeed &excl) {
-    __shared__ int64_t sh[3][kWavesPerBlock];
+// Block-wide exclusive scan of kPlanVals counters; returns block totals.
+__device__ __forceinline__ Need block_excl_scan(const Need &v, Need &excl) {
+    __shared__ int64_t sh[kPlanVals][kWavesPerBlock];
     const int lane = lane_id();
     const int wave = threadIdx.x / kWave;
-    const int64_t ic = wave_incl_scan(v.chunks);
-    const int64_t is = wave_incl_scan(v.slots);
-    const int64_t ip = wave_incl_scan(v.splits);
-    if (lane == kWave - 1) {
-        sh[0][wave] = ic;
-        sh[1][wave] = is;
-        sh[2][wave] = ip;
-    }
-    __syncthreads();
-    int64_t oc = 0, os = 0, op = 0;
-    RowNeed tot{0, 0, 0};
+    Need inc, tot;
 #pragma unroll
-    for (int w = 0; w < kWavesPerBlock; ++w) {
-        if (w < wave) {
-            oc += sh[0][w];
-            os += sh[1][w];
-            op += sh[2][w];
-        }
-        tot.chunks += sh[0][w];
-        tot.slots += sh[1][w];
-        tot.splits += sh[2][w];
+    for (int k = 0; k < kPlanVals; ++k) {
+        inc.v[k] = wave_incl_scan(v.v[k]);
+        if (lane == kWave - 1) sh[k][wave] = inc.v[k];
     }
     __syncthreads();
-    excl.chunks = oc + ic - v.chunks;
-    excl.slots = os + is - v.slots;
-    excl.splits = op + ip - v.splits;
+#pragma unroll
+    for (int k = 0; k < kPlanVals; ++k) {
+        int64_t off = 0, t = 0;
+#pragma unroll
+        for (int w = 0; w < kWavesPerBlock; ++w) {
+            if (w < wave) off += sh[k][w];
+            t += sh[k][w];
+        }
+        excl.v[k] = off + inc.v[k] - v.v[k];
+        tot.v[k] = t;
+    }
+    __syncthreads();
     return tot;
 }
 
-__global__ __launch_bounds__(kBlock) void plan_count_kernel(const int64_t *__restrict__ ptr, int64_t nrows,
-                                                            int DS, int CH, int64_t *__restrict__ tile_vals) {
+__global__ __launch_bounds__(kBlock) void plan_count_kernel(Geom g, const int64_t *__restrict__ ptr, int64_t nrows,
+                                                            int64_t *__restrict__ tile_vals) {
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kPlanTile;
-    RowNeed acc{0, 0, 0};
+    Need acc;
+#pragma unroll
+    for (int k = 0; k < kPlanVals; ++k) acc.v[k] = 0;
 #pragma unroll
     for (int r = 0; r < kPlanRowsPerThread; ++r) {
-        RowNeed n = row_need(ptr, base + r * kBlock + threadIdx.x, nrows, DS, CH);
-        acc.chunks += n.chunks;
-        acc.slots += n.slots;
-        acc.splits += n.splits;
+        int64_t e0, deg;
+        const Need n = row_need(g, ptr, base + r * kBlock + threadIdx.x, nrows, e0, deg);
+#pragma unroll
+        for (int k = 0; k < kPlanVals; ++k) acc.v[k] += n.v[k];
     }
-    RowNeed excl;
-    RowNeed tot = block_excl_scan3(acc, excl);
-    if (threadIdx.x == 0) {
-        tile_vals[3 * blockIdx.x + 0] = tot.chunks;
-        tile_vals[3 * blockIdx.x + 1] = tot.slots;
-        tile_vals[3 * blockIdx.x + 2] = tot.splits;
-    }
+    Need excl;
+    const Need tot = block_excl_scan(acc, excl);
+    if (threadIdx.x < kPlanVals) tile_vals[kPlanVals * blockIdx.x + threadIdx.x] = tot.v[threadIdx.x];
 }
 
-// One block: exclusive scan over the tiles, in place.
+// One block: exclusive scan over the tiles, in place, and the totals.  Each
+// thread first sums a contiguous run of tiles, then one block scan combines
+// the runs.
 __global__ __launch_bounds__(kBlock) void plan_scan_kernel(int64_t *__restrict__ tile_vals, int64_t tiles,
                                                            PlanCounts *__restrict__ counts) {
-    RowNeed carry{0, 0, 0};
-    for (int64_t t0 = 0; t0 < tiles; t0 += kBlock) {
-        const int64_t t = t0 + threadIdx.x;
-        RowNeed v{0, 0, 0};
-        if (t < tiles) {
-            v.chunks = tile_vals[3 * t + 0];
-            v.slots = tile_vals[3 * t + 1];
-            v.splits = tile_vals[3 * t + 2];
+    const int64_t per = (tiles + kBlock - 1) / kBlock;
+    const int64_t t0 = static_cast<int64_t>(threadIdx.x) * per;
+    const int64_t t1 = t0 + per < tiles ? t0 + per : tiles;
+    Need sum;
+#pragma unroll
+    for (int k = 0; k < kPlanVals; ++k) sum.v[k] = 0;
+    for (int64_t t = t0; t < t1; ++t)
+#pragma unroll
+        for (int k = 0; k < kPlanVals; ++k) sum.v[k] += tile_vals[kPlanVals * t + k];
+    Need excl;
+    const Need tot = block_excl_scan(sum, excl);
+    for (int64_t t = t0; t < t1; ++t)
+#pragma unroll
+        for (int k = 0; k < kPlanVals; ++k) {
+            const int64_t v = tile_vals[kPlanVals * t + k];
+            tile_vals[kPlanVals * t + k] = excl.v[k];
+            excl.v[k] += v;
         }
-        RowNeed excl;
-        RowNeed tot = block_excl_scan3(v, excl);
-        if (t < tiles) {
-            tile_vals[3 * t + 0] = carry.chunks + excl.chunks;
-            tile_vals[3 * t + 1] = carry.slots + excl.slots;
-            tile_vals[3 * t + 2] = carry.splits + excl.splits;
-        }
-        carry.chunks += tot.chunks;
-        carry.slots += tot.slots;
-        carry.splits += tot.splits;
-    }
     if (threadIdx.x == 0) {
-        counts->chunks = static_cast<unsigned long long>(carry.chunks);
-        counts->slots = static_cast<unsigned long long>(carry.slots);
-        counts->splits = static_cast<unsigned long long>(carry.splits);
-        counts->pad = 0;
+        for (int c = 0; c < kClasses; ++c) counts->cls[c] = static_cast<unsigned long long>(tot.v[c]);
+        counts->slots = static_cast<unsigned long long>(tot.v[kClasses]);
+        counts->splits = static_cast<unsigned long long>(tot.v[kClasses + 1]);
+        counts->pad[0] = counts->pad[1] = counts->pad[2] = 0;
     }
 }
 
-__global__ __launch_bounds__(kBlock) void plan_write_kernel(const int64_t *__restrict__ ptr, int64_t nrows,
-                                                            int DS, int CH,
+// Descriptors of a tile: thread t owns rows base + r * kBlock + t (r <
+// kPlanRowsPerThread) and writes them after the rows of threads 0..t-1.
+__global__ __launch_bounds__(kBlock) void plan_write_kernel(Geom g, const int64_t *__restrict__ ptr, int64_t nrows,
                                                             const int64_t *__restrict__ tile_vals,
-                                                            Desc *__restrict__ chunks, Desc *__restrict__ splits) {
+                                                            const PlanCounts *__restrict__ counts,
+                                                            Desc *__restrict__ chunks, Split *__restrict__ splits) {
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kPlanTile;
-    RowNeed run{tile_vals[3 * blockIdx.x + 0], tile_vals[3 * blockIdx.x + 1], tile_vals[3 * blockIdx.x + 2]};
+    int64_t cbase[kClasses];
+    int64_t b = 0;
+#pragma unroll
+    for (int c = 0; c < kClasses; ++c) {
+        cbase[c] = b;
+        b += static_cast<int64_t>(counts->cls[c]);
+    }
+    int64_t e0[kPlanRowsPerThread], deg[kPlanRowsPerThread];
+    Need mine;
+#pragma unroll
+    for (int k = 0; k < kPlanVals; ++k) mine.v[k] = 0;
+#pragma unroll
     for (int r = 0; r < kPlanRowsPerThread; ++r) {
+        const Need n = row_need(g, ptr, base + r * kBlock + threadIdx.x, nrows, e0[r], deg[r]);
+#pragma unroll
+        for (int k = 0; k < kPlanVals; ++k) mine.v[k] += n.v[k];
+    }
+    Need run;
+    block_excl_scan(mine, run);
+#pragma unroll
+    for (int k = 0; k < kPlanVals; ++k) run.v[k] += tile_vals[kPlanVals * blockIdx.x + k];
+#pragma unroll
+    for (int r = 0; r < kPlanRowsPerThread; ++r) {
+        if (deg[r] <= g.DS) continue;
         const int64_t row = base + r * kBlock + threadIdx.x;
-        RowNeed n = row_need(ptr, row, nrows, DS, CH);
-        RowNeed excl;
-        RowNeed tot = block_excl_scan3(n, excl);
-        if (n.chunks > 0) {
-            const int64_t c0 = run.chunks + excl.chunks;
-            const int slot0 = n.slots ? static_cast<int>(run.slots + excl.slots) : -1;
-            for (int64_t k = 0; k < n.chunks; ++k)
-                chunks[c0 + k] = make_int4(static_cast<int>(row), static_cast<int>(k),
-                                           slot0 >= 0 ? slot0 + static_cast<int>(k) : -1,
-                                           static_cast<int>(n.chunks));
-            if (n.splits)
-                splits[run.splits + excl.splits] =
-                    make_int4(static_cast<int>(row), slot0, static_cast<int>(n.chunks), 0);
+        const int64_t nch = (deg[r] + g.CH - 1) / g.CH;
+        const int slot0 = nch > 1 ? static_cast<int>(run.v[kClasses]) : -1;
+        for (int64_t k = 0; k < nch; ++k) {
+            const int64_t len = (k + 1 < nch) ? g.CH : deg[r] - k * g.CH;
+            const int c = (k + 1 < nch) ? 0 : chunk_class(g, len);
+            Desc d;
+            d.row = static_cast<int32_t>(row);
+            d.slot = slot0 >= 0 ? slot0 + static_cast<int>(k) : -1;
+            d.range = pack_range(e0[r] + k * g.CH, len);
+            const int64_t pos = c == 0 ? cbase[0] + run.v[0] : (c == 1 ? cbase[1] + run.v[1] : cbase[2] + run.v[2]);
+            chunks[pos] = d;
+            run.v[0] += (c == 0);
+            run.v[1] += (c == 1);
+            run.v[2] += (c == 2);
         }
-        run.chunks += tot.chunks;
-        run.slots += tot.slots;
-        run.splits += tot.splits;
+        if (nch > 1) {
+            Split sp;
+            sp.row = static_cast<int32_t>(row);
+            sp.slot0 = slot0;
+            sp.nch = static_cast<int32_t>(nch);
+            sp.pad = 0;
+            splits[run.v[kClasses + 1]] = sp;
+            run.v[kClasses] += nch;
+            run.v[kClasses + 1] += 1;
+        }
     }
 }
 
@@ -151,13 +184,12 @@ __global__ __launch_bounds__(kBlock) void plan_write_kernel(const int64_t *__res
 int launch_plan(const int64_t *ptr, int64_t nrows, const Geom &g, const PlanBounds &b, const PlanWs &w,
                 hipStream_t stream) {
     const unsigned tiles = static_cast<unsigned>(b.tiles);
-    hipLaunchKernelGGL(plan_count_kernel, dim3(tiles), dim3(kBlock), 0, stream, ptr, nrows, g.DS, g.CH,
-                       w.tile_vals);
+    hipLaunchKernelGGL(plan_count_kernel, dim3(tiles), dim3(kBlock), 0, stream, g, ptr, nrows, w.tile_vals);
     if (int rc = check_launch("plan count")) return rc;
     hipLaunchKernelGGL(plan_scan_kernel, dim3(1), dim3(kBlock), 0, stream, w.tile_vals, b.tiles, w.counts);
     if (int rc = check_launch("plan scan")) return rc;
-    hipLaunchKernelGGL(plan_write_kernel, dim3(tiles), dim3(kBlock), 0, stream, ptr, nrows, g.DS, g.CH,
-                       w.tile_vals, w.chunks, w.splits);
+    hipLaunchKernelGGL(plan_write_kernel, dim3(tiles), dim3(kBlock), 0, stream, g, ptr, nrows, w.tile_vals, w.counts,
+                       w.chunks, w.splits);
     return check_launch("plan write");
 }
 
