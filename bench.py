@@ -44,9 +44,99 @@ def parse():
     p.add_argument("--scale", type=float, default=1.0, help="shrink the headline graph (testing only)")
     p.add_argument("--no-paths", action="store_true", help="skip the per-path figures")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--no-ceilings", action="store_true", help="skip the hardware-ceiling probe")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--check-rows", type=int, default=400)
+    p.add_argument("--profile-pass", action="store_true",
+                   help="for rocprofv3 counter runs: a 4 GiB plain copy (calibration) then 3 headline steps")
+    p.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
+                   help="print the markdown summary of three rocprofv3 runs (kernel trace, FETCH_SIZE, WRITE_SIZE)")
     return p.parse_args()
+
+
+PROFILE_MD = os.path.join(ROOT, "profiles", "gather_reduce_csr_powerlaw_1b_f16.md")
+KERNEL_KEY = "gather_reduce_kernel"
+COPY_BYTES = 1 << 32
+
+
+def source_hash():
+    """sha256 over the HIP sources: a committed counter summary applies only to the kernels it measured."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_24802_amd", "csrc")
+    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp"))):
+        h.update(os.path.basename(f).encode())
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic():
+    """Per-launch HBM bytes of the gather-reduce kernel from the committed summary, if still current."""
+    if not os.path.exists(PROFILE_MD):
+        return None
+    vals = {}
+    for line in open(PROFILE_MD):
+        if line.startswith("- ") and ": " in line:
+            k, v = line[2:].strip().split(": ", 1)
+            vals[k.strip("` ")] = v.strip("` ")
+    if vals.get("source_hash") != source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def _db(d):
+    import glob
+    import sqlite3
+    fs = glob.glob(os.path.join(d, "**", "*_results.db"), recursive=True)
+    if not fs:
+        raise SystemExit(f"no rocprofv3 database under {d}")
+    return sqlite3.connect(fs[0])
+
+
+def summarize(trace_dir, fetch_dir, write_dir):
+    """Markdown summary: per-kernel durations and the scaled HBM traffic of the dominant kernel."""
+    cur = _db(trace_dir).cursor()
+    rows = cur.execute("select name, duration from kernels").fetchall()
+    agg = {}
+    for name, dur in rows:
+        a = agg.setdefault(name, [0, 0.0])
+        a[0] += 1
+        a[1] += dur
+    out = ["| kernel | calls | total ms | avg ms |", "|---|---|---|---|"]
+    for name, (n, d) in sorted(agg.items(), key=lambda kv: -kv[1][1])[:8]:
+        out.append(f"| `{name[:90]}` | {n} | {d / 1e6:.3f} | {d / n / 1e6:.4f} |")
+    dom = [(n, d) for name, (n, d) in agg.items() if KERNEL_KEY in name]
+    avg_ms = dom[0][1] / dom[0][0] / 1e6 if dom else float("nan")
+
+    def counter(d, cname):
+        c = _db(d).cursor()
+        vals = c.execute("select kernel_name, value from counters_collection where counter_name = ?",
+                         (cname,)).fetchall()
+        copy = [v for k, v in vals if "copy" in k.lower() or "elementwise" in k.lower()]
+        kern = [v for k, v in vals if KERNEL_KEY in k]
+        return (max(copy) if copy else float("nan")), (sum(kern) / len(kern) if kern else float("nan"))
+
+    fcopy, fk = counter(fetch_dir, "FETCH_SIZE")
+    wcopy, wk = counter(write_dir, "WRITE_SIZE")
+    fscale = COPY_BYTES / (fcopy * 1024)
+    wscale = COPY_BYTES / (wcopy * 1024)
+    fetch_b = fk * 1024 * fscale
+    write_b = wk * 1024 * wscale
+    out += [
+        "",
+        f"- kernel_avg_ms: {avg_ms:.4f}",
+        f"- copy_calibration: a {COPY_BYTES} B device copy reads FETCH_SIZE {fcopy:.1f} KiB "
+        f"(scale {fscale:.3f}) and WRITE_SIZE {wcopy:.1f} KiB (scale {wscale:.3f})",
+        f"- fetch_bytes_per_launch: {fetch_b:.4g}",
+        f"- write_bytes_per_launch: {write_b:.4g}",
+        f"- hbm_bytes_per_launch: {fetch_b + write_b:.6g}",
+        f"- source_hash: {source_hash()}",
+    ]
+    print("\n".join(out))
 
 
 class Timer:
@@ -133,15 +223,18 @@ def headline(args, torch, tb, synth, oracle):
 def cpu_baseline(args, oracle, rp, col, x, w):
     """The oracle (untuned, fp64) on the first rows of the same graph."""
     n = rp.size - 1
-    # calibrate on ~2M edges, then size the sample for about cpu_seconds
-    k = int(np.searchsorted(rp, 2_000_000))
-    k = max(1, min(k, n))
-    t = time.perf_counter()
-    oracle.csr_sum_fwd(rp, col, x, w, rows=np.arange(k))
-    rate = (rp[k] - rp[0]) / max(time.perf_counter() - t, 1e-6)
-    target = int(rate * args.cpu_seconds)
-    k = int(np.searchsorted(rp, target))
-    k = max(1, min(k, n))
+    # grow the sample until it takes a measurable time, then size it for about cpu_seconds
+    edges = 2_000_000
+    while True:
+        k = max(1, min(int(np.searchsorted(rp, edges)), n))
+        t = time.perf_counter()
+        oracle.csr_sum_fwd(rp, col, x, w, rows=np.arange(k))
+        dt = time.perf_counter() - t
+        if dt > 0.5 or k == n:
+            break
+        edges *= 4
+    rate = (rp[k] - rp[0]) / max(dt, 1e-6)
+    k = max(1, min(int(np.searchsorted(rp, int(rate * args.cpu_seconds))), n))
     rows = np.arange(k)
     t = time.perf_counter()
     oracle.csr_sum_fwd(rp, col, x, w, rows=rows)
@@ -214,8 +307,45 @@ def paths(args, torch, tb, synth):
     return res
 
 
+def profile_pass(args, torch, tb, synth):
+    """Workload for counter runs: a plain copy of known size, then three steps."""
+    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1.0)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+    g = synth.config5(scale=args.scale)
+    dev = lambda a: torch.from_numpy(a).cuda()
+    rel = tb.Csr(dev(g["row_ptr"]), dev(g["col"]), g["num_dst"])
+    xd, wd = dev(g["x"]), dev(g["w"])
+    for _ in range(3):
+        tb.tiga_mp_csr_fwd(rel, xd, wd)
+    torch.cuda.synchronize()
+    log("profile pass done")
+
+
+def ceilings():
+    """Measured hardware ceilings (stream read/copy, random row gathers, VALU), from the probe binary."""
+    import subprocess
+    exe = os.path.join(ROOT, "paper_2609_24802_amd", "ceilings", "tiga_ceilings")
+    if not os.path.exists(exe):
+        log("ceiling probe not built")
+        return None
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=300)
+    if r.returncode != 0:
+        log(f"ceiling probe failed: {r.stderr.strip()[-200:]}")
+        return None
+    c = json.loads(r.stdout.strip().splitlines()[-1])
+    log(f"ceilings: {c}")
+    return c
+
+
 def main():
     args = parse()
+    if args.summarize:
+        summarize(*args.summarize)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
@@ -230,6 +360,10 @@ def main():
         import __graft_entry__
         __graft_entry__.build()
     tb.load()
+    if args.profile_pass:
+        profile_pass(args, torch, tb, synth)
+        return
+    ceil = None if args.no_ceilings else ceilings()
     h, cpu = headline(args, torch, tb, synth, oracle)
     extra = {} if args.no_paths else paths(args, torch, tb, synth)
     value = h["E"] / (h["step_ms"] * 1e-3) / 1e9
@@ -250,10 +384,13 @@ def main():
                    "num_edges": h["E"], "feat": h["F"], "reducer": "sum", "message": "w_e * x_src",
                    "scale": args.scale},
         "roofline": {"bound": "hbm", "achieved": h["achieved"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": h["achieved"] / HBM_PEAK_GBS, "traffic": None,
+                     "frac": h["achieved"] / HBM_PEAK_GBS, "traffic": committed_traffic(),
                      "kernel": "gather_reduce_kernel", "kernel_ms": h["kernel_ms"],
-                     "bytes_per_launch": h["bytes_alg"]},
+                     "bytes_per_launch": h["bytes_alg"],
+                     "frac_of_measured_gather_ceiling": (h["E"] / (h["kernel_ms"] * 1e-3)) / ceil["gather64_rows_per_s"]
+                     if ceil else None},
         "cpu_baseline": cpu,
+        "ceilings": ceil,
         "parity_sampled": h["parity_ok"],
         "paths": extra,
     }

@@ -11,6 +11,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libtiga_mp.so")
+CEIL_SRC = os.path.join(HERE, "ceilings", "ceilings.hip")
+CEIL_OUT = os.path.join(HERE, "ceilings", "tiga_ceilings")
 BUILD = os.path.join(ROOT, "_build")
 
 ARCH = os.environ.get("TIGA_OFFLOAD_ARCH", "gfx950")
@@ -44,6 +46,12 @@ def build(jobs: int = 8) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, OUT)
+    # hardware-ceiling probe used by bench.py
+    tmp = CEIL_OUT + f".tmp{os.getpid()}"
+    r = subprocess.run([HIPCC, *FLAGS, CEIL_SRC, "-o", tmp], capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for {CEIL_SRC}:\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, CEIL_OUT)
     return OUT
 
 
