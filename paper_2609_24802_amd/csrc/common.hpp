@@ -78,6 +78,18 @@ __device__ __forceinline__ int64_t uniform64(int64_t v) {
     return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
 }
 
+// The hardware hands workgroups to the 8 XCDs round-robin (block b runs on
+// XCD b % 8).  This renumbering gives each XCD a contiguous range of logical
+// blocks, so blocks that share data share that XCD's L2.  It is a bijection
+// on [0, gridDim.x).
+constexpr unsigned kXcds = 8;
+__device__ __forceinline__ unsigned xcd_block() {
+    const unsigned b = blockIdx.x, nb = gridDim.x;
+    const unsigned x = b % kXcds, k = b / kXcds;
+    const unsigned per = nb / kXcds, rem = nb % kXcds;
+    return x * per + (x < rem ? x : rem) + k;
+}
+
 __device__ __forceinline__ float shfl_xor_f(float v, int m) { return __shfl_xor(v, m, kWave); }
 __device__ __forceinline__ int shfl_xor_i(int v, int m) { return __shfl_xor(v, m, kWave); }
 

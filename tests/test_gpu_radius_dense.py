@@ -42,7 +42,9 @@ def cloud(kind, n, seed):
 
 @pytest.mark.parametrize("kind,n,r,F", [("uniform", 3000, 0.07, 16), ("grid", 2500, 0.1, 4),
                                         ("cluster", 2000, 0.05, 3), ("flat", 1500, 0.06, 32),
-                                        ("uniform", 777, 0.2, 1), ("uniform", 5000, 0.04, 64)])
+                                        ("uniform", 777, 0.2, 1), ("uniform", 5000, 0.04, 64),
+                                        ("uniform", 2000, 0.08, 8), ("grid", 1200, 0.1, 12),
+                                        ("cluster", 1500, 0.05, 128)])
 def test_radius_forward_backward(lib, kind, n, r, F):
     pos = cloud(kind, n, n + F)
     x = synth.normal_f32(n * F, (82, n, F)).reshape(n, F)
