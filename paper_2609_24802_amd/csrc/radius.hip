@@ -278,432 +278,411 @@ __device__ __forceinline__ void for_candidates(const Params &p, const int64_t *_
     }
 }
 
-// FB float4 units of features per pass (a feature block), scalar tail handled
-// by the K = 1 instantiation.
-template <int K, int NU>
-__global__ __launch_bounds__(kBlock) void radius_fwd_kernel(const Params *__restrict__ prm,
-                                                            const int64_t *__restrict__ start,
-                                                            const float4 *__restrict__ rec,
-                                                            const float *__restrict__ xs, int64_t n, int64_t fu,
-                                                            float r2, float neg_inv_s2, float *__restrict__ y,
-                                                            int32_t *__restrict__ count) {
-    const Params p = *prm;
-    const int64_t s = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (s >= n) return;
-    const float4 pi = rec[s];
-    const int32_t i = __float_as_int(pi.w);
-    for (int64_t fb = 0; fb < fu; fb += NU) {
-        float acc[NU][K];
-#pragma unroll
-        for (int u = 0; u < NU; ++u)
-#pragma unroll
-            for (int k = 0; k < K; ++k) acc[u][k] = 0.0f;
-        int cnt = 0;
-        for_candidates(p, start, pi, [&](int64_t t) {
-            const float4 pj = rec[t];
-            float d2;
-            if (accept(pi, pj, r2, d2) && __float_as_int(pj.w) != i) {
-                ++cnt;
-                const float kw = __expf(d2 * neg_inv_s2);
-#pragma unroll
-                for (int u = 0; u < NU; ++u) {
-                    if (fb + u < fu) {
-                        csr::Vec<K> xv = csr::load_unit<K>(xs, t * fu + fb + u);
-#pragma unroll
-                        for (int k = 0; k < K; ++k) acc[u][k] = fmaf(kw, xv.v[k], acc[u][k]);
-                    }
-                }
-            }
-        });
-#pragma unroll
-        for (int u = 0; u < NU; ++u)
-            if (fb + u < fu) csr::store_unit<K>(y, static_cast<int64_t>(i) * fu + fb + u, acc[u]);
-        if (fb == 0 && count) count[i] = cnt;
-    }
-}
-
-// Backward: dx_i = sum k_ij dy_j and dp_i = sum (2 k_ij / sigma^2)(p_j - p_i)
-// (<dy_i, x_j> + <dy_j, x_i>), one thread per destination point.
-template <int K, int NU, bool DX, bool DP>
-__global__ __launch_bounds__(kBlock) void radius_bwd_kernel(const Params *__restrict__ prm,
-                                                            const int64_t *__restrict__ start,
-                                                            const float4 *__restrict__ rec,
-                                                            const float *__restrict__ xs,
-                                                            const float *__restrict__ ys, int64_t n, int64_t fu,
-                                                            float r2, float neg_inv_s2, float two_inv_s2,
-                                                            float *__restrict__ dx, float *__restrict__ dp) {
-    const Params p = *prm;
-    const int64_t s = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (s >= n) return;
-    const float4 pi = rec[s];
-    const int32_t i = __float_as_int(pi.w);
-    float gp[3] = {0.0f, 0.0f, 0.0f};
-    for (int64_t fb = 0; fb < fu; fb += NU) {
-        float gi[NU][K], xi[NU][K], acc[NU][K];
-#pragma unroll
-        for (int u = 0; u < NU; ++u) {
-            csr::Vec<K> a, b;
-            if (fb + u < fu) {
-                a = csr::load_unit<K>(ys, s * fu + fb + u);
-                if (DP) {
-                    b = csr::load_unit<K>(xs, s * fu + fb + u);
-                } else {
-#pragma unroll
-                    for (int k = 0; k < K; ++k) b.v[k] = 0.0f;
-                }
-            } else {
-#pragma unroll
-                for (int k = 0; k < K; ++k) a.v[k] = b.v[k] = 0.0f;
-            }
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-                gi[u][k] = a.v[k];
-                xi[u][k] = b.v[k];
-                acc[u][k] = 0.0f;
-            }
-        }
-        float blk[3] = {0.0f, 0.0f, 0.0f};
-        for_candidates(p, start, pi, [&](int64_t t) {
-            const float4 pj = rec[t];
-            float d2;
-            if (accept(pi, pj, r2, d2) && __float_as_int(pj.w) != i) {
-                const float kw = __expf(d2 * neg_inv_s2);
-                float dot = 0.0f;
-#pragma unroll
-                for (int u = 0; u < NU; ++u) {
-                    if (fb + u < fu) {
-                        csr::Vec<K> gj = csr::load_unit<K>(ys, t * fu + fb + u);
-                        csr::Vec<K> xj;
-                        if (DP) xj = csr::load_unit<K>(xs, t * fu + fb + u);
-#pragma unroll
-                        for (int k = 0; k < K; ++k) {
-                            if (DX) acc[u][k] = fmaf(kw, gj.v[k], acc[u][k]);
-                            if (DP) dot = fmaf(gi[u][k], xj.v[k], fmaf(gj.v[k], xi[u][k], dot));
-                        }
-                    }
-                }
-                if (DP) {
-                    const float c = two_inv_s2 * kw * dot;
-                    blk[0] = fmaf(c, pj.x - pi.x, blk[0]);
-                    blk[1] = fmaf(c, pj.y - pi.y, blk[1]);
-                    blk[2] = fmaf(c, pj.z - pi.z, blk[2]);
-                }
-            }
-        });
-        if (DX) {
-#pragma unroll
-            for (int u = 0; u < NU; ++u)
-                if (fb + u < fu) csr::store_unit<K>(dx, static_cast<int64_t>(i) * fu + fb + u, acc[u]);
-        }
-        gp[0] += blk[0];
-        gp[1] += blk[1];
-        gp[2] += blk[2];
-    }
-    if (DP) {
-        dp[static_cast<int64_t>(i) * 3 + 0] = gp[0];
-        dp[static_cast<int64_t>(i) * 3 + 1] = gp[1];
-        dp[static_cast<int64_t>(i) * 3 + 2] = gp[2];
-    }
-}
-
 // ---------------------------------------------------------------------------
-// Wave-cooperative consume (16-byte feature units).
+// Consume: one wavefront per destination cell.
 //
-// A wavefront owns 64 consecutive destinations in cell order.  Phase 1: each
-// lane walks the candidate runs of its destination, tests them and appends the
-// accepted (cell-ordered index, kernel weight) pairs to its column of an LDS
-// list, until the list is nearly full or the runs are exhausted.  Phase 2: the
-// wave splits into groups of LPR lanes; a group takes one destination at a
-// time and reads each listed neighbour's feature row as LPR consecutive
-// 16-byte units (one coalesced row per group), accumulating in registers.  The
-// two phases alternate until every lane's runs are exhausted.  The summation
-// order is the candidate order, so results are reproducible.
-constexpr int kCap = 24;    // list entries per destination between flushes
-constexpr int kStep = 8;    // candidates tested per step of a lane
-constexpr int kBatch = 8;   // list entries whose rows are loaded together
-constexpr int kBatchDp = 2; // the same when position gradients are formed (more live registers)
+// Every point of a cell has the same candidate set, the 27 cells around it
+// (9 runs of the cell-ordered arrays), so the run bounds are wave-uniform.
+// Phase 1: the wave loads 64 candidates at a time (one per lane, coalesced)
+// and tests them against each destination of the cell in turn (up to kDch
+// destinations per pass); the accepted lanes of a destination append
+// (cell-ordered index, kernel weight) to that destination's LDS list in
+// candidate order (ballot + prefix count).  Phase 2 (a flush, when a list
+// would overflow and at the end of the pass): lane groups of LPR lanes read
+// each listed neighbour's feature row as LPR consecutive units, one
+// destination per group; when the cell has few destinations, S groups share a
+// destination (interleaved entries) and are combined by a fixed shuffle tree.
+// Every summation order depends only on the input.
+constexpr int kDch = 16;     // destinations per pass over a cell's candidates
+constexpr int kCapC = 64;    // list entries per destination between flushes
+constexpr int kBatch = 8;    // list entries whose rows are loaded together
+constexpr int kBatchDp = 4;  // the same when position gradients are formed
 
-struct Cursor {
-    int cx0, cx1, cy, cz;
-    int k;  // next run (z, y) = (cz - 1 + k / 3, cy - 1 + k % 3)
-    int32_t t, e;
-};
-
-// Load the bounds of the next non-empty run; false when none is left.
-__device__ __forceinline__ bool next_run(const Params &p, const int64_t *__restrict__ start, Cursor &c) {
-    while (c.k < 9) {
-        const int z = c.cz - 1 + c.k / 3;
-        const int y = c.cy - 1 + c.k % 3;
-        ++c.k;
-        if (z < 0 || z >= p.dim[2] || y < 0 || y >= p.dim[1]) continue;
-        const int rowc = (z * p.dim[1] + y) * p.dim[0];
-        c.t = static_cast<int32_t>(start[rowc + c.cx0]);
-        c.e = static_cast<int32_t>(start[rowc + c.cx1 + 1]);
-        if (c.t < c.e) return true;
-    }
-    c.t = c.e = 0;
-    return false;
-}
-
-__device__ __forceinline__ bool open_cursor(const Params &p, const int64_t *__restrict__ start, float4 pi,
-                                            Cursor &c) {
-    const int cx = cell_axis(p, 0, pi.x);
-    c.cy = cell_axis(p, 1, pi.y);
-    c.cz = cell_axis(p, 2, pi.z);
-    c.cx0 = cx > 0 ? cx - 1 : 0;
-    c.cx1 = cx + 1 < p.dim[0] ? cx + 1 : p.dim[0] - 1;
-    c.k = 0;
-    return next_run(p, start, c);
-}
-
-// Phase 1 for one lane: append accepted candidates to its column until the
-// column is full or the runs are exhausted; the cursor stops right after the
-// last candidate taken.  Returns the number of entries written.
-__device__ __forceinline__ int fill_list(const Params &p, const int64_t *__restrict__ start,
-                                         const float4 *__restrict__ rec, float4 pi, int32_t i, float r2,
-                                         float neg_inv_s2, Cursor &c, bool &live, float2 (*list)[kWave], int lane) {
-    int m = 0;
-    while (live && m < kCap) {
-        float4 pj[kStep];
-#pragma unroll
-        for (int u = 0; u < kStep; ++u)
-            pj[u] = c.t + u < c.e ? rec[c.t + u] : make_float4(0.0f, 0.0f, 0.0f, __int_as_float(i));
-        int32_t next = c.t + kStep;
-#pragma unroll
-        for (int u = 0; u < kStep; ++u) {
-            float d2;
-            if (accept(pi, pj[u], r2, d2) && __float_as_int(pj[u].w) != i) {
-                if (m < kCap) {
-                    list[m][lane] = make_float2(__int_as_float(c.t + u), __expf(d2 * neg_inv_s2));
-                    ++m;
-                } else if (next > c.t + u) {
-                    next = c.t + u;  // resume here after the flush
-                }
-            }
-        }
-        c.t = next;
-        if (c.t >= c.e) live = next_run(p, start, c);
-    }
-    return m;
-}
+typedef float2 CellList[kDch][kCapC + 1];  // +1: groups reading different lists hit different banks
 
 __device__ __forceinline__ void lds_fence() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
-__device__ __forceinline__ f32x4 unit4(const float *__restrict__ base, int64_t unit) {
-    return reinterpret_cast<const f32x4 *>(base)[unit];
+__device__ __forceinline__ float readlane_f(float v, int l) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
 }
 
-// y_i = sum_j k_ij x_j over the radius relation; LPR lanes per row, UPL units
-// per lane, feature blocks of LPR * UPL units.
-template <int LPR, int UPL>
-__global__ __launch_bounds__(kBlock) void radius_fwd_coop_kernel(const Params *__restrict__ prm,
-                                                                 const int64_t *__restrict__ start,
-                                                                 const float4 *__restrict__ rec,
-                                                                 const float *__restrict__ xs, int64_t n, int64_t fu,
-                                                                 float r2, float neg_inv_s2, float *__restrict__ y,
-                                                                 int32_t *__restrict__ count) {
-    constexpr int G = kWave / LPR;  // groups per wave
-    constexpr int R = LPR;          // destinations per group
-    __shared__ float2 lists[kBlock / kWave][kCap][kWave];
-    const Params p = *prm;
-    const int lane = lane_id(), wv = threadIdx.x / kWave;
-    const int g = lane / LPR, q = lane % LPR;
-    const int64_t s0 = (static_cast<int64_t>(xcd_block()) * (kBlock / kWave) + wv) * kWave;
-    if (s0 >= n) return;
-    const int64_t s = s0 + lane;
-    const bool own = s < n;
-    const float4 pi = own ? rec[s] : make_float4(0.0f, 0.0f, 0.0f, __int_as_float(-1));
-    const int32_t i = __float_as_int(pi.w);
-    for (int64_t fb = 0; fb < fu; fb += LPR * UPL) {
-        f32x4 acc[R][UPL];
-#pragma unroll
-        for (int r = 0; r < R; ++r)
-#pragma unroll
-            for (int u = 0; u < UPL; ++u) acc[r][u] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-        Cursor c;
-        bool live = own && open_cursor(p, start, pi, c);
-        int cnt = 0;
-        while (true) {
-            const int m = fill_list(p, start, rec, pi, i, r2, neg_inv_s2, c, live, lists[wv], lane);
-            cnt += m;
-            lds_fence();
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const int d = r * G + g;
-                const int md = __shfl(m, d, kWave);
-                for (int k0 = 0; k0 < md; k0 += kBatch) {
-                    float2 en[kBatch];
-#pragma unroll
-                    for (int b = 0; b < kBatch; ++b)
-                        en[b] = k0 + b < md ? lists[wv][k0 + b][d] : make_float2(0.0f, 0.0f);
-                    f32x4 xv[kBatch][UPL];
-#pragma unroll
-                    for (int b = 0; b < kBatch; ++b) {
-                        const int64_t row = static_cast<int64_t>(__float_as_int(en[b].x)) * fu + fb + q;
-#pragma unroll
-                        for (int u = 0; u < UPL; ++u)
-                            xv[b][u] = (k0 + b < md && fb + q + u * LPR < fu) ? unit4(xs, row + u * LPR)
-                                                                              : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-                    }
-#pragma unroll
-                    for (int b = 0; b < kBatch; ++b)
-#pragma unroll
-                        for (int u = 0; u < UPL; ++u) acc[r][u] += en[b].y * xv[b][u];
-                }
-            }
-            lds_fence();
-            if (__ballot(live) == 0) break;
+// Cells of XCD (blockIdx.x % 8) form one contiguous range, strided over that
+// XCD's waves, so neighbouring cells are consumed under one L2.  The grid is a
+// multiple of 8 blocks.
+struct CellSched {
+    int64_t c, hi, step;
+};
+
+__device__ __forceinline__ CellSched cell_sched(int64_t ncell) {
+    const unsigned x = blockIdx.x % kXcds, lb = blockIdx.x / kXcds, nbx = gridDim.x / kXcds;
+    // the wave index, made visibly uniform so that cell bounds and destination
+    // records are fetched with scalar loads
+    const int64_t lw = static_cast<int64_t>(lb) * (kBlock / kWave) + uniform(static_cast<int>(threadIdx.x / kWave));
+    CellSched s;
+    s.c = ncell * x / kXcds + lw;
+    s.hi = ncell * (x + 1) / kXcds;
+    s.step = static_cast<int64_t>(nbx) * (kBlock / kWave);
+    return s;
+}
+
+// Wave-uniform candidate runs of cell (cx, cy, cz): run k covers positions
+// [pre[k], pre[k] + len_k) of the flattened candidate sequence, starting at
+// cell-ordered index b[k].  Returns the number of candidates.
+__device__ __forceinline__ int32_t cell_runs(const Params &p, const int64_t *__restrict__ start, int cx, int cy,
+                                             int cz, int32_t (&b)[9], int32_t (&pre)[9]) {
+    const int lane = lane_id();
+    const int x0 = cx > 0 ? cx - 1 : 0;
+    const int x1 = cx + 1 < p.dim[0] ? cx + 1 : p.dim[0] - 1;
+    int32_t rb = 0, rl = 0;
+    if (lane < 9) {
+        const int z = cz - 1 + lane / 3;
+        const int y = cy - 1 + lane % 3;
+        if (z >= 0 && z < p.dim[2] && y >= 0 && y < p.dim[1]) {
+            const int rowc = (z * p.dim[1] + y) * p.dim[0];
+            const int64_t s0 = start[rowc + x0];
+            rb = static_cast<int32_t>(s0);
+            rl = static_cast<int32_t>(start[rowc + x1 + 1] - s0);
         }
+    }
+    int32_t total = 0;
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const int d = r * G + g;
-            const int32_t id = __shfl(i, d, kWave);
-            if (s0 + d < n) {
+    for (int k = 0; k < 9; ++k) {
+        b[k] = __builtin_amdgcn_readlane(rb, k);
+        pre[k] = total;
+        total += __builtin_amdgcn_readlane(rl, k);
+    }
+    return total;
+}
+
+// Split factor for a flush over dn destinations with G groups: the largest
+// power of two S with S * dn <= G (1 when dn > G / 2).
+__device__ __forceinline__ int split_for(int dn, int groups) {
+    int s = 1;
+    while (2 * s * dn <= groups) s *= 2;
+    return s;
+}
+
+template <int K>
+__device__ __forceinline__ void load_k(const float *__restrict__ base, int64_t unit, bool ok, float (&v)[K]) {
+    if (ok) {
+        const csr::Vec<K> t = csr::load_unit<K>(base, unit);
 #pragma unroll
-                for (int u = 0; u < UPL; ++u) {
-                    const int64_t unit = fb + q + u * LPR;
-                    if (unit < fu) stg_stream(reinterpret_cast<f32x4 *>(y) + static_cast<int64_t>(id) * fu + unit,
-                                              acc[r][u]);
-                }
-            }
-        }
-        if (fb == 0 && own && count) count[i] = cnt;
+        for (int k = 0; k < K; ++k) v[k] = t.v[k];
+    } else {
+#pragma unroll
+        for (int k = 0; k < K; ++k) v[k] = 0.0f;
     }
 }
 
-// Backward with the same schedule: dx_i = sum_j k_ij dy_j and
-// dp_i = sum_j (2 k_ij / sigma^2) (p_j - p_i) (<dy_i, x_j> + <dy_j, x_i>).
-// Each lane accumulates dp from the part of the inner products its units
-// cover; the LPR partial sums of a destination are added once at the end.
-template <int LPR, int UPL, bool DX, bool DP>
-__global__ __launch_bounds__(kBlock) void radius_bwd_coop_kernel(const Params *__restrict__ prm,
+// Write (first flush of a pass) or accumulate (later flushes) one unit.
+template <int K>
+__device__ __forceinline__ void put_k(float *__restrict__ base, int64_t unit, const float (&v)[K], bool first) {
+    if (first) {
+        csr::store_unit<K>(base, unit, v);
+    } else {
+        const csr::Vec<K> o = csr::load_unit<K>(base, unit);
+        float s[K];
+#pragma unroll
+        for (int k = 0; k < K; ++k) s[k] = o.v[k] + v[k];
+        csr::store_unit<K>(base, unit, s);
+    }
+}
+
+// Phase 1 over every cell of this wave; `flush(cnt, dn, d0, id, first)` runs
+// phase 2 for the destinations d0 .. d0 + dn - 1 (lane d holds the list
+// length `cnt` and point id `id` of destination d).
+template <class Flush>
+__device__ __forceinline__ void cell_consume(const Params &p, const int64_t *__restrict__ start,
+                                             const float4 *__restrict__ rec, float r2, float neg_inv_s2,
+                                             CellList &list, int32_t *__restrict__ count, Flush &&flush) {
+    const int lane = lane_id();
+    const int64_t ncell = p.ncell;
+    for (CellSched sc = cell_sched(ncell); sc.c < sc.hi; sc.c += sc.step) {
+        const int64_t c = sc.c;
+        const int64_t ds = start[c], de = start[c + 1];
+        if (ds == de) continue;
+        const int cx = static_cast<int>(c % p.dim[0]);
+        const int cy = static_cast<int>((c / p.dim[0]) % p.dim[1]);
+        const int cz = static_cast<int>(c / (static_cast<int64_t>(p.dim[0]) * p.dim[1]));
+        int32_t b[9], pre[9];
+        const int32_t total = cell_runs(p, start, cx, cy, cz, b, pre);
+        for (int64_t d0 = ds; d0 < de; d0 += kDch) {
+            const int dn = static_cast<int>(de - d0 < kDch ? de - d0 : kDch);
+            const int32_t idl = lane < dn ? __float_as_int(rec[d0 + lane].w) : -1;
+            int cnt = 0, tot = 0;
+            bool first = true;
+            for (int32_t c0 = 0; c0 < total; c0 += kWave) {
+                const int32_t pos = c0 + lane;
+                const bool inr = pos < total;
+                int32_t t = 0;
+#pragma unroll
+                for (int k = 0; k < 9; ++k)
+                    if (pos >= pre[k]) t = b[k] + (pos - pre[k]);
+                const float4 pj = inr ? rec[t] : make_float4(0.0f, 0.0f, 0.0f, __int_as_float(-1));
+                for (int d = 0; d < dn; ++d) {
+                    const float4 pd = rec[d0 + d];  // uniform address: a scalar load
+                    float d2;
+                    const bool near = accept(pd, pj, r2, d2);
+                    const bool ok = inr & near & (__float_as_int(pj.w) != __float_as_int(pd.w));
+                    const uint64_t mask = __builtin_amdgcn_ballot_w64(ok);
+                    if (mask == 0) continue;
+                    const int nnew = __popcll(mask);
+                    int cd = __builtin_amdgcn_readlane(cnt, d);
+                    if (cd + nnew > kCapC) {
+                        tot += cnt;
+                        flush(cnt, dn, d0, idl, first);
+                        first = false;
+                        cnt = 0;
+                        cd = 0;
+                    }
+                    if (ok) {
+                        const int pfx = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                                                  __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0));
+                        list[d][cd + pfx] = make_float2(__int_as_float(t), __expf(d2 * neg_inv_s2));
+                    }
+                    cnt = lane == d ? cd + nnew : cnt;
+                }
+            }
+            tot += cnt;
+            flush(cnt, dn, d0, idl, first);
+            if (count && lane < dn) count[idl] = tot;
+        }
+    }
+}
+
+// y_i = sum_j k_ij x_j; K floats per unit, LPR lanes per row, UPL units per
+// lane per feature block.
+template <int K, int LPR, int UPL>
+__global__ __launch_bounds__(kBlock) void radius_fwd_cell_kernel(const Params *__restrict__ prm,
                                                                  const int64_t *__restrict__ start,
                                                                  const float4 *__restrict__ rec,
-                                                                 const float *__restrict__ xs,
-                                                                 const float *__restrict__ ys, int64_t n, int64_t fu,
-                                                                 float r2, float neg_inv_s2, float two_inv_s2,
-                                                                 float *__restrict__ dx, float *__restrict__ dp) {
+                                                                 const float *__restrict__ xs, int64_t fu, float r2,
+                                                                 float neg_inv_s2, float *__restrict__ y,
+                                                                 int32_t *__restrict__ count) {
     constexpr int G = kWave / LPR;
-    constexpr int R = LPR;
-    constexpr int B = DP ? kBatchDp : kBatch;
-    __shared__ float2 lists[kBlock / kWave][kCap][kWave];
+    __shared__ CellList lists[kBlock / kWave];
     const Params p = *prm;
-    const int lane = lane_id(), wv = threadIdx.x / kWave;
-    const int g = lane / LPR, q = lane % LPR;
-    const int64_t s0 = (static_cast<int64_t>(xcd_block()) * (kBlock / kWave) + wv) * kWave;
-    if (s0 >= n) return;
-    const int64_t s = s0 + lane;
-    const bool own = s < n;
-    const float4 pi = own ? rec[s] : make_float4(0.0f, 0.0f, 0.0f, __int_as_float(-1));
-    const int32_t i = __float_as_int(pi.w);
-    float gp[R][3];
+    CellList &list = lists[threadIdx.x / kWave];
+    const int lane = lane_id(), g = lane / LPR, q = lane % LPR;
+    const uint32_t ufu = static_cast<uint32_t>(fu);  // n * fu < 2^32 (checked by the host)
+    auto flush = [&](int cnt, int dn, int64_t, int32_t idl, bool first) {
+        lds_fence();
+        const int S = split_for(dn, G);
+        const int D = G / S;
+        const int slot = g % D, sp = g / D;
+        for (int r0 = 0; r0 < dn; r0 += D) {
+            const int d = r0 + slot;
+            const bool dv = d < dn;
+            // every lane takes part in the shuffles: a lane outside the exec
+            // mask would read as zero
+            const int mds = __shfl(cnt, dv ? d : 0, kWave);
+            const int md = dv ? mds : 0;
+            const int32_t id = __shfl(idl, dv ? d : 0, kWave);
+            if (!first && __ballot(md > 0) == 0) continue;
+            for (int64_t fb = 0; fb < fu; fb += LPR * UPL) {
+                const uint32_t ufb = static_cast<uint32_t>(fb);
+                float acc[UPL][K];
 #pragma unroll
-    for (int r = 0; r < R; ++r) gp[r][0] = gp[r][1] = gp[r][2] = 0.0f;
-    for (int64_t fb = 0; fb < fu; fb += LPR * UPL) {
-        f32x4 acc[R][UPL];
+                for (int u = 0; u < UPL; ++u)
 #pragma unroll
-        for (int r = 0; r < R; ++r)
+                    for (int k = 0; k < K; ++k) acc[u][k] = 0.0f;
+                // units past the row end (fu not a multiple of LPR) load the
+                // last unit instead; their sums are never stored
+                uint32_t uc[UPL];
 #pragma unroll
-            for (int u = 0; u < UPL; ++u) acc[r][u] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-        Cursor c;
-        bool live = own && open_cursor(p, start, pi, c);
-        while (true) {
-            const int m = fill_list(p, start, rec, pi, i, r2, neg_inv_s2, c, live, lists[wv], lane);
-            lds_fence();
+                for (int u = 0; u < UPL; ++u) {
+                    const uint32_t unit = ufb + q + u * LPR;
+                    uc[u] = unit < ufu ? unit : ufu - 1;
+                }
+                // FULL: all kBatch entries exist, no per-entry masks
+                auto batch = [&](int k0, auto full) __attribute__((always_inline)) {
+                    constexpr bool FULL = decltype(full)::value;
+                    float2 en[kBatch];
 #pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const int d = r * G + g;
-                const int md = __shfl(m, d, kWave);
-                if (md == 0) continue;
-                const int64_t sd = s0 + d;
-                f32x4 gi[UPL], xi[UPL];
-                float4 pd;
-                if (DP) {
-                    pd = rec[sd];
+                    for (int b = 0; b < kBatch; ++b)
+                        en[b] = FULL || k0 + b * S < md ? list[d][k0 + b * S] : make_float2(0.0f, 0.0f);
+                    float xv[kBatch][UPL][K];
+#pragma unroll
+                    for (int b = 0; b < kBatch; ++b) {
+                        const uint32_t row = static_cast<uint32_t>(__float_as_int(en[b].x)) * ufu;
+#pragma unroll
+                        for (int u = 0; u < UPL; ++u) load_k<K>(xs, row + uc[u], FULL || k0 + b * S < md, xv[b][u]);
+                    }
+#pragma unroll
+                    for (int b = 0; b < kBatch; ++b)
+#pragma unroll
+                        for (int u = 0; u < UPL; ++u)
+#pragma unroll
+                            for (int k = 0; k < K; ++k) acc[u][k] = fmaf(en[b].y, xv[b][u][k], acc[u][k]);
+                };
+                int k0 = sp;
+                for (; k0 + (kBatch - 1) * S < md; k0 += S * kBatch) batch(k0, std::true_type{});
+                if (k0 < md) batch(k0, std::false_type{});
+                for (int o = D * LPR; o < kWave; o <<= 1)
+#pragma unroll
+                    for (int u = 0; u < UPL; ++u)
+#pragma unroll
+                        for (int k = 0; k < K; ++k) acc[u][k] += shfl_xor_f(acc[u][k], o);
+                if (sp == 0 && dv) {
 #pragma unroll
                     for (int u = 0; u < UPL; ++u) {
                         const int64_t unit = fb + q + u * LPR;
-                        const bool ok = unit < fu;
-                        gi[u] = ok ? unit4(ys, sd * fu + unit) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-                        xi[u] = ok ? unit4(xs, sd * fu + unit) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                        if (unit < fu) put_k<K>(y, static_cast<int64_t>(id) * fu + unit, acc[u], first);
                     }
                 }
-                for (int k0 = 0; k0 < md; k0 += B) {
+            }
+        }
+        lds_fence();
+    };
+    cell_consume(p, start, rec, r2, neg_inv_s2, list, count, flush);
+}
+
+// Backward on the same schedule: dx_i = sum_j k_ij dy_j and
+// dp_i = sum_j (2 k_ij / sigma^2) (p_j - p_i) (<dy_i, x_j> + <dy_j, x_i>).
+// Each lane forms the part of the inner products its units cover; the parts
+// of a destination are added by the shuffle tree once per flush.
+template <int K, int LPR, int UPL, bool DX, bool DP>
+__global__ __launch_bounds__(kBlock) void radius_bwd_cell_kernel(const Params *__restrict__ prm,
+                                                                 const int64_t *__restrict__ start,
+                                                                 const float4 *__restrict__ rec,
+                                                                 const float *__restrict__ xs,
+                                                                 const float *__restrict__ ys, int64_t fu, float r2,
+                                                                 float neg_inv_s2, float two_inv_s2,
+                                                                 float *__restrict__ dx, float *__restrict__ dp) {
+    constexpr int G = kWave / LPR;
+    constexpr int B = DP ? kBatchDp : kBatch;
+    __shared__ CellList lists[kBlock / kWave];
+    const Params p = *prm;
+    CellList &list = lists[threadIdx.x / kWave];
+    const int lane = lane_id(), g = lane / LPR, q = lane % LPR;
+    const uint32_t ufu = static_cast<uint32_t>(fu);  // n * fu < 2^32 (checked by the host)
+    auto flush = [&](int cnt, int dn, int64_t d0, int32_t idl, bool first) {
+        lds_fence();
+        const int S = split_for(dn, G);
+        const int D = G / S;
+        const int slot = g % D, sp = g / D;
+        for (int r0 = 0; r0 < dn; r0 += D) {
+            const int d = r0 + slot;
+            const bool dv = d < dn;
+            // every lane takes part in the shuffles: a lane outside the exec
+            // mask would read as zero
+            const int mds = __shfl(cnt, dv ? d : 0, kWave);
+            const int md = dv ? mds : 0;
+            const int32_t id = __shfl(idl, dv ? d : 0, kWave);
+            if (!first && __ballot(md > 0) == 0) continue;
+            const int64_t sd = d0 + (dv ? d : 0);
+            const float4 pd = DP ? rec[sd] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);  // sd is a valid point
+            float gp[3] = {0.0f, 0.0f, 0.0f};
+            for (int64_t fb = 0; fb < fu; fb += LPR * UPL) {
+                const uint32_t ufb = static_cast<uint32_t>(fb);
+                float acc[UPL][K], gi[UPL][K], xi[UPL][K];
+#pragma unroll
+                for (int u = 0; u < UPL; ++u) {
+                    const int64_t unit = fb + q + u * LPR;
+                    const bool ok = DP && dv && unit < fu;
+                    const int64_t at = ok ? sd * fu + unit : 0;
+                    const csr::Vec<K> a = csr::load_unit<K>(ys, at);
+                    const csr::Vec<K> c = csr::load_unit<K>(xs, at);
+#pragma unroll
+                    for (int k = 0; k < K; ++k) {
+                        gi[u][k] = ok ? a.v[k] : 0.0f;
+                        xi[u][k] = ok ? c.v[k] : 0.0f;
+                        acc[u][k] = 0.0f;
+                    }
+                }
+                // units past the row end (fu not a multiple of LPR) load the
+                // last unit instead and take no part in the inner products
+                uint32_t uc[UPL];
+                bool uok[UPL];
+#pragma unroll
+                for (int u = 0; u < UPL; ++u) {
+                    const uint32_t unit = ufb + q + u * LPR;
+                    uok[u] = unit < ufu;
+                    uc[u] = uok[u] ? unit : ufu - 1;
+                }
+                auto batch = [&](int k0, auto full) __attribute__((always_inline)) {
+                    constexpr bool FULL = decltype(full)::value;
                     float2 en[B];
 #pragma unroll
-                    for (int b = 0; b < B; ++b) en[b] = k0 + b < md ? lists[wv][k0 + b][d] : make_float2(0.0f, 0.0f);
-                    f32x4 gj[B][UPL], xj[B][UPL];
-                    float4 pj[B];
+                    for (int b = 0; b < B; ++b)
+                        en[b] = FULL || k0 + b * S < md ? list[d][k0 + b * S] : make_float2(0.0f, 0.0f);
+                    float gj[B][UPL][K], xj[B][UPL][K];
+                    f32x4 pj[B];
 #pragma unroll
                     for (int b = 0; b < B; ++b) {
-                        const bool live_b = k0 + b < md;
-                        const int64_t t = __float_as_int(en[b].x);
-                        const int64_t row = t * fu + fb + q;
+                        const bool live = FULL || k0 + b * S < md;
+                        const uint32_t t = static_cast<uint32_t>(__float_as_int(en[b].x));
 #pragma unroll
                         for (int u = 0; u < UPL; ++u) {
-                            const bool ok = live_b && fb + q + u * LPR < fu;
-                            gj[b][u] = ok ? unit4(ys, row + u * LPR) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-                            if (DP) xj[b][u] = ok ? unit4(xs, row + u * LPR) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                            load_k<K>(ys, t * ufu + uc[u], live, gj[b][u]);
+                            if (DP) load_k<K>(xs, t * ufu + uc[u], live, xj[b][u]);
                         }
-                        if (DP) pj[b] = live_b ? rec[t] : pd;
+                        if (DP) {
+                            // t is a valid point for every entry (0 past the list end)
+                            const f32x4 v = reinterpret_cast<const f32x4 *>(rec)[t];
+                            pj[b] = live ? v : f32x4{pd.x, pd.y, pd.z, pd.w};
+                        }
                     }
 #pragma unroll
                     for (int b = 0; b < B; ++b) {
                         float dot = 0.0f;
 #pragma unroll
                         for (int u = 0; u < UPL; ++u) {
-                            if (DX) acc[r][u] += en[b].y * gj[b][u];
-                            if (DP) {
-                                const f32x4 a = gi[u] * xj[b][u] + gj[b][u] * xi[u];
-                                dot += (a.x + a.y) + (a.z + a.w);
+                            float du = 0.0f;
+#pragma unroll
+                            for (int k = 0; k < K; ++k) {
+                                if (DX) acc[u][k] = fmaf(en[b].y, gj[b][u][k], acc[u][k]);
+                                if (DP) du = fmaf(gi[u][k], xj[b][u][k], fmaf(gj[b][u][k], xi[u][k], du));
                             }
+                            dot += uok[u] ? du : 0.0f;
                         }
                         if (DP) {
                             const float cc = two_inv_s2 * en[b].y * dot;
-                            gp[r][0] = fmaf(cc, pj[b].x - pd.x, gp[r][0]);
-                            gp[r][1] = fmaf(cc, pj[b].y - pd.y, gp[r][1]);
-                            gp[r][2] = fmaf(cc, pj[b].z - pd.z, gp[r][2]);
+                            gp[0] = fmaf(cc, pj[b].x - pd.x, gp[0]);
+                            gp[1] = fmaf(cc, pj[b].y - pd.y, gp[1]);
+                            gp[2] = fmaf(cc, pj[b].z - pd.z, gp[2]);
+                        }
+                    }
+                };
+                int k0 = sp;
+                for (; k0 + (B - 1) * S < md; k0 += S * B) batch(k0, std::true_type{});
+                if (k0 < md) batch(k0, std::false_type{});
+                if (DX) {
+                    for (int o = D * LPR; o < kWave; o <<= 1)
+#pragma unroll
+                        for (int u = 0; u < UPL; ++u)
+#pragma unroll
+                            for (int k = 0; k < K; ++k) acc[u][k] += shfl_xor_f(acc[u][k], o);
+                    if (sp == 0 && dv) {
+#pragma unroll
+                        for (int u = 0; u < UPL; ++u) {
+                            const int64_t unit = fb + q + u * LPR;
+                            if (unit < fu) put_k<K>(dx, static_cast<int64_t>(id) * fu + unit, acc[u], first);
                         }
                     }
                 }
             }
-            lds_fence();
-            if (__ballot(live) == 0) break;
-        }
-        if (DX) {
+            if (DP) {
 #pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const int d = r * G + g;
-                const int32_t id = __shfl(i, d, kWave);
-                if (s0 + d < n) {
+                for (int o = 1; o < LPR; o <<= 1)
 #pragma unroll
-                    for (int u = 0; u < UPL; ++u) {
-                        const int64_t unit = fb + q + u * LPR;
-                        if (unit < fu)
-                            stg_stream(reinterpret_cast<f32x4 *>(dx) + static_cast<int64_t>(id) * fu + unit,
-                                       acc[r][u]);
-                    }
+                    for (int a = 0; a < 3; ++a) gp[a] += shfl_xor_f(gp[a], o);
+                for (int o = D * LPR; o < kWave; o <<= 1)
+#pragma unroll
+                    for (int a = 0; a < 3; ++a) gp[a] += shfl_xor_f(gp[a], o);
+                if (sp == 0 && q == 0 && dv) {
+                    float *o = dp + static_cast<int64_t>(id) * 3;
+#pragma unroll
+                    for (int a = 0; a < 3; ++a) o[a] = first ? gp[a] : o[a] + gp[a];
                 }
             }
         }
-    }
-    if (DP) {
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-#pragma unroll
-            for (int m = 1; m < LPR; m <<= 1)
-#pragma unroll
-                for (int a = 0; a < 3; ++a) gp[r][a] += shfl_xor_f(gp[r][a], m);
-            const int d = r * G + g;
-            const int32_t id = __shfl(i, d, kWave);
-            if (q == 0 && s0 + d < n)
-#pragma unroll
-                for (int a = 0; a < 3; ++a) dp[static_cast<int64_t>(id) * 3 + a] = gp[r][a];
-        }
-    }
+        lds_fence();
+    };
+    cell_consume(p, start, rec, r2, neg_inv_s2, list, nullptr, flush);
 }
 
 __global__ __launch_bounds__(kBlock) void neighbor_count_kernel(const Params *__restrict__ prm,
@@ -842,63 +821,58 @@ int launch_gather_rows(const int32_t *perm, int64_t n, int64_t fu, const float *
     return check_launch("radius rows");
 }
 
-template <int K>
-int fwd_units(int64_t fu, const Ws &w, const int64_t *start, int64_t n, float r2, float nis, float *y,
-              int32_t *count, hipStream_t stream) {
-    const dim3 grid(static_cast<unsigned>(ceil_div(n, kBlock)));
+// Persistent grid for the cell kernels: a multiple of 8 blocks (one share
+// per XCD), as many as stay resident.
+int cell_grid(const void *kernel) {
+    int64_t blocks = static_cast<int64_t>(resident_blocks(kernel, kBlock)) * device_cus();
+    blocks = blocks / kXcds * kXcds;
+    return static_cast<int>(blocks < kXcds ? kXcds : blocks);
+}
+
+template <int K, int LPR, int UPL>
+int fwd_cell(int64_t fu, const Ws &w, const int64_t *start, float r2, float nis, float *y, int32_t *count,
+             hipStream_t stream) {
+    const void *kern = reinterpret_cast<const void *>(&radius_fwd_cell_kernel<K, LPR, UPL>);
+    static const int grid = cell_grid(kern);
     prof_before(stream);
-    if constexpr (K == 4) {
-#define TIGA_RF(LPR, UPL)                                                                                    \
-    hipLaunchKernelGGL((radius_fwd_coop_kernel<LPR, UPL>), grid, dim3(kBlock), 0, stream, w.prm, start, w.rec, \
-                       w.as, n, fu, r2, nis, y, count)
-        if (fu <= 1) TIGA_RF(1, 1);
-        else if (fu <= 2) TIGA_RF(2, 1);
-        else if (fu <= 4) TIGA_RF(4, 1);
-        else if (fu <= 8) TIGA_RF(8, 1);
-        else TIGA_RF(8, 2);
-#undef TIGA_RF
-    } else {
-#define TIGA_RF(NU)                                                                                            \
-    hipLaunchKernelGGL((radius_fwd_kernel<K, NU>), grid, dim3(kBlock), 0, stream, w.prm, start, w.rec, w.as, n, \
-                       fu, r2, nis, y, count)
-        if (fu <= 1) TIGA_RF(1);
-        else if (fu <= 2) TIGA_RF(2);
-        else if (fu <= 4) TIGA_RF(4);
-        else if (fu <= 8) TIGA_RF(8);
-        else TIGA_RF(16);
-#undef TIGA_RF
-    }
+    hipLaunchKernelGGL((radius_fwd_cell_kernel<K, LPR, UPL>), dim3(grid), dim3(kBlock), 0, stream, w.prm, start,
+                       w.rec, w.as, fu, r2, nis, y, count);
     prof_after(stream);
     return check_launch("radius forward");
 }
 
-template <int K, bool DX, bool DP>
-int bwd_units(int64_t fu, const Ws &w, const int64_t *start, int64_t n, float r2, float nis, float tis, float *dx,
-              float *dp, hipStream_t stream) {
-    const dim3 grid(static_cast<unsigned>(ceil_div(n, kBlock)));
+// Lanes per row: the smallest power of two covering the row's units, at most
+// 8 (16 with two units per lane); wider rows loop over feature blocks.
+template <int K>
+int fwd_units(int64_t fu, const Ws &w, const int64_t *start, float r2, float nis, float *y, int32_t *count,
+              hipStream_t stream) {
+    if (fu <= 1) return fwd_cell<K, 1, 1>(fu, w, start, r2, nis, y, count, stream);
+    if (fu <= 2) return fwd_cell<K, 2, 1>(fu, w, start, r2, nis, y, count, stream);
+    if (fu <= 4) return fwd_cell<K, 4, 1>(fu, w, start, r2, nis, y, count, stream);
+    if (fu <= 8) return fwd_cell<K, 8, 1>(fu, w, start, r2, nis, y, count, stream);
+    return fwd_cell<K, 8, 2>(fu, w, start, r2, nis, y, count, stream);
+}
+
+template <int K, int LPR, int UPL, bool DX, bool DP>
+int bwd_cell(int64_t fu, const Ws &w, const int64_t *start, float r2, float nis, float tis, float *dx, float *dp,
+             hipStream_t stream) {
+    const void *kern = reinterpret_cast<const void *>(&radius_bwd_cell_kernel<K, LPR, UPL, DX, DP>);
+    static const int grid = cell_grid(kern);
     prof_before(stream);
-    if constexpr (K == 4) {
-#define TIGA_RB(LPR, UPL)                                                                                     \
-    hipLaunchKernelGGL((radius_bwd_coop_kernel<LPR, UPL, DX, DP>), grid, dim3(kBlock), 0, stream, w.prm, start, \
-                       w.rec, w.bs, w.as, n, fu, r2, nis, tis, dx, dp)
-        if (fu <= 1) TIGA_RB(1, 1);
-        else if (fu <= 2) TIGA_RB(2, 1);
-        else if (fu <= 4) TIGA_RB(4, 1);
-        else if (fu <= 8) TIGA_RB(8, 1);
-        else TIGA_RB(8, 2);
-#undef TIGA_RB
-    } else {
-#define TIGA_RB(NU)                                                                                          \
-    hipLaunchKernelGGL((radius_bwd_kernel<K, NU, DX, DP>), grid, dim3(kBlock), 0, stream, w.prm, start, w.rec, \
-                       w.bs, w.as, n, fu, r2, nis, tis, dx, dp)
-        if (fu <= 1) TIGA_RB(1);
-        else if (fu <= 2) TIGA_RB(2);
-        else if (fu <= 4) TIGA_RB(4);
-        else TIGA_RB(8);
-#undef TIGA_RB
-    }
+    hipLaunchKernelGGL((radius_bwd_cell_kernel<K, LPR, UPL, DX, DP>), dim3(grid), dim3(kBlock), 0, stream, w.prm,
+                       start, w.rec, w.bs, w.as, fu, r2, nis, tis, dx, dp);
     prof_after(stream);
     return check_launch("radius backward");
+}
+
+template <int K, bool DX, bool DP>
+int bwd_units(int64_t fu, const Ws &w, const int64_t *start, float r2, float nis, float tis, float *dx, float *dp,
+              hipStream_t stream) {
+    if (fu <= 1) return bwd_cell<K, 1, 1, DX, DP>(fu, w, start, r2, nis, tis, dx, dp, stream);
+    if (fu <= 2) return bwd_cell<K, 2, 1, DX, DP>(fu, w, start, r2, nis, tis, dx, dp, stream);
+    if (fu <= 4) return bwd_cell<K, 4, 1, DX, DP>(fu, w, start, r2, nis, tis, dx, dp, stream);
+    if (fu <= 8) return bwd_cell<K, 8, 1, DX, DP>(fu, w, start, r2, nis, tis, dx, dp, stream);
+    return bwd_cell<K, 8, 2, DX, DP>(fu, w, start, r2, nis, tis, dx, dp, stream);
 }
 
 }  // namespace
@@ -909,21 +883,34 @@ size_t workspace_bytes(int64_t n, int64_t feat) {
     return c.bytes();
 }
 
+// The consume kernels index feature units with 32-bit arithmetic.
+int check_units(int64_t n, int64_t fu) {
+    if (static_cast<uint64_t>(n) * static_cast<uint64_t>(fu) >= (uint64_t{1} << 32))
+        return fail(TIGA_EUNSUPPORTED, "radius: n * feature units (%lld * %lld) reaches 2^32",
+                    static_cast<long long>(n), static_cast<long long>(fu));
+    return TIGA_OK;
+}
+
 int forward(int64_t n, int32_t feat, const float *pos, const float *x, float radius, float sigma, float *y,
             int32_t *count, void *ws, hipStream_t stream) {
+    const bool vec = feat % 4 == 0 && aligned16(y);
+    const int64_t fu = vec ? feat / 4 : feat;
+    if (int rc = check_units(n, fu)) return rc;
     Carve c(ws);
     Ws w = carve(c, n, feat);
     if (int rc = build(n, pos, radius, x, nullptr, feat, w, stream)) return rc;
     const int64_t *start = reinterpret_cast<const int64_t *>(w.count);
     const float r2 = radius * radius;
     const float nis = -1.0f / (sigma * sigma);
-    const bool vec = feat % 4 == 0 && aligned16(y);
-    if (vec) return fwd_units<4>(feat / 4, w, start, n, r2, nis, y, count, stream);
-    return fwd_units<1>(feat, w, start, n, r2, nis, y, count, stream);
+    if (vec) return fwd_units<4>(fu, w, start, r2, nis, y, count, stream);
+    return fwd_units<1>(fu, w, start, r2, nis, y, count, stream);
 }
 
 int backward(int64_t n, int32_t feat, const float *pos, const float *x, float radius, float sigma, const float *dy,
              float *dx, float *dpos, void *ws, hipStream_t stream) {
+    const bool vec = feat % 4 == 0 && (!dx || aligned16(dx));
+    const int64_t fu = vec ? feat / 4 : feat;
+    if (int rc = check_units(n, fu)) return rc;
     Carve c(ws);
     Ws w = carve(c, n, feat);
     // as = cell-ordered dy, bs = cell-ordered x (only needed for dpos)
@@ -932,12 +919,10 @@ int backward(int64_t n, int32_t feat, const float *pos, const float *x, float ra
     const float r2 = radius * radius;
     const float nis = -1.0f / (sigma * sigma);
     const float tis = 2.0f / (sigma * sigma);
-    const bool vec = feat % 4 == 0 && (!dx || aligned16(dx));
-    const int64_t fu = vec ? feat / 4 : feat;
-#define TIGA_B(KK)                                                                          \
-    if (dx && dpos) return bwd_units<KK, true, true>(fu, w, start, n, r2, nis, tis, dx, dpos, stream); \
-    if (dx) return bwd_units<KK, true, false>(fu, w, start, n, r2, nis, tis, dx, dpos, stream);        \
-    return bwd_units<KK, false, true>(fu, w, start, n, r2, nis, tis, dx, dpos, stream)
+#define TIGA_B(KK)                                                                                    \
+    if (dx && dpos) return bwd_units<KK, true, true>(fu, w, start, r2, nis, tis, dx, dpos, stream); \
+    if (dx) return bwd_units<KK, true, false>(fu, w, start, r2, nis, tis, dx, dpos, stream);        \
+    return bwd_units<KK, false, true>(fu, w, start, r2, nis, tis, dx, dpos, stream)
     if (vec) {
         TIGA_B(4);
     } else {
