@@ -293,11 +293,12 @@ __device__ __forceinline__ void for_candidates(const Params &p, const int64_t *_
 // destination per group; when the cell has few destinations, S groups share a
 // destination (interleaved entries) and are combined by a fixed shuffle tree.
 // Every summation order depends only on the input.
-constexpr int kDch = 16;     // destinations per pass over a cell's candidates
+constexpr int kDch = 8;      // destinations per pass over a cell's candidates
 constexpr int kCapC = 64;    // list entries per destination between flushes
 constexpr int kBatch = 8;    // list entries whose rows are loaded together
-constexpr int kBatchDp = 4;  // the same when position gradients are formed
+constexpr int kBatchDp = 2;  // the same when position gradients are formed
 
+static_assert(kCapC >= kWave, "one candidate chunk may add a wave's worth of entries after a flush");
 typedef float2 CellList[kDch][kCapC + 1];  // +1: groups reading different lists hit different banks
 
 __device__ __forceinline__ void lds_fence() {
