@@ -29,6 +29,13 @@ int launch_transpose(const tiga_csr *rel, int64_t *src_ptr, int32_t *edge_id, in
 
 int launch_validate(const tiga_csr *rel, hipStream_t stream);
 
+// Stable sort of n keys in [0, key_limit): sorted keys to keys_out, the input
+// position of each to idx_out (ascending within equal keys), and
+// ptr[j] = first sorted position with key >= j for j in [0, key_limit].
+size_t sort_keys_ws_bytes(int64_t n);
+int launch_sort_keys(const int32_t *keys, int64_t n, int64_t key_limit, int32_t *keys_out, int32_t *idx_out,
+                     int64_t *ptr, void *ws, hipStream_t stream);
+
 // Device-wide exclusive prefix sum of n int64 values (in may equal out).
 size_t scan_ws_bytes(int64_t n);
 int launch_excl_scan(const int64_t *in, int64_t *out, int64_t n, void *ws, hipStream_t stream);

@@ -100,7 +100,8 @@ __global__ __launch_bounds__(kBlock) void radix_hist_kernel(const int32_t *__res
 }
 
 // Stable scatter.  Elements of a tile are ranked in (round, wave, lane) order,
-// which is their input order; equal digits keep that order.
+// which is their input order; equal digits keep that order.  The second
+// payload is optional (null in and out).
 __global__ __launch_bounds__(kBlock) void radix_scatter_kernel(
     const int32_t *__restrict__ keys_in, const int32_t *__restrict__ v0_in, const int32_t *__restrict__ v1_in,
     int32_t *__restrict__ keys_out, int32_t *__restrict__ v0_out, int32_t *__restrict__ v1_out, int64_t n,
@@ -123,7 +124,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter_kernel(
         if (valid) {
             key = keys_in[i];
             a = iota_v0 ? static_cast<int32_t>(i) : v0_in[i];
-            b = v1_in[i];
+            b = v1_in ? v1_in[i] : 0;
             digit = (static_cast<uint32_t>(key) >> shift) & (kRadix - 1);
         }
         uint64_t peers = __ballot(valid);
@@ -140,7 +141,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter_kernel(
             for (int w = 0; w < wave; ++w) pos += wcnt[w][digit];
             keys_out[pos] = key;
             v0_out[pos] = a;
-            v1_out[pos] = b;
+            if (v1_out) v1_out[pos] = b;
         }
         __syncthreads();
         int64_t add = 0;
@@ -162,14 +163,19 @@ __global__ __launch_bounds__(kBlock) void expand_rows_kernel(const int64_t *__re
     }
 }
 
-// src_ptr[j] = first sorted position with key >= j.
+// ptr[j] = first sorted position with key >= j, for j in [0, nkeys]: one
+// binary search per j, so long runs of absent keys cost no serial work.
 __global__ __launch_bounds__(kBlock) void ptr_from_sorted_kernel(const int32_t *__restrict__ sorted, int64_t n,
                                                                  int64_t nkeys, int64_t *__restrict__ ptr) {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
-    for (int64_t k = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; k <= n; k += stride) {
-        const int64_t lo = (k == 0) ? -1 : static_cast<int64_t>(sorted[k - 1]);
-        const int64_t hi = (k == n) ? nkeys : static_cast<int64_t>(sorted[k]);
-        for (int64_t j = lo + 1; j <= hi; ++j) ptr[j] = k;
+    for (int64_t j = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; j <= nkeys; j += stride) {
+        int64_t lo = 0, hi = n;
+        while (lo < hi) {
+            const int64_t mid = lo + (hi - lo) / 2;
+            if (static_cast<int64_t>(sorted[mid]) < j) lo = mid + 1;
+            else hi = mid;
+        }
+        ptr[j] = lo;
     }
 }
 
@@ -234,17 +240,57 @@ struct SortWs {
     void *scan;
 };
 
-SortWs carve_sort(Carve &c, int64_t n) {
+SortWs carve_sort(Carve &c, int64_t n, bool payload) {
     SortWs s;
     const int64_t nb = ceil_div(n > 0 ? n : 1, kSortTile);
     for (int i = 0; i < 2; ++i) {
         s.k[i] = c.take<int32_t>(n);
         s.a[i] = c.take<int32_t>(n);
-        s.b[i] = c.take<int32_t>(n);
+        s.b[i] = payload ? c.take<int32_t>(n) : nullptr;
     }
     s.counts = c.take<int64_t>(nb * kRadix);
     s.scan = c.take<char>(scan_ws_bytes(nb * kRadix));
     return s;
+}
+
+// Stable LSD radix sort of n keys in [0, key_limit), 8 bits per pass.  Carries
+// the input position of every key (to idx_out) and optionally one payload
+// (pay -> pay_out).  The sorted keys go to keys_out when given; *sorted points
+// at them in any case.
+int radix_sort(const int32_t *keys, const int32_t *pay, int64_t n, int64_t key_limit, int32_t *keys_out,
+               int32_t *idx_out, int32_t *pay_out, const SortWs &s, const int32_t **sorted, hipStream_t stream) {
+    int bits = 1;
+    while (bits < 31 && (int64_t{1} << bits) < key_limit) ++bits;
+    const int passes = (bits + kRadixBits - 1) / kRadixBits;
+    const int64_t nb = ceil_div(n, kSortTile);
+    const int32_t *kin = keys, *ain = nullptr, *bin = pay;
+    for (int p = 0; p < passes; ++p) {
+        const int shift = p * kRadixBits;
+        hipLaunchKernelGGL(radix_hist_kernel, dim3(static_cast<unsigned>(nb)), dim3(kBlock), 0, stream, kin, n, shift,
+                           nb, s.counts);
+        if (int rc = check_launch("radix histogram")) return rc;
+        if (int rc = launch_excl_scan(s.counts, s.counts, nb * kRadix, s.scan, stream)) return rc;
+        // ping-pong through the workspace; the last pass writes the caller's arrays
+        const bool last = p == passes - 1;
+        const int buf = p & 1;
+        int32_t *ko = last && keys_out ? keys_out : s.k[buf];
+        int32_t *ao = last ? idx_out : s.a[buf];
+        int32_t *bo = pay ? (last ? pay_out : s.b[buf]) : nullptr;
+        hipLaunchKernelGGL(radix_scatter_kernel, dim3(static_cast<unsigned>(nb)), dim3(kBlock), 0, stream, kin, ain,
+                           bin, ko, ao, bo, n, shift, nb, s.counts, p == 0 ? 1 : 0);
+        if (int rc = check_launch("radix scatter")) return rc;
+        kin = ko;
+        ain = ao;
+        bin = bo;
+    }
+    *sorted = kin;
+    return TIGA_OK;
+}
+
+int ptr_from_sorted(const int32_t *sorted, int64_t n, int64_t nkeys, int64_t *ptr, hipStream_t stream) {
+    const int pb = persistent_blocks(ceil_div(nkeys + 1, kWave), 8);
+    hipLaunchKernelGGL(ptr_from_sorted_kernel, dim3(pb), dim3(kBlock), 0, stream, sorted, n, nkeys, ptr);
+    return check_launch("pointers from sorted keys");
 }
 }  // namespace
 
@@ -252,7 +298,7 @@ size_t transpose_ws_bytes(int64_t num_dst, int64_t num_src, int64_t num_edges) {
     (void)num_dst;
     (void)num_src;
     Carve c(nullptr);
-    carve_sort(c, num_edges);
+    carve_sort(c, num_edges, true);
     return c.bytes();
 }
 
@@ -260,44 +306,33 @@ int launch_transpose(const tiga_csr *rel, int64_t *src_ptr, int32_t *edge_id, in
                      hipStream_t stream) {
     const int64_t n = rel->num_edges;
     Carve c(ws);
-    SortWs s = carve_sort(c, n);
-    if (n > 0) {
-        const int eb = persistent_blocks(rel->num_dst, 8);
-        hipLaunchKernelGGL(expand_rows_kernel, dim3(eb), dim3(kBlock), 0, stream, rel->row_ptr, rel->num_dst, s.b[0]);
-        if (int rc = check_launch("expand rows")) return rc;
-        int bits = 1;
-        while (bits < 31 && (int64_t{1} << bits) < rel->num_src) ++bits;
-        const int passes = (bits + kRadixBits - 1) / kRadixBits;
-        const int64_t nb = ceil_div(n, kSortTile);
-        const int32_t *kin = rel->col_idx;
-        int cur = 0;
-        for (int p = 0; p < passes; ++p) {
-            const int shift = p * kRadixBits;
-            hipLaunchKernelGGL(radix_hist_kernel, dim3(static_cast<unsigned>(nb)), dim3(kBlock), 0, stream, kin, n,
-                               shift, nb, s.counts);
-            if (int rc = check_launch("radix histogram")) return rc;
-            if (int rc = launch_excl_scan(s.counts, s.counts, nb * kRadix, s.scan, stream)) return rc;
-            // the last pass writes straight into the caller's arrays
-            const bool last = p == passes - 1;
-            int32_t *ko = s.k[cur ^ 1];
-            int32_t *ao = last ? edge_id : s.a[cur ^ 1];
-            int32_t *bo = last ? dst_idx : s.b[cur ^ 1];
-            const int32_t *ai = s.a[cur];
-            const int32_t *bi = s.b[cur];
-            hipLaunchKernelGGL(radix_scatter_kernel, dim3(static_cast<unsigned>(nb)), dim3(kBlock), 0, stream, kin,
-                               ai, bi, ko, ao, bo, n, shift, nb, s.counts, p == 0 ? 1 : 0);
-            if (int rc = check_launch("radix scatter")) return rc;
-            kin = ko;
-            cur ^= 1;
-            if (!last) {
-                // the payloads of the next pass come from the buffers just written
-            }
-        }
-        const int pb = persistent_blocks(ceil_div(n + 1, kWave), 8);
-        hipLaunchKernelGGL(ptr_from_sorted_kernel, dim3(pb), dim3(kBlock), 0, stream, kin, n, rel->num_src, src_ptr);
-        return check_launch("source pointers");
-    }
-    return fill_u32(src_ptr, 0u, 2 * (rel->num_src + 1), stream);
+    SortWs s = carve_sort(c, n, true);
+    if (n == 0) return fill_u32(src_ptr, 0u, 2 * (rel->num_src + 1), stream);
+    // destination of every edge position, sorted along as the payload; the
+    // first pass reads it from the second ping-pong buffer
+    const int eb = persistent_blocks(rel->num_dst, 8);
+    hipLaunchKernelGGL(expand_rows_kernel, dim3(eb), dim3(kBlock), 0, stream, rel->row_ptr, rel->num_dst, s.b[1]);
+    if (int rc = check_launch("expand rows")) return rc;
+    const int32_t *sorted = nullptr;
+    if (int rc = radix_sort(rel->col_idx, s.b[1], n, rel->num_src, nullptr, edge_id, dst_idx, s, &sorted, stream))
+        return rc;
+    return ptr_from_sorted(sorted, n, rel->num_src, src_ptr, stream);
+}
+
+size_t sort_keys_ws_bytes(int64_t n) {
+    Carve c(nullptr);
+    carve_sort(c, n, false);
+    return c.bytes();
+}
+
+int launch_sort_keys(const int32_t *keys, int64_t n, int64_t key_limit, int32_t *keys_out, int32_t *idx_out,
+                     int64_t *ptr, void *ws, hipStream_t stream) {
+    Carve c(ws);
+    SortWs s = carve_sort(c, n, false);
+    const int32_t *sorted = nullptr;
+    if (n > 0)
+        if (int rc = radix_sort(keys, nullptr, n, key_limit, keys_out, idx_out, nullptr, s, &sorted, stream)) return rc;
+    return ptr_from_sorted(n > 0 ? sorted : keys_out, n, key_limit, ptr, stream);
 }
 
 int launch_validate(const tiga_csr *rel, hipStream_t stream) {

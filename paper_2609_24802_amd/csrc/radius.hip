@@ -4,12 +4,12 @@
 //
 // Build (every call, stateless):
 //   bounding box -> cell size h >= r (1 + 2^-10), at most n + 64 cells ->
-//   cell id per point (fp64 coordinates) -> counts -> exclusive scan ->
-//   scatter (counting sort) -> per-cell sort by point id (deterministic order)
-//   -> cell-ordered records (p, id) and feature rows.
-// Consume: one thread per destination point in cell order; the 27 neighbour
-// cells are 9 contiguous runs of the cell-ordered arrays (x-adjacent cells are
-// adjacent in memory).
+//   cell id per point (fp64 coordinates) -> stable radix sort of the cell ids
+//   (ascending point ids within a cell: a deterministic order) -> cell
+//   boundaries -> cell-ordered records (p, id) and feature rows.
+// Consume: one wavefront per destination cell; the 27 neighbour cells are 9
+// contiguous runs of the cell-ordered arrays (x-adjacent cells are adjacent
+// in memory).
 #include "csr_bwd.hpp"
 #include "radius.hpp"
 
@@ -150,58 +150,16 @@ __device__ __forceinline__ int cell_axis(const Params &p, int a, float v) {
     return c;
 }
 
-__global__ __launch_bounds__(kBlock) void cell_count_kernel(const float *__restrict__ pos, int64_t n,
-                                                            const Params *__restrict__ prm,
-                                                            int32_t *__restrict__ cell,
-                                                            unsigned long long *__restrict__ count) {
+// Cell id of every point (z-major, x fastest).
+__global__ __launch_bounds__(kBlock) void cell_key_kernel(const float *__restrict__ pos, int64_t n,
+                                                          const Params *__restrict__ prm, int32_t *__restrict__ cell) {
     const Params p = *prm;
     const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
     for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
         const int cx = cell_axis(p, 0, pos[i * 3 + 0]);
         const int cy = cell_axis(p, 1, pos[i * 3 + 1]);
         const int cz = cell_axis(p, 2, pos[i * 3 + 2]);
-        const int c = (cz * p.dim[1] + cy) * p.dim[0] + cx;
-        cell[i] = c;
-        atomicAdd(&count[c], 1ull);
-    }
-}
-
-__global__ __launch_bounds__(kBlock) void cell_scatter_kernel(const int32_t *__restrict__ cell, int64_t n,
-                                                              const int64_t *__restrict__ start,
-                                                              unsigned int *__restrict__ cursor,
-                                                              int32_t *__restrict__ perm) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
-        const int c = cell[i];
-        perm[start[c] + atomicAdd(&cursor[c], 1u)] = static_cast<int32_t>(i);
-    }
-}
-
-// Sort the point ids of each cell ascending so that the candidate order (and
-// hence every summation order) depends only on the input.  A wavefront per
-// cell computes each element's rank; cells beyond kSortMax points keep the
-// order of the scatter (still correct, not bit-reproducible).
-constexpr int kSortMax = 4096;
-
-__global__ __launch_bounds__(kBlock) void cell_sort_kernel(const int64_t *__restrict__ start,
-                                                           const Params *__restrict__ prm,
-                                                           const int32_t *__restrict__ perm_in,
-                                                           int32_t *__restrict__ perm_out) {
-    const int ncell = prm->ncell;
-    const int64_t wave = static_cast<int64_t>(blockIdx.x) * (kBlock / kWave) + threadIdx.x / kWave;
-    const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (kBlock / kWave);
-    for (int64_t c = wave; c < ncell; c += nwaves) {
-        const int64_t b = start[c], e = start[c + 1], d = e - b;
-        if (d > kSortMax) {
-            for (int64_t k = b + lane_id(); k < e; k += kWave) perm_out[k] = perm_in[k];
-            continue;
-        }
-        for (int64_t k = b + lane_id(); k < e; k += kWave) {
-            const int32_t v = perm_in[k];
-            int64_t rank = 0;
-            for (int64_t m = b; m < e; ++m) rank += perm_in[m] < v;
-            perm_out[b + rank] = v;
-        }
+        cell[i] = (cz * p.dim[1] + cy) * p.dim[0] + cx;
     }
 }
 
@@ -739,12 +697,12 @@ __global__ __launch_bounds__(kBlock) void neighbor_fill_kernel(const Params *__r
 struct Ws {
     Params *prm;
     float *bbox;
-    int32_t *cell;
-    unsigned long long *count;  // ncell_max + 1, scanned in place into `start`
-    unsigned int *cursor;
-    int32_t *perm_a, *perm_b;
+    int32_t *cell, *cell_sorted;
+    int32_t *perm_b;  // point id at each cell-ordered position
+    int64_t *start;   // max_cells + 1 cell boundaries in cell order
     float4 *rec;
     float *as, *bs;
+    void *sort;
     void *scan;
     int64_t max_cells;
     int bbox_blocks;
@@ -757,14 +715,14 @@ Ws carve(Carve &c, int64_t n, int64_t feat) {
     w.prm = c.take<Params>(1);
     w.bbox = c.take<float>(6 * w.bbox_blocks);
     w.cell = c.take<int32_t>(n);
-    w.count = c.take<unsigned long long>(w.max_cells + 1);
-    w.cursor = c.take<unsigned int>(w.max_cells);
-    w.perm_a = c.take<int32_t>(n);
+    w.cell_sorted = c.take<int32_t>(n);
     w.perm_b = c.take<int32_t>(n);
+    w.start = c.take<int64_t>(w.max_cells + 1);
     w.rec = c.take<float4>(n);
     w.as = c.take<float>(n * feat);
     w.bs = c.take<float>(n * feat);
-    w.scan = c.take<char>(scan_ws_bytes(w.max_cells + 1));
+    w.sort = c.take<char>(csr::sort_keys_ws_bytes(n));
+    w.scan = c.take<char>(scan_ws_bytes(n + 1));
     return w;
 }
 
@@ -785,19 +743,12 @@ int build(int64_t n, const float *pos, float radius, const float *a, const float
     hipLaunchKernelGGL(grid_params_kernel, dim3(1), dim3(kBlock), 0, stream, w.bbox, nb, n, radius, w.max_cells,
                        w.prm);
     if (int rc = check_launch("radius grid")) return rc;
-    if (int rc = fill_u32(w.count, 0u, 2 * (w.max_cells + 1), stream)) return rc;
-    if (int rc = fill_u32(w.cursor, 0u, w.max_cells, stream)) return rc;
-    hipLaunchKernelGGL(cell_count_kernel, dim3(blocks_for(n)), dim3(kBlock), 0, stream, pos, n, w.prm, w.cell,
-                       w.count);
-    if (int rc = check_launch("radius cell count")) return rc;
-    int64_t *start = reinterpret_cast<int64_t *>(w.count);
-    if (int rc = launch_excl_scan(start, start, w.max_cells + 1, w.scan, stream)) return rc;
-    hipLaunchKernelGGL(cell_scatter_kernel, dim3(blocks_for(n)), dim3(kBlock), 0, stream, w.cell, n, start,
-                       w.cursor, w.perm_a);
-    if (int rc = check_launch("radius scatter")) return rc;
-    hipLaunchKernelGGL(cell_sort_kernel, dim3(blocks_for(w.max_cells * kWave)), dim3(kBlock), 0, stream, start, w.prm,
-                       w.perm_a, w.perm_b);
-    if (int rc = check_launch("radius cell sort")) return rc;
+    // cell-ordered positions: a stable sort by cell keeps ascending point ids
+    // within a cell, so every candidate order depends only on the input
+    hipLaunchKernelGGL(cell_key_kernel, dim3(blocks_for(n)), dim3(kBlock), 0, stream, pos, n, w.prm, w.cell);
+    if (int rc = check_launch("radius cell keys")) return rc;
+    if (int rc = csr::launch_sort_keys(w.cell, n, w.max_cells, w.cell_sorted, w.perm_b, w.start, w.sort, stream))
+        return rc;
     hipLaunchKernelGGL(gather_records_kernel, dim3(blocks_for(n)), dim3(kBlock), 0, stream, w.perm_b, n, pos, w.rec);
     if (int rc = check_launch("radius records")) return rc;
     if (feat > 0 && (a || b)) {
@@ -900,7 +851,7 @@ int forward(int64_t n, int32_t feat, const float *pos, const float *x, float rad
     Carve c(ws);
     Ws w = carve(c, n, feat);
     if (int rc = build(n, pos, radius, x, nullptr, feat, w, stream)) return rc;
-    const int64_t *start = reinterpret_cast<const int64_t *>(w.count);
+    const int64_t *start = w.start;
     const float r2 = radius * radius;
     const float nis = -1.0f / (sigma * sigma);
     if (vec) return fwd_units<4>(fu, w, start, r2, nis, y, count, stream);
@@ -916,7 +867,7 @@ int backward(int64_t n, int32_t feat, const float *pos, const float *x, float ra
     Ws w = carve(c, n, feat);
     // as = cell-ordered dy, bs = cell-ordered x (only needed for dpos)
     if (int rc = build(n, pos, radius, dy, dpos ? x : nullptr, feat, w, stream)) return rc;
-    const int64_t *start = reinterpret_cast<const int64_t *>(w.count);
+    const int64_t *start = w.start;
     const float r2 = radius * radius;
     const float nis = -1.0f / (sigma * sigma);
     const float tis = 2.0f / (sigma * sigma);
@@ -937,7 +888,7 @@ int neighbors(int64_t n, const float *pos, float radius, int32_t *count, int64_t
     Carve c(ws);
     Ws w = carve(c, n, 0);
     if (int rc = build(n, pos, radius, nullptr, nullptr, 0, w, stream)) return rc;
-    const int64_t *start = reinterpret_cast<const int64_t *>(w.count);
+    const int64_t *start = w.start;
     const float r2 = radius * radius;
     const dim3 grid(static_cast<unsigned>(ceil_div(n, kBlock)));
     if (!nbr_idx) {
