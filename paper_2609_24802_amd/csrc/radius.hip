@@ -163,8 +163,7 @@ __global__ __launch_bounds__(kBlock) void cell_key_kernel(const float *__restric
     }
 }
 
-// Cell-ordered records and feature rows (one thread per 16-byte unit when the
-// width allows it, else per float).
+// Cell-ordered records (position, point id).
 __global__ __launch_bounds__(kBlock) void gather_records_kernel(const int32_t *__restrict__ perm, int64_t n,
                                                                 const float *__restrict__ pos,
                                                                 float4 *__restrict__ rec) {
@@ -175,31 +174,6 @@ __global__ __launch_bounds__(kBlock) void gather_records_kernel(const int32_t *_
     }
 }
 
-// I is the index type of the (row, unit) enumeration: 32-bit division when the
-// product fits, which is the common case.
-template <int K, class I>
-__global__ __launch_bounds__(kBlock) void gather_rows_kernel(const int32_t *__restrict__ perm, I total, I fu,
-                                                             const float *__restrict__ a, const float *__restrict__ b,
-                                                             float *__restrict__ as, float *__restrict__ bs) {
-    const I stride = static_cast<I>(gridDim.x) * blockDim.x;
-    for (I k = static_cast<I>(blockIdx.x) * blockDim.x + threadIdx.x; k < total; k += stride) {
-        const I s = k / fu;
-        const I u = k - s * fu;
-        const int64_t src = static_cast<int64_t>(perm[s]) * fu + u;
-        if (a) {
-            const csr::Vec<K> v = csr::load_unit<K>(a, src);
-            csr::store_unit<K>(as, static_cast<int64_t>(k), v.v);
-        }
-        if (b) {
-            const csr::Vec<K> v = csr::load_unit<K>(b, src);
-            csr::store_unit<K>(bs, static_cast<int64_t>(k), v.v);
-        }
-    }
-}
-
-template <int K>
-int launch_gather_rows(const int32_t *perm, int64_t n, int64_t fu, const float *a, const float *b, float *as,
-                       float *bs, hipStream_t stream);
 
 // Exact membership test: direct fp32 differences, products and sums, each
 // rounded once (no contraction), strict comparison with fp32(r*r).
@@ -244,13 +218,14 @@ __device__ __forceinline__ void for_candidates(const Params &p, const int64_t *_
 // Phase 1: the wave loads 64 candidates at a time (one per lane, coalesced)
 // and tests them against each destination of the cell in turn (up to kDch
 // destinations per pass); the accepted lanes of a destination append
-// (cell-ordered index, kernel weight) to that destination's LDS list in
-// candidate order (ballot + prefix count).  Phase 2 (a flush, when a list
-// would overflow and at the end of the pass): lane groups of LPR lanes read
-// each listed neighbour's feature row as LPR consecutive units, one
-// destination per group; when the cell has few destinations, S groups share a
-// destination (interleaved entries) and are combined by a fixed shuffle tree.
-// Every summation order depends only on the input.
+// (point id, kernel weight) to that destination's LDS list in candidate order
+// (ballot + prefix count).  Phase 2 (a flush, when a list would overflow and
+// at the end of the pass): lane groups of LPR lanes read each listed
+// neighbour's feature row in place (caller's layout, no reordered copy) as
+// LPR consecutive units, one destination per group; when the cell has few
+// destinations, S groups share a destination (interleaved entries) and are
+// combined by a fixed shuffle tree.  Every summation order depends only on the
+// input.
 constexpr int kDch = 8;      // destinations per pass over a cell's candidates
 constexpr int kCapC = 64;    // list entries per destination between flushes
 constexpr int kBatch = 8;    // list entries whose rows are loaded together
@@ -400,7 +375,7 @@ __device__ __forceinline__ void cell_consume(const Params &p, const int64_t *__r
                     if (ok) {
                         const int pfx = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
                                                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0));
-                        list[d][cd + pfx] = make_float2(__int_as_float(t), __expf(d2 * neg_inv_s2));
+                        list[d][cd + pfx] = make_float2(pj.w, __expf(d2 * neg_inv_s2));  // (point id, weight)
                     }
                     cnt = lane == d ? cd + nnew : cnt;
                 }
@@ -507,6 +482,7 @@ template <int K, int LPR, int UPL, bool DX, bool DP>
 __global__ __launch_bounds__(kBlock) void radius_bwd_cell_kernel(const Params *__restrict__ prm,
                                                                  const int64_t *__restrict__ start,
                                                                  const float4 *__restrict__ rec,
+                                                                 const float *__restrict__ pos,
                                                                  const float *__restrict__ xs,
                                                                  const float *__restrict__ ys, int64_t fu, float r2,
                                                                  float neg_inv_s2, float two_inv_s2,
@@ -542,7 +518,7 @@ __global__ __launch_bounds__(kBlock) void radius_bwd_cell_kernel(const Params *_
                 for (int u = 0; u < UPL; ++u) {
                     const int64_t unit = fb + q + u * LPR;
                     const bool ok = DP && dv && unit < fu;
-                    const int64_t at = ok ? sd * fu + unit : 0;
+                    const int64_t at = ok ? static_cast<int64_t>(id) * fu + unit : 0;
                     const csr::Vec<K> a = csr::load_unit<K>(ys, at);
                     const csr::Vec<K> c = csr::load_unit<K>(xs, at);
 #pragma unroll
@@ -573,15 +549,15 @@ __global__ __launch_bounds__(kBlock) void radius_bwd_cell_kernel(const Params *_
 #pragma unroll
                     for (int b = 0; b < B; ++b) {
                         const bool live = FULL || k0 + b * S < md;
-                        const uint32_t t = static_cast<uint32_t>(__float_as_int(en[b].x));
+                        const uint32_t t = static_cast<uint32_t>(__float_as_int(en[b].x));  // point id
 #pragma unroll
                         for (int u = 0; u < UPL; ++u) {
                             load_k<K>(ys, t * ufu + uc[u], live, gj[b][u]);
                             if (DP) load_k<K>(xs, t * ufu + uc[u], live, xj[b][u]);
                         }
                         if (DP) {
-                            // t is a valid point for every entry (0 past the list end)
-                            const f32x4 v = reinterpret_cast<const f32x4 *>(rec)[t];
+                            // t is a valid point id for every entry (0 past the list end)
+                            const f32x4 v = {pos[t * 3 + 0], pos[t * 3 + 1], pos[t * 3 + 2], 0.0f};
                             pj[b] = live ? v : f32x4{pd.x, pd.y, pd.z, pd.w};
                         }
                     }
@@ -701,14 +677,13 @@ struct Ws {
     int32_t *perm_b;  // point id at each cell-ordered position
     int64_t *start;   // max_cells + 1 cell boundaries in cell order
     float4 *rec;
-    float *as, *bs;
     void *sort;
     void *scan;
     int64_t max_cells;
     int bbox_blocks;
 };
 
-Ws carve(Carve &c, int64_t n, int64_t feat) {
+Ws carve(Carve &c, int64_t n) {
     Ws w;
     w.max_cells = n + 64;
     w.bbox_blocks = 1024;
@@ -719,8 +694,6 @@ Ws carve(Carve &c, int64_t n, int64_t feat) {
     w.perm_b = c.take<int32_t>(n);
     w.start = c.take<int64_t>(w.max_cells + 1);
     w.rec = c.take<float4>(n);
-    w.as = c.take<float>(n * feat);
-    w.bs = c.take<float>(n * feat);
     w.sort = c.take<char>(csr::sort_keys_ws_bytes(n));
     w.scan = c.take<char>(scan_ws_bytes(n + 1));
     return w;
@@ -732,9 +705,8 @@ int blocks_for(int64_t n) {
     return static_cast<int>(b < cap ? b : cap);
 }
 
-// Build the cell directory and the cell-ordered copies of `a` and `b`.
-int build(int64_t n, const float *pos, float radius, const float *a, const float *b, int32_t feat, Ws &w,
-          hipStream_t stream) {
+// Build the cell directory and the cell-ordered records.
+int build(int64_t n, const float *pos, float radius, Ws &w, hipStream_t stream) {
     int nb = w.bbox_blocks;
     const int64_t need = ceil_div(n, kBlock);
     if (need < nb) nb = static_cast<int>(need);
@@ -750,27 +722,7 @@ int build(int64_t n, const float *pos, float radius, const float *a, const float
     if (int rc = csr::launch_sort_keys(w.cell, n, w.max_cells, w.cell_sorted, w.perm_b, w.start, w.sort, stream))
         return rc;
     hipLaunchKernelGGL(gather_records_kernel, dim3(blocks_for(n)), dim3(kBlock), 0, stream, w.perm_b, n, pos, w.rec);
-    if (int rc = check_launch("radius records")) return rc;
-    if (feat > 0 && (a || b)) {
-        const bool vec = feat % 4 == 0 && (!a || aligned16(a)) && (!b || aligned16(b));
-        if (vec) return launch_gather_rows<4>(w.perm_b, n, feat / 4, a, b, w.as, w.bs, stream);
-        return launch_gather_rows<1>(w.perm_b, n, feat, a, b, w.as, w.bs, stream);
-    }
-    return TIGA_OK;
-}
-
-template <int K>
-int launch_gather_rows(const int32_t *perm, int64_t n, int64_t fu, const float *a, const float *b, float *as,
-                       float *bs, hipStream_t stream) {
-    const int64_t total = n * fu;
-    const dim3 grid(static_cast<unsigned>(blocks_for(total)));
-    if (total < (int64_t{1} << 32) - kBlock * int64_t{65536})
-        hipLaunchKernelGGL((gather_rows_kernel<K, uint32_t>), grid, dim3(kBlock), 0, stream, perm,
-                           static_cast<uint32_t>(total), static_cast<uint32_t>(fu), a, b, as, bs);
-    else
-        hipLaunchKernelGGL((gather_rows_kernel<K, int64_t>), grid, dim3(kBlock), 0, stream, perm, total, fu, a, b, as,
-                           bs);
-    return check_launch("radius rows");
+    return check_launch("radius records");
 }
 
 // Persistent grid for the cell kernels: a multiple of 8 blocks (one share
@@ -782,57 +734,52 @@ int cell_grid(const void *kernel) {
 }
 
 template <int K, int LPR, int UPL>
-int fwd_cell(int64_t fu, const Ws &w, const int64_t *start, float r2, float nis, float *y, int32_t *count,
+int fwd_cell(int64_t fu, const Ws &w, const float *x, float r2, float nis, float *y, int32_t *count,
              hipStream_t stream) {
     const void *kern = reinterpret_cast<const void *>(&radius_fwd_cell_kernel<K, LPR, UPL>);
     static const int grid = cell_grid(kern);
     prof_before(stream);
-    hipLaunchKernelGGL((radius_fwd_cell_kernel<K, LPR, UPL>), dim3(grid), dim3(kBlock), 0, stream, w.prm, start,
-                       w.rec, w.as, fu, r2, nis, y, count);
+    hipLaunchKernelGGL((radius_fwd_cell_kernel<K, LPR, UPL>), dim3(grid), dim3(kBlock), 0, stream, w.prm, w.start,
+                       w.rec, x, fu, r2, nis, y, count);
     prof_after(stream);
     return check_launch("radius forward");
 }
 
 // Lanes per row: the smallest power of two covering the row's units, at most
-// 8 (16 with two units per lane); wider rows loop over feature blocks.
+// 8 (with two units per lane beyond that); wider rows loop over feature blocks.
 template <int K>
-int fwd_units(int64_t fu, const Ws &w, const int64_t *start, float r2, float nis, float *y, int32_t *count,
+int fwd_units(int64_t fu, const Ws &w, const float *x, float r2, float nis, float *y, int32_t *count,
               hipStream_t stream) {
-    if (fu <= 1) return fwd_cell<K, 1, 1>(fu, w, start, r2, nis, y, count, stream);
-    if (fu <= 2) return fwd_cell<K, 2, 1>(fu, w, start, r2, nis, y, count, stream);
-    if (fu <= 4) return fwd_cell<K, 4, 1>(fu, w, start, r2, nis, y, count, stream);
-    if (fu <= 8) return fwd_cell<K, 8, 1>(fu, w, start, r2, nis, y, count, stream);
-    return fwd_cell<K, 8, 2>(fu, w, start, r2, nis, y, count, stream);
+    if (fu <= 1) return fwd_cell<K, 1, 1>(fu, w, x, r2, nis, y, count, stream);
+    if (fu <= 2) return fwd_cell<K, 2, 1>(fu, w, x, r2, nis, y, count, stream);
+    if (fu <= 4) return fwd_cell<K, 4, 1>(fu, w, x, r2, nis, y, count, stream);
+    if (fu <= 8) return fwd_cell<K, 8, 1>(fu, w, x, r2, nis, y, count, stream);
+    return fwd_cell<K, 8, 2>(fu, w, x, r2, nis, y, count, stream);
 }
 
+struct BwdIo {
+    const float *pos, *x, *dy;
+    float *dx, *dp;
+};
+
 template <int K, int LPR, int UPL, bool DX, bool DP>
-int bwd_cell(int64_t fu, const Ws &w, const int64_t *start, float r2, float nis, float tis, float *dx, float *dp,
-             hipStream_t stream) {
+int bwd_cell(int64_t fu, const Ws &w, const BwdIo &io, float r2, float nis, float tis, hipStream_t stream) {
     const void *kern = reinterpret_cast<const void *>(&radius_bwd_cell_kernel<K, LPR, UPL, DX, DP>);
     static const int grid = cell_grid(kern);
     prof_before(stream);
     hipLaunchKernelGGL((radius_bwd_cell_kernel<K, LPR, UPL, DX, DP>), dim3(grid), dim3(kBlock), 0, stream, w.prm,
-                       start, w.rec, w.bs, w.as, fu, r2, nis, tis, dx, dp);
+                       w.start, w.rec, io.pos, io.x, io.dy, fu, r2, nis, tis, io.dx, io.dp);
     prof_after(stream);
     return check_launch("radius backward");
 }
 
 template <int K, bool DX, bool DP>
-int bwd_units(int64_t fu, const Ws &w, const int64_t *start, float r2, float nis, float tis, float *dx, float *dp,
-              hipStream_t stream) {
-    if (fu <= 1) return bwd_cell<K, 1, 1, DX, DP>(fu, w, start, r2, nis, tis, dx, dp, stream);
-    if (fu <= 2) return bwd_cell<K, 2, 1, DX, DP>(fu, w, start, r2, nis, tis, dx, dp, stream);
-    if (fu <= 4) return bwd_cell<K, 4, 1, DX, DP>(fu, w, start, r2, nis, tis, dx, dp, stream);
-    if (fu <= 8) return bwd_cell<K, 8, 1, DX, DP>(fu, w, start, r2, nis, tis, dx, dp, stream);
-    return bwd_cell<K, 8, 2, DX, DP>(fu, w, start, r2, nis, tis, dx, dp, stream);
-}
-
-}  // namespace
-
-size_t workspace_bytes(int64_t n, int64_t feat) {
-    Carve c(nullptr);
-    carve(c, n, feat);
-    return c.bytes();
+int bwd_units(int64_t fu, const Ws &w, const BwdIo &io, float r2, float nis, float tis, hipStream_t stream) {
+    if (fu <= 1) return bwd_cell<K, 1, 1, DX, DP>(fu, w, io, r2, nis, tis, stream);
+    if (fu <= 2) return bwd_cell<K, 2, 1, DX, DP>(fu, w, io, r2, nis, tis, stream);
+    if (fu <= 4) return bwd_cell<K, 4, 1, DX, DP>(fu, w, io, r2, nis, tis, stream);
+    if (fu <= 8) return bwd_cell<K, 8, 1, DX, DP>(fu, w, io, r2, nis, tis, stream);
+    return bwd_cell<K, 8, 2, DX, DP>(fu, w, io, r2, nis, tis, stream);
 }
 
 // The consume kernels index feature units with 32-bit arithmetic.
@@ -843,38 +790,46 @@ int check_units(int64_t n, int64_t fu) {
     return TIGA_OK;
 }
 
+}  // namespace
+
+size_t workspace_bytes(int64_t n, int64_t feat) {
+    (void)feat;  // feature rows are read in place
+    Carve c(nullptr);
+    carve(c, n);
+    return c.bytes();
+}
+
 int forward(int64_t n, int32_t feat, const float *pos, const float *x, float radius, float sigma, float *y,
             int32_t *count, void *ws, hipStream_t stream) {
-    const bool vec = feat % 4 == 0 && aligned16(y);
+    // 16-byte units when every row starts on a 16-byte boundary
+    const bool vec = feat % 4 == 0 && aligned16(x) && aligned16(y);
     const int64_t fu = vec ? feat / 4 : feat;
     if (int rc = check_units(n, fu)) return rc;
     Carve c(ws);
-    Ws w = carve(c, n, feat);
-    if (int rc = build(n, pos, radius, x, nullptr, feat, w, stream)) return rc;
-    const int64_t *start = w.start;
+    Ws w = carve(c, n);
+    if (int rc = build(n, pos, radius, w, stream)) return rc;
     const float r2 = radius * radius;
     const float nis = -1.0f / (sigma * sigma);
-    if (vec) return fwd_units<4>(fu, w, start, r2, nis, y, count, stream);
-    return fwd_units<1>(fu, w, start, r2, nis, y, count, stream);
+    if (vec) return fwd_units<4>(fu, w, x, r2, nis, y, count, stream);
+    return fwd_units<1>(fu, w, x, r2, nis, y, count, stream);
 }
 
 int backward(int64_t n, int32_t feat, const float *pos, const float *x, float radius, float sigma, const float *dy,
              float *dx, float *dpos, void *ws, hipStream_t stream) {
-    const bool vec = feat % 4 == 0 && (!dx || aligned16(dx));
+    const bool vec = feat % 4 == 0 && aligned16(dy) && (!dpos || aligned16(x)) && (!dx || aligned16(dx));
     const int64_t fu = vec ? feat / 4 : feat;
     if (int rc = check_units(n, fu)) return rc;
     Carve c(ws);
-    Ws w = carve(c, n, feat);
-    // as = cell-ordered dy, bs = cell-ordered x (only needed for dpos)
-    if (int rc = build(n, pos, radius, dy, dpos ? x : nullptr, feat, w, stream)) return rc;
-    const int64_t *start = w.start;
+    Ws w = carve(c, n);
+    if (int rc = build(n, pos, radius, w, stream)) return rc;
     const float r2 = radius * radius;
     const float nis = -1.0f / (sigma * sigma);
     const float tis = 2.0f / (sigma * sigma);
-#define TIGA_B(KK)                                                                                    \
-    if (dx && dpos) return bwd_units<KK, true, true>(fu, w, start, r2, nis, tis, dx, dpos, stream); \
-    if (dx) return bwd_units<KK, true, false>(fu, w, start, r2, nis, tis, dx, dpos, stream);        \
-    return bwd_units<KK, false, true>(fu, w, start, r2, nis, tis, dx, dpos, stream)
+    const BwdIo io{pos, x, dy, dx, dpos};
+#define TIGA_B(KK)                                                                  \
+    if (dx && dpos) return bwd_units<KK, true, true>(fu, w, io, r2, nis, tis, stream); \
+    if (dx) return bwd_units<KK, true, false>(fu, w, io, r2, nis, tis, stream);        \
+    return bwd_units<KK, false, true>(fu, w, io, r2, nis, tis, stream)
     if (vec) {
         TIGA_B(4);
     } else {
@@ -886,8 +841,8 @@ int backward(int64_t n, int32_t feat, const float *pos, const float *x, float ra
 int neighbors(int64_t n, const float *pos, float radius, int32_t *count, int64_t *nbr_ptr, int32_t *nbr_idx,
               void *ws, hipStream_t stream) {
     Carve c(ws);
-    Ws w = carve(c, n, 0);
-    if (int rc = build(n, pos, radius, nullptr, nullptr, 0, w, stream)) return rc;
+    Ws w = carve(c, n);
+    if (int rc = build(n, pos, radius, w, stream)) return rc;
     const int64_t *start = w.start;
     const float r2 = radius * radius;
     const dim3 grid(static_cast<unsigned>(ceil_div(n, kBlock)));

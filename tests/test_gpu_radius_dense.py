@@ -64,6 +64,32 @@ def test_radius_forward_backward(lib, kind, n, r, F):
     assert none is None and np.array_equal(host(dx2), host(dx))
 
 
+def test_radius_rows_not_16_byte_aligned(lib):
+    """Feature rows read in place from views that start 4 bytes into a buffer
+    take the one-float-per-unit path; results still match the oracle."""
+    n, F = 1800, 8
+    pos = cloud("uniform", n, 11)
+    x = synth.normal_f32(n * F, (85, n)).reshape(n, F)
+    dy = synth.normal_f32(n * F, (86, n)).reshape(n, F)
+    r, s = np.float32(0.08), np.float32(0.04)
+
+    def shifted(a):
+        buf = torch.zeros(a.size + 1, dtype=torch.float32, device="cuda")
+        buf[1:] = torch.from_numpy(a.reshape(-1)).cuda()
+        v = buf[1:].view(a.shape)
+        assert v.data_ptr() % 16 != 0
+        return v
+
+    y, cnt = lib.tiga_mp_radius_fwd(dev(pos), shifted(x), r, s)
+    ry, rya, rcnt = oracle.radius_fwd(pos, x, r, s)
+    assert np.array_equal(host(cnt), rcnt)
+    assert_terms_close(host(y), ry, rya, what="radius y (unaligned rows)")
+    dx, dp = lib.tiga_mp_radius_bwd(dev(pos), shifted(x), shifted(dy), r, s)
+    rdx, rdxa, rdp, rdpa = oracle.radius_bwd(pos, x, dy, r, s)
+    assert_terms_close(host(dx), rdx, rdxa, what="radius dx (unaligned rows)")
+    assert_terms_close(host(dp), rdp, rdpa, what="radius dpos (unaligned rows)")
+
+
 @pytest.mark.parametrize("kind,n,r", [("uniform", 4000, 0.06), ("grid", 3000, 0.09), ("cluster", 2500, 0.03)])
 def test_radius_neighbour_lists_exact(lib, kind, n, r):
     pos = cloud(kind, n, 7)
