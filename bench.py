@@ -47,27 +47,40 @@ def parse():
     p.add_argument("--no-ceilings", action="store_true", help="skip the hardware-ceiling probe")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--check-rows", type=int, default=400)
-    p.add_argument("--profile-pass", action="store_true",
-                   help="for rocprofv3 counter runs: a 4 GiB plain copy (calibration) then 3 headline steps")
+    p.add_argument("--profile-pass", nargs="?", const="csr", choices=["csr", "radius", "dense"],
+                   help="for rocprofv3 counter runs: csr = a 4 GiB plain copy (calibration) then 3 headline steps; "
+                        "radius / dense = 3 forward calls on the radius (1M points) / dense (65536 points) workload")
+    p.add_argument("--paths-only", action="store_true", help="only the per-path figures (for kernel traces)")
     p.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                    help="print the markdown summary of three rocprofv3 runs (kernel trace, FETCH_SIZE, WRITE_SIZE)")
+    p.add_argument("--summarize-kernels", nargs="+", metavar="DIR",
+                   help="markdown table of a kernel-trace run (first DIR) and the per-kernel averages of the "
+                        "counters in further --pmc run directories")
+    p.add_argument("--match", default="", help="with --summarize-kernels: only kernels whose name contains this")
     return p.parse_args()
 
 
 PROFILE_MD = os.path.join(ROOT, "profiles", "gather_reduce_csr_powerlaw_1b_f16.md")
+VALU_LANE_OPS_PER_S = 256 * 4 * 16 * 2.4e9  # CUs * SIMDs * lanes per cycle * clock
+VALU_INSTR_PER_PAIR = 12
 KERNEL_KEY = "gather_reduce_kernel"
 COPY_BYTES = 1 << 32
 
 
+# The translation unit of the gather-reduce kernel (and the plan it consumes).
+KERNEL_SOURCES = ["include/tiga_mp.h", "paper_2609_24802_amd/csrc/common.hpp",
+                  "paper_2609_24802_amd/csrc/csr_common.hpp", "paper_2609_24802_amd/csrc/csr_fwd.hpp",
+                  "paper_2609_24802_amd/csrc/csr_fwd.hip", "paper_2609_24802_amd/csrc/csr_plan.hip"]
+
+
 def source_hash():
-    """sha256 over the HIP sources: a committed counter summary applies only to the kernels it measured."""
-    import glob
+    """sha256 over the sources of the gather-reduce kernel: a committed counter summary applies only to the
+    kernel it measured."""
     import hashlib
     h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2609_24802_amd", "csrc")
-    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp"))):
+    for f in KERNEL_SOURCES:
         h.update(os.path.basename(f).encode())
-        h.update(open(f, "rb").read())
+        h.update(open(os.path.join(ROOT, f), "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -136,6 +149,35 @@ def summarize(trace_dir, fetch_dir, write_dir):
         f"- hbm_bytes_per_launch: {fetch_b + write_b:.6g}",
         f"- source_hash: {source_hash()}",
     ]
+    print("\n".join(out))
+
+
+def summarize_kernels(dirs, match):
+    """Markdown: kernel durations of a trace run, then per-kernel counter averages of --pmc runs."""
+    cur = _db(dirs[0]).cursor()
+    agg = {}
+    for name, dur in cur.execute("select name, duration from kernels").fetchall():
+        if match in name:
+            a = agg.setdefault(name, [0, 0.0])
+            a[0] += 1
+            a[1] += dur
+    out = ["| kernel | calls | total ms | avg ms |", "|---|---|---|---|"]
+    for name, (n, d) in sorted(agg.items(), key=lambda kv: -kv[1][1])[:16]:
+        out.append(f"| `{name[:110]}` | {n} | {d / 1e6:.3f} | {d / n / 1e6:.4f} |")
+    for d in dirs[1:]:
+        c = _db(d).cursor()
+        per = {}
+        for k, cn, v in c.execute("select kernel_name, counter_name, value from counters_collection").fetchall():
+            if match in k:
+                per.setdefault(k, {}).setdefault(cn, []).append(v)
+        if not per:
+            continue
+        names = sorted({cn for v in per.values() for cn in v})
+        out += ["", f"Counters ({os.path.basename(os.path.normpath(d))}), mean per dispatch:", "",
+                "| kernel | " + " | ".join(names) + " |", "|---" * (len(names) + 1) + "|"]
+        for k, v in sorted(per.items()):
+            cells = [f"{sum(v[cn]) / len(v[cn]):.4g}" if cn in v else "" for cn in names]
+            out.append(f"| `{k[:70]}` | " + " | ".join(cells) + " |")
     print("\n".join(out))
 
 
@@ -271,13 +313,24 @@ def paths(args, torch, tb, synth):
                                                                              reducer=tb.REDUCE_MAX, argmax=am,
                                                                              rev=rev),
     }
-    fwd_bytes = E * (8 + 4 * F) + n * (8 + 4 * F)
+    # algorithmic HBM bytes: forward = per edge (col, w, x row) + per row (row_ptr, y row [, argmax row]);
+    # sum backward = per edge (col, w, x row for dw, dy row for dx, dw) + dy rows + dx rows
+    ns = int(g["x"].shape[0])
+    alg = {"sum_fwd": E * (8 + 4 * F) + n * (8 + 4 * F),
+           "max_fwd": E * (8 + 4 * F) + n * (8 + 8 * F),
+           "sum_bwd_atomic": E * (12 + 8 * F) + n * (8 + 4 * F) + ns * 4 * F,
+           "sum_bwd_gather": E * (12 + 8 * F) + n * (8 + 4 * F) + ns * 4 * F}
     for name, fn in cases.items():
         r = time_steps(torch, tb, fn, steps, warm)
         d = dict(ms=r["step_ms"], gedges_per_s=E / r["step_ms"] / 1e6)
-        if name.endswith("sum_fwd"):
+        key = name.split("f64_")[1]
+        if key in alg:
+            d.update(alg_bytes=alg[key], alg_gbs=alg[key] / r["step_ms"] / 1e6,
+                     frac_hbm=alg[key] / r["step_ms"] / 1e6 / HBM_PEAK_GBS)
+        if key == "sum_fwd":
             k = float(np.mean(r["kernel_ms"]))
-            d.update(kernel_ms=k, alg_gbs=fwd_bytes / k / 1e6, frac_hbm=fwd_bytes / k / 1e6 / HBM_PEAK_GBS)
+            d.update(kernel_ms=k, kernel_alg_gbs=alg[key] / k / 1e6,
+                     kernel_frac_hbm=alg[key] / k / 1e6 / HBM_PEAK_GBS)
         res[name] = d
         log(f"{name}: {d['ms']:.3f} ms")
     del rel, xd, wd, dyd, rev, am
@@ -288,11 +341,18 @@ def paths(args, torch, tb, synth):
     r, s = g["radius"], g["sigma"]
     _, cnt = tb.tiga_mp_radius_fwd(pd, xd, r, s)
     pairs = int(cnt.long().sum().item())
+    npt, Fr = int(g["x"].shape[0]), int(g["x"].shape[1])
+    # unique HBM bytes of the consume kernel: records, x rows, y rows (fwd); records, positions, x, dy, dx,
+    # dpos rows (bwd).  Accepted pairs re-read rows from the caches, so this sits far below the HBM peak:
+    # the kernel is bound by candidate tests (VALU) and gather latency instead.
+    uniq = {"fwd": npt * (16 + 8 * Fr), "bwd": npt * (16 + 12 + 12 * Fr + 12)}
     for name, fn in {"radius_1m_f32_fwd_with_build": lambda: tb.tiga_mp_radius_fwd(pd, xd, r, s, want_count=False),
                      "radius_1m_f32_bwd_with_build": lambda: tb.tiga_mp_radius_bwd(pd, xd, dyd, r, s)}.items():
         rr = time_steps(torch, tb, fn, steps, warm)
+        k = float(np.mean(rr["kernel_ms"]))
+        u = uniq["fwd" if "_fwd_" in name else "bwd"]
         res[name] = dict(ms=rr["step_ms"], gedges_per_s=pairs / rr["step_ms"] / 1e6, accepted_pairs=pairs,
-                         kernel_ms=float(np.mean(rr["kernel_ms"])))
+                         kernel_ms=k, kernel_unique_gbs=u / k / 1e6, kernel_frac_hbm=u / k / 1e6 / HBM_PEAK_GBS)
         log(f"{name}: {rr['step_ms']:.3f} ms")
     del pd, xd, dyd
     g = synth.config4()
@@ -301,14 +361,36 @@ def paths(args, torch, tb, synth):
     rr = time_steps(torch, tb, lambda: tb.tiga_mp_dense_fwd(pd, qd, g["eps"]), steps, warm)
     k = float(np.mean(rr["kernel_ms"]))
     tf = nn * (nn - 1) * 20 / (k * 1e-3) / 1e12
+    # issue bound: 12 non-transcendental VALU instructions per pair (the reciprocal square root co-issues);
+    # a wave64 VALU instruction occupies a SIMD for 4 cycles: 1024 SIMDs * 2.4 GHz / 4 * 64 lanes
+    issue_peak = VALU_LANE_OPS_PER_S / VALU_INSTR_PER_PAIR
     res["dense_65536_fwd"] = dict(ms=rr["step_ms"], gpairs_per_s=nn * (nn - 1) / rr["step_ms"] / 1e6, kernel_ms=k,
-                                  tflops_20_per_pair=tf, frac_valu=tf / VALU_PEAK_TFLOPS)
+                                  tflops_20_per_pair=tf, frac_valu=tf / VALU_PEAK_TFLOPS,
+                                  frac_valu_issue=nn * (nn - 1) / (k * 1e-3) / issue_peak)
     log(f"dense: {rr['step_ms']:.3f} ms ({tf:.1f} TFLOP/s)")
     return res
 
 
 def profile_pass(args, torch, tb, synth):
-    """Workload for counter runs: a plain copy of known size, then three steps."""
+    """Workload for counter runs: a plain copy of known size, then three steps (csr); or three forward calls on
+    the radius or dense workload."""
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    if args.profile_pass == "radius":
+        g = synth.config3()
+        pd, xd = dev(g["pos"]), dev(g["x"])
+        for _ in range(3):
+            tb.tiga_mp_radius_fwd(pd, xd, g["radius"], g["sigma"])
+        torch.cuda.synchronize()
+        log("profile pass done")
+        return
+    if args.profile_pass == "dense":
+        g = synth.config4()
+        pd, qd = dev(g["pos"]), dev(g["q"])
+        for _ in range(3):
+            tb.tiga_mp_dense_fwd(pd, qd, g["eps"])
+        torch.cuda.synchronize()
+        log("profile pass done")
+        return
     src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
     src.fill_(1.0)
@@ -346,6 +428,9 @@ def main():
     if args.summarize:
         summarize(*args.summarize)
         return
+    if args.summarize_kernels:
+        summarize_kernels(args.summarize_kernels, args.match)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
@@ -362,6 +447,9 @@ def main():
     tb.load()
     if args.profile_pass:
         profile_pass(args, torch, tb, synth)
+        return
+    if args.paths_only:
+        print(json.dumps(paths(args, torch, tb, synth)), flush=True)
         return
     ceil = None if args.no_ceilings else ceilings()
     h, cpu = headline(args, torch, tb, synth, oracle)
