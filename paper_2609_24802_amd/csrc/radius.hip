@@ -38,9 +38,13 @@ __global__ __launch_bounds__(kBlock) void bbox_partial_kernel(const float *__res
     for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
 #pragma unroll
         for (int a = 0; a < 3; ++a) {
+            // the box covers finite coordinates only; a non-finite one is
+            // never within the radius of anything and lands in a border cell
             const float v = pos[i * 3 + a];
-            mn[a] = fminf(mn[a], v);
-            mx[a] = fmaxf(mx[a], v);
+            if (__builtin_isfinite(v)) {
+                mn[a] = fminf(mn[a], v);
+                mx[a] = fmaxf(mx[a], v);
+            }
         }
     }
 #pragma unroll
@@ -120,13 +124,13 @@ __global__ __launch_bounds__(kBlock) void grid_params_kernel(const float *__rest
     int64_t d[3] = {1, 1, 1};
     bool fits = false;
     for (int it = 0; it < 200 && !fits; ++it) {
-        int64_t cells = 1;
+        double cells = 1.0;  // in double: the product of three capped extents cannot overflow
         for (int a = 0; a < 3; ++a) {
             const double t = floor(ext[a] / h) + 1.0;
             d[a] = t > 2e9 ? static_cast<int64_t>(2e9) : static_cast<int64_t>(t);
-            cells = (cells > (int64_t{1} << 40)) ? cells : cells * d[a];
+            cells *= static_cast<double>(d[a]);
         }
-        fits = cells <= max_cells;
+        fits = cells <= static_cast<double>(max_cells);
         if (!fits) h *= 1.25;
     }
     if (!fits) {
@@ -142,12 +146,14 @@ __global__ __launch_bounds__(kBlock) void grid_params_kernel(const float *__rest
     prm->ncell = static_cast<int>(d[0] * d[1] * d[2]);
 }
 
+// Cell coordinate along axis a, clamped to [0, dim - 1] before conversion
+// (NaN and -inf go to 0, +inf to the last cell).
 __device__ __forceinline__ int cell_axis(const Params &p, int a, float v) {
     double t = floor((static_cast<double>(v) - p.lo[a]) * p.inv_h);
-    int c = static_cast<int>(t);
-    if (t < 0.0) c = 0;
-    if (c >= p.dim[a]) c = p.dim[a] - 1;
-    return c;
+    if (!(t >= 0.0)) t = 0.0;
+    const double top = static_cast<double>(p.dim[a] - 1);
+    if (t > top) t = top;
+    return static_cast<int>(t);
 }
 
 // Cell id of every point (z-major, x fastest).

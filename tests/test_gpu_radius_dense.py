@@ -64,6 +64,48 @@ def test_radius_forward_backward(lib, kind, n, r, F):
     assert none is None and np.array_equal(host(dx2), host(dx))
 
 
+def edge_cloud(case):
+    rng = np.random.default_rng(12)
+    if case == "single":
+        return np.zeros((1, 3), np.float32), 0.1
+    if case == "pair":
+        return np.array([[0, 0, 0], [0.05, 0, 0]], np.float32), 0.1
+    if case == "coincident":  # one cell, every pair at distance 0
+        return np.full((300, 3), 0.25, np.float32), 0.01
+    if case == "all_pairs":  # radius beyond the cloud: one cell of 300 points, lists longer than 64
+        return rng.random((300, 3)).astype(np.float32), 10.0
+    if case == "tiny_radius":  # r^2 underflows to 0 in fp32: no pair is accepted
+        return rng.random((500, 3)).astype(np.float32), 1e-30
+    if case == "non_finite":  # NaN / inf coordinates: such points have no neighbours
+        p = rng.random((400, 3)).astype(np.float32)
+        p[::37, 0] = np.nan
+        p[5, 1] = np.inf
+        p[9, 2] = -np.inf
+        return p, 0.15
+    raise ValueError(case)
+
+
+@pytest.mark.parametrize("case", ["single", "pair", "coincident", "all_pairs", "tiny_radius", "non_finite"])
+def test_radius_edge_cases(lib, case):
+    pos, r = edge_cloud(case)
+    n, F = pos.shape[0], 8
+    r = np.float32(r)
+    s = np.float32(max(float(r), 1e-3) / 2)
+    x = synth.normal_f32(n * F, (87, n)).reshape(n, F)
+    dy = synth.normal_f32(n * F, (88, n)).reshape(n, F)
+    y, cnt = lib.tiga_mp_radius_fwd(dev(pos), dev(x), r, s)
+    ry, rya, rcnt = oracle.radius_fwd(pos, x, r, s)
+    assert np.array_equal(host(cnt), rcnt)
+    assert_terms_close(host(y), ry, rya, what=f"radius y {case}")
+    dx, dp = lib.tiga_mp_radius_bwd(dev(pos), dev(x), dev(dy), r, s)
+    rdx, rdxa, rdp, rdpa = oracle.radius_bwd(pos, x, dy, r, s)
+    assert_terms_close(host(dx), rdx, rdxa, what=f"radius dx {case}")
+    assert_terms_close(host(dp), rdp, rdpa, what=f"radius dpos {case}")
+    c2, ptr, idx = lib.tiga_radius_neighbors(dev(pos), r)
+    rptr, ridx = oracle.radius_neighbors(pos, r)
+    assert np.array_equal(host(ptr), rptr) and np.array_equal(host(idx), ridx)
+
+
 def test_radius_rows_not_16_byte_aligned(lib):
     """Feature rows read in place from views that start 4 bytes into a buffer
     take the one-float-per-unit path; results still match the oracle."""
