@@ -234,7 +234,7 @@ __device__ __forceinline__ void for_candidates(const Params &p, const int64_t *_
 // input.
 constexpr int kDch = 8;      // destinations per pass over a cell's candidates
 constexpr int kCapC = 64;    // list entries per destination between flushes
-constexpr int kBatch = 8;    // list entries whose rows are loaded together
+constexpr int kBatch = 6;    // list entries whose rows are loaded together
 constexpr int kBatchDp = 2;  // the same when position gradients are formed
 
 static_assert(kCapC >= kWave, "one candidate chunk may add a wave's worth of entries after a flush");
