@@ -320,6 +320,8 @@ def paths(args, torch, tb, synth):
            "max_fwd": E * (8 + 4 * F) + n * (8 + 8 * F),
            "sum_bwd_atomic": E * (12 + 8 * F) + n * (8 + 4 * F) + ns * 4 * F,
            "sum_bwd_gather": E * (12 + 8 * F) + n * (8 + 4 * F) + ns * 4 * F}
+    # the reverse incidence is topology set-up (built once, reused by every gather-mode backward)
+    cases["csr_powerlaw_1m_16m_f64_transpose"] = lambda: tb.tiga_csr_transpose(rel)
     for name, fn in cases.items():
         r = time_steps(torch, tb, fn, steps, warm)
         d = dict(ms=r["step_ms"], gedges_per_s=E / r["step_ms"] / 1e6)

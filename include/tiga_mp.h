@@ -143,8 +143,11 @@ size_t tiga_mp_csr_bwd_workspace(const tiga_csr *rel, int32_t feat, int reducer)
  * (w = 1 under TIGA_MSG_SRC.)  dx: fp32 [num_src, feat]; dw: fp32 [num_edges];
  * either may be NULL (skipped) and each is overwritten.  dw requires
  * TIGA_MSG_EDGE_SCALED_SRC.
- * rev == NULL: dx accumulates with device atomics (fast, order not fixed).
- * rev != NULL: dx is gathered over the reverse incidence (deterministic).
+ * rev == NULL: dx accumulates with device fp32 atomics: no set-up, summation
+ *   order not fixed, and bound by the atomics (at feat = 64 about six times
+ *   slower than the gather mode).
+ * rev != NULL: dx is gathered over the reverse incidence (deterministic); build
+ *   it once per topology with tiga_csr_transpose.
  * Errors: as tiga_mp_csr_fwd. */
 int tiga_mp_csr_bwd(const tiga_csr *rel, const tiga_csr_t *rev, int32_t feat,
                     const float *x_src, int msg, const float *w_edge, int reducer,
