@@ -314,12 +314,14 @@ def paths(args, torch, tb, synth):
                                                                              rev=rev),
     }
     # algorithmic HBM bytes: forward = per edge (col, w, x row) + per row (row_ptr, y row [, argmax row]);
-    # sum backward = per edge (col, w, x row for dw, dy row for dx, dw) + dy rows + dx rows
+    # sum backward, atomic mode = per edge (col, w, x row for dw, dw, dy row added into dx) + dy rows + dx rows;
+    # sum backward, gather mode (one traversal of the reverse incidence) = per edge (edge id, destination,
+    # w, dy row, dw) + per source (src_ptr, x row, dx row)
     ns = int(g["x"].shape[0])
     alg = {"sum_fwd": E * (8 + 4 * F) + n * (8 + 4 * F),
            "max_fwd": E * (8 + 4 * F) + n * (8 + 8 * F),
            "sum_bwd_atomic": E * (12 + 8 * F) + n * (8 + 4 * F) + ns * 4 * F,
-           "sum_bwd_gather": E * (12 + 8 * F) + n * (8 + 4 * F) + ns * 4 * F}
+           "sum_bwd_gather": E * (16 + 4 * F) + ns * (8 + 8 * F)}
     # the reverse incidence is topology set-up (built once, reused by every gather-mode backward)
     cases["csr_powerlaw_1m_16m_f64_transpose"] = lambda: tb.tiga_csr_transpose(rel)
     for name, fn in cases.items():

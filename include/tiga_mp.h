@@ -230,12 +230,14 @@ int tiga_mp_dense_fwd(int64_t n, const float *pos, const float *q, float eps, in
 
 /* ------------------------------------------------------------- profiling */
 
-/* Profiling aid.  Arms the calling thread so that its next fused entry point
+/* Profiling aid.  Arms the calling thread so that its next entry-point call
  * records hipEvent `start` on its stream immediately before, and `stop`
  * immediately after, the launch of that call's dominant kernel (the one that
  * streams the edges or pairs).  The events (hipEvent_t passed as void*) stay
- * owned by the caller; the arming is consumed by that one call.  Passing NULL
- * for both disarms.  Returns TIGA_OK. */
+ * owned by the caller and must live until that call returns.  The arming is
+ * consumed by that one call; a call without a fused kernel (transpose,
+ * validation, neighbour lists) records nothing and drops it.  Passing NULL for
+ * both disarms.  Returns TIGA_OK. */
 int tiga_mp_set_kernel_events(void *start, void *stop);
 
 #ifdef __cplusplus

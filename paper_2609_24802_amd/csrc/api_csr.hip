@@ -61,7 +61,7 @@ size_t tiga_mp_csr_fwd_workspace(const tiga_csr *rel, int32_t feat, int reducer)
 
 int tiga_mp_csr_fwd(const tiga_csr *rel, int32_t feat, const float *x_src, int msg, const float *w_edge,
                     int reducer, float *y, int32_t *argmax, void *ws, size_t ws_bytes, void *stream) {
-    clear_error();
+    EntryScope scope;
     if (int rc = check_common(rel, feat, msg, w_edge, reducer)) return rc;
     if (rel->num_dst == 0) return TIGA_OK;
     if (!y) return fail(TIGA_EINVAL, "y is NULL");
@@ -87,7 +87,7 @@ size_t tiga_mp_csr_bwd_workspace(const tiga_csr *rel, int32_t feat, int reducer)
 int tiga_mp_csr_bwd(const tiga_csr *rel, const tiga_csr_t *rev, int32_t feat, const float *x_src, int msg,
                     const float *w_edge, int reducer, const int32_t *argmax, const float *dy, float *dx,
                     float *dw, void *ws, size_t ws_bytes, void *stream) {
-    clear_error();
+    EntryScope scope;
     if (int rc = check_common(rel, feat, msg, w_edge, reducer)) return rc;
     if (dw && msg != TIGA_MSG_EDGE_SCALED_SRC)
         return fail(TIGA_EINVAL, "dw requires TIGA_MSG_EDGE_SCALED_SRC");
@@ -117,7 +117,7 @@ size_t tiga_csr_transpose_workspace(const tiga_csr *rel) {
 
 int tiga_csr_transpose(const tiga_csr *rel, int64_t *src_ptr, int32_t *edge_id, int32_t *dst_idx, void *ws,
                        size_t ws_bytes, void *stream) {
-    clear_error();
+    EntryScope scope;
     if (int rc = check_csr_meta(rel)) return rc;
     if (rel->num_edges > INT32_MAX) return fail(TIGA_EUNSUPPORTED, "transpose needs num_edges < 2^31");
     if (!src_ptr) return fail(TIGA_EINVAL, "src_ptr is NULL");
@@ -128,7 +128,7 @@ int tiga_csr_transpose(const tiga_csr *rel, int64_t *src_ptr, int32_t *edge_id, 
 }
 
 int tiga_csr_validate(const tiga_csr *rel, int level, void *stream) {
-    clear_error();
+    EntryScope scope;
     if (level != 1 && level != 2) return fail(TIGA_EINVAL, "validation level must be 1 or 2 (got %d)", level);
     if (int rc = check_csr_meta(rel)) return rc == TIGA_EINVAL ? TIGA_EGRAPH : rc;
     if (level == 1) return TIGA_OK;

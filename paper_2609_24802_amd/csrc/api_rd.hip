@@ -38,7 +38,7 @@ size_t tiga_mp_radius_workspace(int64_t n, int32_t feat) {
 
 int tiga_mp_radius_fwd(int64_t n, int32_t feat, const float *pos, const float *x, float radius, float sigma,
                        int reducer, float *y, int32_t *count, void *ws, size_t ws_bytes, void *stream) {
-    clear_error();
+    EntryScope scope;
     if (int rc = check_points(n, pos)) return rc;
     if (feat < 1) return fail(TIGA_EINVAL, "feat must be >= 1 (got %d)", feat);
     if (reducer == TIGA_REDUCE_MAX) return fail(TIGA_EUNSUPPORTED, "the radius relation supports the sum reducer only");
@@ -52,7 +52,7 @@ int tiga_mp_radius_fwd(int64_t n, int32_t feat, const float *pos, const float *x
 
 int tiga_mp_radius_bwd(int64_t n, int32_t feat, const float *pos, const float *x, float radius, float sigma,
                        const float *dy, float *dx, float *dpos, void *ws, size_t ws_bytes, void *stream) {
-    clear_error();
+    EntryScope scope;
     if (int rc = check_points(n, pos)) return rc;
     if (feat < 1) return fail(TIGA_EINVAL, "feat must be >= 1 (got %d)", feat);
     if (int rc = check_radius(radius, sigma)) return rc;
@@ -65,7 +65,7 @@ int tiga_mp_radius_bwd(int64_t n, int32_t feat, const float *pos, const float *x
 
 int tiga_radius_neighbors(int64_t n, const float *pos, float radius, int32_t *count, int64_t *nbr_ptr,
                           int32_t *nbr_idx, void *ws, size_t ws_bytes, void *stream) {
-    clear_error();
+    EntryScope scope;
     if (int rc = check_points(n, pos)) return rc;
     if (int rc = check_radius(radius, 1.0f)) return rc;
     if (!nbr_ptr) return fail(TIGA_EINVAL, "nbr_ptr is NULL");
@@ -85,7 +85,7 @@ size_t tiga_mp_dense_workspace(int64_t n) {
 
 int tiga_mp_dense_fwd(int64_t n, const float *pos, const float *q, float eps, int reducer, float *y, void *ws,
                       size_t ws_bytes, void *stream) {
-    clear_error();
+    EntryScope scope;
     if (int rc = check_points(n, pos)) return rc;
     if (reducer == TIGA_REDUCE_MAX) return fail(TIGA_EUNSUPPORTED, "the dense relation supports the sum reducer only");
     if (reducer != TIGA_REDUCE_SUM) return fail(TIGA_EINVAL, "unknown reducer %d", reducer);

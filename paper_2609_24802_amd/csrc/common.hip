@@ -49,6 +49,12 @@ void prof_after(hipStream_t stream) {
     g_prof_stop = nullptr;
 }
 
+void prof_disarm() {
+    g_prof_started = false;
+    g_prof_start = nullptr;
+    g_prof_stop = nullptr;
+}
+
 int device_cus() {
     static std::mutex mu;
     static std::vector<int> cache;

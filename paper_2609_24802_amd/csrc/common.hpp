@@ -28,6 +28,17 @@ int fail(int code, const char *fmt, ...);
 // the dominant launch the stop event; then disarm.
 void prof_before(hipStream_t stream);
 void prof_after(hipStream_t stream);
+void prof_disarm();
+
+// Scope of one C entry-point call: clears the thread's error message on entry
+// and drops any kernel-event arming on exit, so an arming lasts exactly one
+// call whether or not that call launched a timed kernel.
+struct EntryScope {
+    EntryScope() { clear_error(); }
+    ~EntryScope() { prof_disarm(); }
+    EntryScope(const EntryScope &) = delete;
+    EntryScope &operator=(const EntryScope &) = delete;
+};
 
 // Check the result of a launch or HIP call; return TIGA_EDEVICE on failure.
 int check_hip(hipError_t err, const char *what);

@@ -162,10 +162,12 @@ int launch_bwd(const BwdArgs &a, void *ws, hipStream_t stream) {
     if (atomic_dx) {
         if (int rc = fill_u32(a.dx, 0u, rel->num_src * static_cast<int64_t>(a.feat), stream)) return rc;
     }
-    if (a.dw && rel->num_edges == 0 && rel->num_dst == 0) {
-        // nothing to write
-    }
-    if ((a.dw || atomic_dx) && rel->num_dst > 0) {
+    // Sum with the reverse incidence and both gradients: one traversal of the
+    // reverse incidence gathers each dy row once and forms dx_j and dw_e
+    // together (x_j is the source's own row), when the row fits one feature
+    // block.  Otherwise dw comes from the row-parallel edge kernel.
+    const bool fused = a.red == RED_SUM && a.rev && a.dx && a.dw && a.x && lay.fu <= lay.L;
+    if ((a.dw || atomic_dx) && !fused && rel->num_dst > 0) {
         EdgeT t{rel->row_ptr, rel->col_idx, a.w, a.x, a.dy, a.arg, atomic_dx ? a.dx : nullptr, a.dw,
                 rel->num_dst, lay.fu};
         int rc;
@@ -181,7 +183,13 @@ int launch_bwd(const BwdArgs &a, void *ws, hipStream_t stream) {
         Trav t{a.rev->src_ptr, a.rev->dst_idx, a.w, a.rev->edge_id, a.dy, rel->num_src, lay.fu, a.arg, 0u,
                rel->num_edges};
         const int wm = a.red == RED_MAX ? W_ROUTE : W_INDIRECT;
-        if (int rc = launch_traversal(t, rel->num_dst, rel->num_edges, lay, RED_SUM, wm, ws, a.dx, nullptr, stream))
+        EdgeGrad eg;
+        if (fused) {
+            eg.x = a.x;
+            eg.dw = a.dw;
+        }
+        if (int rc = launch_traversal(t, rel->num_dst, rel->num_edges, lay, RED_SUM, wm, ws, a.dx, nullptr, stream,
+                                      eg))
             return rc;
     }
     return TIGA_OK;

@@ -390,10 +390,18 @@ struct Table {
 // the other resident wavefronts.  Offsets inside the row are 32-bit (a row
 // piece is at most one chunk of edges).  Lanes past the row's end issue no
 // loads at all (their exec bit is off).
-template <int K, int RED, int WM, int SL, bool BUF, bool NT, class A>
+// Per-edge side computation of a traversal, called with each gathered unit
+// (zero for lanes past the row end) before it is weighted.  The default does
+// nothing.
+struct NoEdgeHook {
+    template <int K>
+    __device__ __forceinline__ void edge(const Vec<K> &, int32_t, bool) {}
+};
+
+template <int K, int RED, int WM, int SL, bool BUF, bool NT, class A, class H = NoEdgeHook>
 __device__ __forceinline__ void run_edges(const Trav &t, const Table<K, BUF, NT> &tab,
                                           const __amdgpu_buffer_rsrc_t &ars, int64_t e0, int64_t e1, int s,
-                                          int64_t u, bool uok, A &acc) {
+                                          int64_t u, bool uok, A &acc, H &&hook = H{}) {
     constexpr int STEP = SL * kUnroll;
     const int n = static_cast<int>(e1 - e0);
     const int32_t *__restrict__ colr = t.idx + e0;
@@ -443,6 +451,7 @@ __device__ __forceinline__ void run_edges(const Trav &t, const Table<K, BUF, NT>
                 if constexpr (WM == W_ROUTE) keep = keep && sel[r][k] == ee[r];
                 xv[r].v[k] = keep ? xv[r].v[k] : 0.0f;
             }
+            hook.template edge<K>(xv[r], ee[r], ok[r]);
             acc.add(wv[r], xv[r], e0 + k0 + r * SL + s, live);
         }
     }

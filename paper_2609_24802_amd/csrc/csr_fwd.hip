@@ -7,9 +7,31 @@ namespace csr {
 
 namespace {
 
+// Edge gradient of the sum backward, formed during the traversal of the
+// reverse incidence: dw[e] = <x_j, dy[dst(e)]> for the source row j being
+// folded.  Each lane holds one unit of x_j; the L lanes of an edge slot add
+// their parts by a fixed shuffle tree and the slot's first lane writes dw[e].
+// The row must fit one feature block (fu <= L).
+template <int K, int L>
+struct DwHook {
+    float xj[K];
+    float *__restrict__ dw;
+    int l;
+    template <int KK>
+    __device__ __forceinline__ void edge(const Vec<KK> &g, int32_t e, bool ok) {
+        float p = 0.0f;
+#pragma unroll
+        for (int k = 0; k < K; ++k) p = fmaf(xj[k], g.v[k], p);
+#pragma unroll
+        for (int m = 1; m < L; m <<= 1) p += shfl_xor_f(p, m);
+        if (ok && l == 0) dw[e] = p;
+    }
+};
+
 // Fold one chunk (or short row) per group, reduce the group's slots, and
-// write the finalized output row or the chunk's partial state.
-template <int K, int L, int RED, int WM, bool BUF, bool NT>
+// write the finalized output row or the chunk's partial state.  With DW the
+// fold also forms the edge gradients (DwHook; x rows in hx, output hdw).
+template <int K, int L, int RED, int WM, bool BUF, bool NT, bool DW = false>
 struct GatherBody {
     const Trav &t;
     const Table<K, BUF, NT> &tab;
@@ -18,6 +40,8 @@ struct GatherBody {
     int32_t *__restrict__ out_arg;
     float *__restrict__ part_v;
     int32_t *__restrict__ part_e;
+    const float *__restrict__ hx;
+    float *__restrict__ hdw;
 
     template <int GL>
     __device__ __forceinline__ void run(const Meta &m, int glane) {
@@ -29,7 +53,18 @@ struct GatherBody {
             const bool uok = u < t.fu;
             A acc;
             acc.init();
-            run_edges<K, RED, WM, GL / L, BUF, NT>(t, tab, ars, m.e0, m.e0 + m.n, s, u, uok, acc);
+            if constexpr (DW) {
+                DwHook<K, L> h;
+                h.dw = hdw;
+                h.l = l;
+                const bool own = uok && m.n > 0;
+                const Vec<K> xr = load_unit<K>(hx, own ? static_cast<int64_t>(m.row) * t.fu + u : 0);
+#pragma unroll
+                for (int k = 0; k < K; ++k) h.xj[k] = own ? xr.v[k] : 0.0f;
+                run_edges<K, RED, WM, GL / L, BUF, NT>(t, tab, ars, m.e0, m.e0 + m.n, s, u, uok, acc, h);
+            } else {
+                run_edges<K, RED, WM, GL / L, BUF, NT>(t, tab, ars, m.e0, m.e0 + m.n, s, u, uok, acc);
+            }
             reduce_lanes<L, GL>(acc);
             if (m.write && s == 0 && uok) {
                 if (m.slot < 0) {
@@ -47,19 +82,21 @@ struct GatherBody {
     }
 };
 
-template <int K, int L, int RED, int WM, bool BUF, bool NT>
+template <int K, int L, int RED, int WM, bool BUF, bool NT, bool DW>
 __global__ __launch_bounds__(kBlock) void gather_reduce_kernel(Trav t, int64_t n_groups,
                                                                const Desc *__restrict__ chunks,
                                                                const PlanCounts *__restrict__ counts,
                                                                float *__restrict__ out,
                                                                int32_t *__restrict__ out_arg,
                                                                float *__restrict__ part_v,
-                                                               int32_t *__restrict__ part_e) {
+                                                               int32_t *__restrict__ part_e,
+                                                               const float *__restrict__ hx,
+                                                               float *__restrict__ hdw) {
     const Table<K, BUF, NT> tab(t.table, t.fu, t.table_bytes);
     // argmax table (max-routing gather only; otherwise an unused empty resource)
     const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<int32_t *>(t.arg), 0, (BUF && WM == W_ROUTE) ? t.table_bytes : 0u, kBufWord3);
-    GatherBody<K, L, RED, WM, BUF, NT> body{t, tab, ars, out, out_arg, part_v, part_e};
+    GatherBody<K, L, RED, WM, BUF, NT, DW> body{t, tab, ars, out, out_arg, part_v, part_e, hx, hdw};
     const Items items = make_items(counts, n_groups);
     for_each_item<L>(items, chunks, t.ptr, t.nrows, body);
 }
@@ -112,32 +149,32 @@ __global__ __launch_bounds__(kBlock) void merge_kernel(const Split *__restrict__
     }
 }
 
-template <int K, int L, int RED, int WM, bool BUF, bool NT>
+template <int K, int L, int RED, int WM, bool BUF, bool NT, bool DW>
 int launch_gather_reduce(const Trav &t, int64_t n_groups, const PlanWs &w, const PlanBounds &b, float *out,
-                         int32_t *out_arg, hipStream_t stream) {
-    auto kern = gather_reduce_kernel<K, L, RED, WM, BUF, NT>;
+                         int32_t *out_arg, const EdgeGrad &eg, hipStream_t stream) {
+    auto kern = gather_reduce_kernel<K, L, RED, WM, BUF, NT, DW>;
     static const int per_cu = resident_blocks(reinterpret_cast<const void *>(kern), kBlock);
     const int blocks = persistent_blocks(n_groups + b.max_chunks, per_cu);
     prof_before(stream);
     hipLaunchKernelGGL(kern, dim3(blocks), dim3(kBlock), 0, stream, t, n_groups, w.chunks, w.counts, out, out_arg,
-                       w.part_v, w.part_e);
+                       w.part_v, w.part_e, eg.x, eg.dw);
     prof_after(stream);
     return check_launch("gather-reduce");
 }
 
-template <int K, int L, int RED, int WM>
+template <int K, int L, int RED, int WM, bool DW>
 int launch_traversal_t(const Trav &t, int64_t nedges, const PlanWs &w, const PlanBounds &b, float *out,
-                       int32_t *out_arg, hipStream_t stream) {
+                       int32_t *out_arg, const EdgeGrad &eg, hipStream_t stream) {
     constexpr Geom g = make_geom(L);
     if (int rc = launch_plan(t.ptr, t.nrows, g, b, w, stream)) return rc;
     const int64_t n_groups = ceil_div(t.nrows, g.RPW);
     int rc;
     if (!t.table_bytes)
-        rc = launch_gather_reduce<K, L, RED, WM, false, true>(t, n_groups, w, b, out, out_arg, stream);
+        rc = launch_gather_reduce<K, L, RED, WM, false, true, DW>(t, n_groups, w, b, out, out_arg, eg, stream);
     else if (t.table_bytes > kStreamTableBytes)
-        rc = launch_gather_reduce<K, L, RED, WM, true, true>(t, n_groups, w, b, out, out_arg, stream);
+        rc = launch_gather_reduce<K, L, RED, WM, true, true, DW>(t, n_groups, w, b, out, out_arg, eg, stream);
     else
-        rc = launch_gather_reduce<K, L, RED, WM, true, false>(t, n_groups, w, b, out, out_arg, stream);
+        rc = launch_gather_reduce<K, L, RED, WM, true, false, DW>(t, n_groups, w, b, out, out_arg, eg, stream);
     if (rc) return rc;
     const int mblocks = persistent_blocks(b.max_splits, 4);
     hipLaunchKernelGGL((merge_kernel<K, L, RED>), dim3(mblocks), dim3(kBlock), 0, stream, w.splits, w.counts,
@@ -145,17 +182,17 @@ int launch_traversal_t(const Trav &t, int64_t nedges, const PlanWs &w, const Pla
     return check_launch("merge");
 }
 
-template <int K, int RED, int WM>
+template <int K, int RED, int WM, bool DW = false>
 int dispatch_lanes(int L, const Trav &t, int64_t nedges, const PlanWs &w, const PlanBounds &b, float *out,
-                   int32_t *out_arg, hipStream_t stream) {
+                   int32_t *out_arg, const EdgeGrad &eg, hipStream_t stream) {
     switch (L) {
-        case 1: return launch_traversal_t<K, 1, RED, WM>(t, nedges, w, b, out, out_arg, stream);
-        case 2: return launch_traversal_t<K, 2, RED, WM>(t, nedges, w, b, out, out_arg, stream);
-        case 4: return launch_traversal_t<K, 4, RED, WM>(t, nedges, w, b, out, out_arg, stream);
-        case 8: return launch_traversal_t<K, 8, RED, WM>(t, nedges, w, b, out, out_arg, stream);
-        case 16: return launch_traversal_t<K, 16, RED, WM>(t, nedges, w, b, out, out_arg, stream);
-        case 32: return launch_traversal_t<K, 32, RED, WM>(t, nedges, w, b, out, out_arg, stream);
-        case 64: return launch_traversal_t<K, 64, RED, WM>(t, nedges, w, b, out, out_arg, stream);
+        case 1: return launch_traversal_t<K, 1, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream);
+        case 2: return launch_traversal_t<K, 2, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream);
+        case 4: return launch_traversal_t<K, 4, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream);
+        case 8: return launch_traversal_t<K, 8, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream);
+        case 16: return launch_traversal_t<K, 16, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream);
+        case 32: return launch_traversal_t<K, 32, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream);
+        case 64: return launch_traversal_t<K, 64, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream);
         default: return fail(TIGA_EINVAL, "internal: lanes per edge %d", L);
     }
 }
@@ -184,7 +221,7 @@ size_t traversal_ws_bytes(int64_t nrows, int64_t nedges, int64_t feat, bool with
 }
 
 int launch_traversal(const Trav &t0, int64_t table_rows, int64_t nedges, const Layout &lay, int red, int wm, void *ws,
-                     float *out, int32_t *out_arg, hipStream_t stream) {
+                     float *out, int32_t *out_arg, hipStream_t stream, const EdgeGrad &eg) {
     if (t0.nrows == 0) return TIGA_OK;
     Trav t = t0;
     const int64_t tb = table_rows * lay.fu * lay.K * 4;
@@ -192,8 +229,15 @@ int launch_traversal(const Trav &t0, int64_t table_rows, int64_t nedges, const L
     const PlanBounds b = plan_bounds(t.nrows, nedges, lay.g);
     Carve c(ws);
     const PlanWs w = carve_plan(c, b, lay.fu * lay.K, red == RED_MAX);
+    if (eg.dw) {
+        // fused sum backward over the reverse incidence: one feature block
+        if (red != RED_SUM || wm != W_INDIRECT || lay.fu > lay.L)
+            return fail(TIGA_EUNSUPPORTED, "internal: fused edge gradients need a sum over one feature block");
+        if (lay.K == 4) return dispatch_lanes<4, RED_SUM, W_INDIRECT, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream);
+        return dispatch_lanes<1, RED_SUM, W_INDIRECT, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream);
+    }
 #define TIGA_DISPATCH(KK, RR, WW) \
-    if (lay.K == KK && red == RR && wm == WW) return dispatch_lanes<KK, RR, WW>(lay.L, t, nedges, w, b, out, out_arg, stream)
+    if (lay.K == KK && red == RR && wm == WW) return dispatch_lanes<KK, RR, WW>(lay.L, t, nedges, w, b, out, out_arg, eg, stream)
     TIGA_DISPATCH(4, RED_SUM, W_DIRECT);
     TIGA_DISPATCH(4, RED_SUM, W_NONE);
     TIGA_DISPATCH(4, RED_SUM, W_INDIRECT);

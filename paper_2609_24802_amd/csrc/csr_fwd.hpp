@@ -18,11 +18,19 @@ Layout layout_for(int64_t feat, bool vec);
 // Workspace bytes for one traversal over (nrows, nedges) with `feat` features.
 size_t traversal_ws_bytes(int64_t nrows, int64_t nedges, int64_t feat, bool with_arg);
 
+// Optional edge gradients formed during a traversal of the reverse incidence
+// (sum backward): dw[eid[e]] = <x[row], table[idx[e]]> for every folded edge.
+struct EdgeGrad {
+    const float *x = nullptr;  // [nrows, feat] rows of the traversal's own rows
+    float *dw = nullptr;       // [nedges], indexed by eid
+};
+
 // Enqueue plan + gather-reduce + merge: out[i, :] = reduce_{e in row i} w(e) * table[idx[e], :].
 // `table_rows` is the row count of t.table (and t.arg); tables below 4 GiB are
-// read through buffer resources.
+// read through buffer resources.  With eg.dw the traversal must be a sum with
+// W_INDIRECT weights over one feature block (fu <= L).
 int launch_traversal(const Trav &t, int64_t table_rows, int64_t nedges, const Layout &lay, int red, int wm, void *ws,
-                     float *out, int32_t *out_arg, hipStream_t stream);
+                     float *out, int32_t *out_arg, hipStream_t stream, const EdgeGrad &eg = EdgeGrad{});
 
 }  // namespace csr
 }  // namespace tiga

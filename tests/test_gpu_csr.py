@@ -163,6 +163,50 @@ def test_sum_backward_random(lib):
     assert np.array_equal(outs[1][0], outs[2][0]) and np.array_equal(outs[1][1], outs[2][1])
 
 
+@pytest.mark.parametrize("F", [1, 3, 16, 17, 64, 260])
+def test_sum_backward_gather_modes(lib, F):
+    """With the reverse incidence: both gradients in one traversal (rows of one
+    feature block), dw from the edge kernel when the row needs several blocks,
+    and each gradient alone."""
+    deg = mixed_degrees(600, 21 + F, big=(9000,))
+    row_ptr, col, x, w, dy = make_graph(deg, 700, F, seed=21 + F)
+    rel = lib.Csr(dev(row_ptr), dev(col), 700)
+    rdx, rdxa, rdw, rdwa = oracle.csr_sum_bwd(row_ptr, col, x, w, dy, 700)
+    rev = lib.tiga_csr_transpose(rel)
+    dx, dw = lib.tiga_mp_csr_bwd(rel, dev(dy), dev(x), dev(w), rev=rev)
+    assert_terms_close(host(dx), rdx, rdxa, what=f"sum dx F={F}")
+    assert_terms_close(host(dw), rdw, rdwa, what=f"sum dw F={F}")
+    dx1, none = lib.tiga_mp_csr_bwd(rel, dev(dy), dev(x), dev(w), rev=rev, want_dw=False)
+    assert none is None
+    assert_terms_close(host(dx1), rdx, rdxa, what=f"sum dx alone F={F}")
+    none, dw1 = lib.tiga_mp_csr_bwd(rel, dev(dy), dev(x), dev(w), rev=rev, want_dx=False)
+    assert none is None
+    assert_terms_close(host(dw1), rdw, rdwa, what=f"sum dw alone F={F}")
+
+
+def test_kernel_events_last_one_call(lib):
+    """Events armed before a call without a fused kernel (the transpose) are
+    dropped by it: the next forward records nothing into them."""
+    deg = mixed_degrees(300, 5)
+    row_ptr, col, x, w, _ = make_graph(deg, 400, 16, seed=5)
+    rel = lib.Csr(dev(row_ptr), dev(col), 400)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    b.record()
+    torch.cuda.synchronize()
+    before = a.elapsed_time(b)
+    lib.tiga_mp_set_kernel_events(a, b)
+    lib.tiga_csr_transpose(rel)
+    lib.tiga_mp_csr_fwd(rel, dev(x), dev(w))
+    torch.cuda.synchronize()
+    assert a.elapsed_time(b) == before
+    # armed right before a forward, the events bracket its kernel
+    lib.tiga_mp_set_kernel_events(a, b)
+    lib.tiga_mp_csr_fwd(rel, dev(x), dev(w))
+    torch.cuda.synchronize()
+    assert a.elapsed_time(b) != before
+
+
 def test_transpose_is_stable_sort(lib):
     deg = mixed_degrees(3000, 13, big=(70000,))
     row_ptr, col, *_ = make_graph(deg, 100_000, 1, seed=13)
