@@ -162,11 +162,11 @@ int launch_bwd(const BwdArgs &a, void *ws, hipStream_t stream) {
     if (atomic_dx) {
         if (int rc = fill_u32(a.dx, 0u, rel->num_src * static_cast<int64_t>(a.feat), stream)) return rc;
     }
-    // Sum with the reverse incidence and both gradients: one traversal of the
+    // With the reverse incidence and both gradients: one traversal of the
     // reverse incidence gathers each dy row once and forms dx_j and dw_e
     // together (x_j is the source's own row), when the row fits one feature
     // block.  Otherwise dw comes from the row-parallel edge kernel.
-    const bool fused = a.red == RED_SUM && a.rev && a.dx && a.dw && a.x && lay.fu <= lay.L;
+    const bool fused = a.rev && a.dx && a.dw && a.x && lay.fu <= lay.L;
     if ((a.dw || atomic_dx) && !fused && rel->num_dst > 0) {
         EdgeT t{rel->row_ptr, rel->col_idx, a.w, a.x, a.dy, a.arg, atomic_dx ? a.dx : nullptr, a.dw,
                 rel->num_dst, lay.fu};

@@ -7,9 +7,9 @@ namespace csr {
 
 namespace {
 
-// Edge gradient of the sum backward, formed during the traversal of the
-// reverse incidence: dw[e] = <x_j, dy[dst(e)]> for the source row j being
-// folded.  Each lane holds one unit of x_j; the L lanes of an edge slot add
+// Edge gradient of the backward, formed during the traversal of the reverse
+// incidence: dw[e] = <x_j, dy[dst(e)]> for the source row j being folded
+// (for max, only the units whose argmax is e are nonzero when they arrive).  Each lane holds one unit of x_j; the L lanes of an edge slot add
 // their parts by a fixed shuffle tree and the slot's first lane writes dw[e].
 // The row must fit one feature block (fu <= L).
 template <int K, int L>
@@ -230,11 +230,18 @@ int launch_traversal(const Trav &t0, int64_t table_rows, int64_t nedges, const L
     Carve c(ws);
     const PlanWs w = carve_plan(c, b, lay.fu * lay.K, red == RED_MAX);
     if (eg.dw) {
-        // fused sum backward over the reverse incidence: one feature block
-        if (red != RED_SUM || wm != W_INDIRECT || lay.fu > lay.L)
-            return fail(TIGA_EUNSUPPORTED, "internal: fused edge gradients need a sum over one feature block");
-        if (lay.K == 4) return dispatch_lanes<4, RED_SUM, W_INDIRECT, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream);
-        return dispatch_lanes<1, RED_SUM, W_INDIRECT, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream);
+        // fused backward over the reverse incidence (sum: W_INDIRECT; max: the
+        // argmax-routed W_ROUTE, whose unselected units reach the hook as zero)
+        if (red != RED_SUM || (wm != W_INDIRECT && wm != W_ROUTE) || lay.fu > lay.L)
+            return fail(TIGA_EUNSUPPORTED, "internal: fused edge gradients need a routed sum over one feature block");
+        if (wm == W_INDIRECT) {
+            if (lay.K == 4)
+                return dispatch_lanes<4, RED_SUM, W_INDIRECT, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream);
+            return dispatch_lanes<1, RED_SUM, W_INDIRECT, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream);
+        }
+        if (lay.K == 4)
+            return dispatch_lanes<4, RED_SUM, W_ROUTE, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream);
+        return dispatch_lanes<1, RED_SUM, W_ROUTE, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream);
     }
 #define TIGA_DISPATCH(KK, RR, WW) \
     if (lay.K == KK && red == RR && wm == WW) return dispatch_lanes<KK, RR, WW>(lay.L, t, nedges, w, b, out, out_arg, eg, stream)

@@ -28,7 +28,7 @@ struct EdgeGrad {
 // Enqueue plan + gather-reduce + merge: out[i, :] = reduce_{e in row i} w(e) * table[idx[e], :].
 // `table_rows` is the row count of t.table (and t.arg); tables below 4 GiB are
 // read through buffer resources.  With eg.dw the traversal must be a sum with
-// W_INDIRECT weights over one feature block (fu <= L).
+// W_INDIRECT or W_ROUTE weights over one feature block (fu <= L).
 int launch_traversal(const Trav &t, int64_t table_rows, int64_t nedges, const Layout &lay, int red, int wm, void *ws,
                      float *out, int32_t *out_arg, hipStream_t stream, const EdgeGrad &eg = EdgeGrad{});
 

@@ -114,7 +114,7 @@ def test_sum_integer_inputs_bit_exact(lib, F):
         assert np.array_equal(host(dw), rdw.astype(np.float32))
 
 
-@pytest.mark.parametrize("F", [1, 3, 16, 17, 64])
+@pytest.mark.parametrize("F", [1, 3, 16, 17, 64, 260])
 def test_max_forward_backward_exact(lib, F):
     deg = mixed_degrees(800, 200 + F, big=(12000,))
     row_ptr, col, x, w, dy = make_graph(deg, 600, F, seed=F + 11)
