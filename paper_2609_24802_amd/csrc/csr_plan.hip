@@ -3,8 +3,9 @@
 // count: per tile of kPlanTile rows, the chunks of each class, partial slots
 //        and split rows its non-short rows need;
 // scan:  exclusive prefix over tiles (one block), totals to PlanCounts;
-// write: each tile recomputes its rows and writes descriptors at its offsets;
-//        class c's descriptors follow those of classes 0..c-1.
+// write: each tile recomputes its rows and writes descriptors at its offsets,
+//        in row order within each class; class c's descriptors follow those
+//        of classes 0..c-1.
 // Descriptor positions depend only on the topology.
 #include "csr_common.hpp"
 
@@ -17,30 +18,35 @@ struct Need {
     int64_t v[kPlanVals];  // chunks per class, partial slots, split rows
 };
 
-__device__ __forceinline__ Need row_need(const Geom &g, const int64_t *__restrict__ ptr, int64_t row, int64_t nrows,
-                                         int64_t &e0, int64_t &deg) {
+// Chunks per class, partial slots and split rows needed by a row of degree deg.
+__device__ __forceinline__ Need need_of(const Geom &g, int64_t deg) {
     Need r;
 #pragma unroll
     for (int k = 0; k < kPlanVals; ++k) r.v[k] = 0;
+    if (deg > g.DS) {
+        const int64_t nch = (deg + g.CH - 1) / g.CH;
+        const int64_t last = deg - (nch - 1) * g.CH;
+        const int c = chunk_class(g, last);
+        r.v[0] += nch - 1 + (c == 0);
+        r.v[1] += (c == 1);
+        r.v[2] += (c == 2);
+        if (nch > 1) {
+            r.v[kClasses] = nch;
+            r.v[kClasses + 1] = 1;
+        }
+    }
+    return r;
+}
+
+__device__ __forceinline__ Need row_need(const Geom &g, const int64_t *__restrict__ ptr, int64_t row, int64_t nrows,
+                                         int64_t &e0, int64_t &deg) {
     e0 = 0;
     deg = 0;
     if (row < nrows) {
         e0 = ptr[row];
         deg = ptr[row + 1] - e0;
-        if (deg > g.DS) {
-            const int64_t nch = (deg + g.CH - 1) / g.CH;
-            const int64_t last = deg - (nch - 1) * g.CH;
-            const int c = chunk_class(g, last);
-            r.v[0] += nch - 1 + (c == 0);
-            r.v[1] += (c == 1);
-            r.v[2] += (c == 2);
-            if (nch > 1) {
-                r.v[kClasses] = nch;
-                r.v[kClasses + 1] = 1;
-            }
-        }
     }
-    return r;
+    return need_of(g, deg);
 }
 
 // Block-wide exclusive scan of kPlanVals counters; returns block totals.
@@ -119,13 +125,25 @@ __global__ __launch_bounds__(kBlock) void plan_scan_kernel(int64_t *__restrict__
     }
 }
 
-// Descriptors of a tile: thread t owns rows base + r * kBlock + t (r <
-// kPlanRowsPerThread) and writes them after the rows of threads 0..t-1.
+// Descriptors of a tile in row order: thread t owns the kPlanRowsPerThread
+// consecutive rows base + t * kPlanRowsPerThread + r and writes them after the
+// rows of threads 0..t-1, so consecutive descriptors of a class are rows in
+// ascending order (a work item of several chunks writes neighbouring output
+// rows).  The tile's row pointers are staged in LDS first (coalesced loads;
+// one pad slot per 8 entries keeps the per-thread reads off a single bank).
+__host__ __device__ constexpr int pad_ix(int i) { return i + (i >> 3); }
+
 __global__ __launch_bounds__(kBlock) void plan_write_kernel(Geom g, const int64_t *__restrict__ ptr, int64_t nrows,
                                                             const int64_t *__restrict__ tile_vals,
                                                             const PlanCounts *__restrict__ counts,
                                                             Desc *__restrict__ chunks, Split *__restrict__ splits) {
+    __shared__ int64_t sptr[pad_ix(kPlanTile) + 1];
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kPlanTile;
+    for (int i = threadIdx.x; i <= kPlanTile; i += kBlock) {
+        const int64_t row = base + i;
+        sptr[pad_ix(i)] = ptr[row < nrows ? row : nrows];
+    }
+    __syncthreads();
     int64_t cbase[kClasses];
     int64_t b = 0;
 #pragma unroll
@@ -139,7 +157,11 @@ __global__ __launch_bounds__(kBlock) void plan_write_kernel(Geom g, const int64_
     for (int k = 0; k < kPlanVals; ++k) mine.v[k] = 0;
 #pragma unroll
     for (int r = 0; r < kPlanRowsPerThread; ++r) {
-        const Need n = row_need(g, ptr, base + r * kBlock + threadIdx.x, nrows, e0[r], deg[r]);
+        const int i = threadIdx.x * kPlanRowsPerThread + r;
+        const bool in = base + i < nrows;
+        e0[r] = in ? sptr[pad_ix(i)] : 0;
+        deg[r] = in ? sptr[pad_ix(i + 1)] - e0[r] : 0;
+        const Need n = need_of(g, deg[r]);
 #pragma unroll
         for (int k = 0; k < kPlanVals; ++k) mine.v[k] += n.v[k];
     }
@@ -150,7 +172,7 @@ __global__ __launch_bounds__(kBlock) void plan_write_kernel(Geom g, const int64_
 #pragma unroll
     for (int r = 0; r < kPlanRowsPerThread; ++r) {
         if (deg[r] <= g.DS) continue;
-        const int64_t row = base + r * kBlock + threadIdx.x;
+        const int64_t row = base + threadIdx.x * kPlanRowsPerThread + r;
         const int64_t nch = (deg[r] + g.CH - 1) / g.CH;
         const int slot0 = nch > 1 ? static_cast<int>(run.v[kClasses]) : -1;
         for (int64_t k = 0; k < nch; ++k) {
