@@ -49,9 +49,12 @@ __device__ __forceinline__ Need row_need(const Geom &g, const int64_t *__restric
     return need_of(g, deg);
 }
 
-// Block-wide exclusive scan of kPlanVals counters; returns block totals.
+// Block-wide exclusive scan of kPlanVals counters over BLOCK threads; returns
+// the block totals.
+template <int BLOCK = kBlock>
 __device__ __forceinline__ Need block_excl_scan(const Need &v, Need &excl) {
-    __shared__ int64_t sh[kPlanVals][kWavesPerBlock];
+    constexpr int W = BLOCK / kWave;
+    __shared__ int64_t sh[kPlanVals][W];
     const int lane = lane_id();
     const int wave = threadIdx.x / kWave;
     Need inc, tot;
@@ -65,7 +68,7 @@ __device__ __forceinline__ Need block_excl_scan(const Need &v, Need &excl) {
     for (int k = 0; k < kPlanVals; ++k) {
         int64_t off = 0, t = 0;
 #pragma unroll
-        for (int w = 0; w < kWavesPerBlock; ++w) {
+        for (int w = 0; w < W; ++w) {
             if (w < wave) off += sh[k][w];
             t += sh[k][w];
         }
@@ -76,8 +79,10 @@ __device__ __forceinline__ Need block_excl_scan(const Need &v, Need &excl) {
     return tot;
 }
 
-__global__ __launch_bounds__(kBlock) void plan_count_kernel(Geom g, const int64_t *__restrict__ ptr, int64_t nrows,
+template <int L>
+__global__ __launch_bounds__(kBlock) void plan_count_kernel(const int64_t *__restrict__ ptr, int64_t nrows,
                                                             int64_t *__restrict__ tile_vals) {
+    constexpr Geom g = make_geom(L);  // compile-time chunk geometry: divisions by constants
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kPlanTile;
     Need acc;
 #pragma unroll
@@ -89,27 +94,48 @@ __global__ __launch_bounds__(kBlock) void plan_count_kernel(Geom g, const int64_
 #pragma unroll
         for (int k = 0; k < kPlanVals; ++k) acc.v[k] += n.v[k];
     }
-    Need excl;
-    const Need tot = block_excl_scan(acc, excl);
-    if (threadIdx.x < kPlanVals) tile_vals[kPlanVals * blockIdx.x + threadIdx.x] = tot.v[threadIdx.x];
+    // block totals: wave sums, then thread 0 adds the waves
+    __shared__ int64_t sh[kPlanVals][kWavesPerBlock];
+#pragma unroll
+    for (int k = 0; k < kPlanVals; ++k) {
+        int64_t v = acc.v[k];
+#pragma unroll
+        for (int m = 1; m < kWave; m <<= 1) v += __shfl_xor(v, m, kWave);
+        if (lane_id() == 0) sh[k][threadIdx.x / kWave] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int k = 0; k < kPlanVals; ++k) {
+            int64_t t = 0;
+#pragma unroll
+            for (int w = 0; w < kWavesPerBlock; ++w) t += sh[k][w];
+            tile_vals[kPlanVals * blockIdx.x + k] = t;
+        }
+    }
 }
 
-// One block: exclusive scan over the tiles, in place, and the totals.  Each
-// thread first sums a contiguous run of tiles, then one block scan combines
-// the runs.
-__global__ __launch_bounds__(kBlock) void plan_scan_kernel(int64_t *__restrict__ tile_vals, int64_t tiles,
-                                                           PlanCounts *__restrict__ counts) {
-    const int64_t per = (tiles + kBlock - 1) / kBlock;
+// One block of kScanBlock threads: exclusive scan over the tiles, in place,
+// and the totals.  Each thread first sums a contiguous run of tiles, then one
+// block scan combines the runs.
+constexpr int kScanBlock = 1024;
+
+__global__ __launch_bounds__(kScanBlock) void plan_scan_kernel(int64_t *__restrict__ tile_vals, int64_t tiles,
+                                                               PlanCounts *__restrict__ counts) {
+    const int64_t per = (tiles + kScanBlock - 1) / kScanBlock;
     const int64_t t0 = static_cast<int64_t>(threadIdx.x) * per;
     const int64_t t1 = t0 + per < tiles ? t0 + per : tiles;
     Need sum;
 #pragma unroll
     for (int k = 0; k < kPlanVals; ++k) sum.v[k] = 0;
+    // unrolled so that several tiles' loads are in flight at once
+#pragma unroll 8
     for (int64_t t = t0; t < t1; ++t)
 #pragma unroll
         for (int k = 0; k < kPlanVals; ++k) sum.v[k] += tile_vals[kPlanVals * t + k];
     Need excl;
-    const Need tot = block_excl_scan(sum, excl);
+    const Need tot = block_excl_scan<kScanBlock>(sum, excl);
+#pragma unroll 8
     for (int64_t t = t0; t < t1; ++t)
 #pragma unroll
         for (int k = 0; k < kPlanVals; ++k) {
@@ -133,10 +159,12 @@ __global__ __launch_bounds__(kBlock) void plan_scan_kernel(int64_t *__restrict__
 // one pad slot per 8 entries keeps the per-thread reads off a single bank).
 __host__ __device__ constexpr int pad_ix(int i) { return i + (i >> 3); }
 
-__global__ __launch_bounds__(kBlock) void plan_write_kernel(Geom g, const int64_t *__restrict__ ptr, int64_t nrows,
+template <int L>
+__global__ __launch_bounds__(kBlock) void plan_write_kernel(const int64_t *__restrict__ ptr, int64_t nrows,
                                                             const int64_t *__restrict__ tile_vals,
                                                             const PlanCounts *__restrict__ counts,
                                                             Desc *__restrict__ chunks, Split *__restrict__ splits) {
+    constexpr Geom g = make_geom(L);
     __shared__ int64_t sptr[pad_ix(kPlanTile) + 1];
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kPlanTile;
     for (int i = threadIdx.x; i <= kPlanTile; i += kBlock) {
@@ -203,16 +231,32 @@ __global__ __launch_bounds__(kBlock) void plan_write_kernel(Geom g, const int64_
 
 }  // namespace
 
-int launch_plan(const int64_t *ptr, int64_t nrows, const Geom &g, const PlanBounds &b, const PlanWs &w,
-                hipStream_t stream) {
+namespace {
+template <int L>
+int launch_plan_t(const int64_t *ptr, int64_t nrows, const PlanBounds &b, const PlanWs &w, hipStream_t stream) {
     const unsigned tiles = static_cast<unsigned>(b.tiles);
-    hipLaunchKernelGGL(plan_count_kernel, dim3(tiles), dim3(kBlock), 0, stream, g, ptr, nrows, w.tile_vals);
+    hipLaunchKernelGGL(plan_count_kernel<L>, dim3(tiles), dim3(kBlock), 0, stream, ptr, nrows, w.tile_vals);
     if (int rc = check_launch("plan count")) return rc;
-    hipLaunchKernelGGL(plan_scan_kernel, dim3(1), dim3(kBlock), 0, stream, w.tile_vals, b.tiles, w.counts);
+    hipLaunchKernelGGL(plan_scan_kernel, dim3(1), dim3(kScanBlock), 0, stream, w.tile_vals, b.tiles, w.counts);
     if (int rc = check_launch("plan scan")) return rc;
-    hipLaunchKernelGGL(plan_write_kernel, dim3(tiles), dim3(kBlock), 0, stream, g, ptr, nrows, w.tile_vals, w.counts,
+    hipLaunchKernelGGL(plan_write_kernel<L>, dim3(tiles), dim3(kBlock), 0, stream, ptr, nrows, w.tile_vals, w.counts,
                        w.chunks, w.splits);
     return check_launch("plan write");
+}
+}  // namespace
+
+int launch_plan(const int64_t *ptr, int64_t nrows, const Geom &g, const PlanBounds &b, const PlanWs &w,
+                hipStream_t stream) {
+    switch (g.L) {
+        case 1: return launch_plan_t<1>(ptr, nrows, b, w, stream);
+        case 2: return launch_plan_t<2>(ptr, nrows, b, w, stream);
+        case 4: return launch_plan_t<4>(ptr, nrows, b, w, stream);
+        case 8: return launch_plan_t<8>(ptr, nrows, b, w, stream);
+        case 16: return launch_plan_t<16>(ptr, nrows, b, w, stream);
+        case 32: return launch_plan_t<32>(ptr, nrows, b, w, stream);
+        case 64: return launch_plan_t<64>(ptr, nrows, b, w, stream);
+        default: return fail(TIGA_EINVAL, "internal: plan for %d lanes per edge", g.L);
+    }
 }
 
 }  // namespace csr
