@@ -116,10 +116,6 @@ __device__ __forceinline__ int64_t wave_incl_scan(int64_t v) {
 }
 
 template <class T>
-__device__ __forceinline__ T ldg_stream(const T *p) {
-    return __builtin_nontemporal_load(p);
-}
-template <class T>
 __device__ __forceinline__ void stg_stream(T *p, T v) {
     __builtin_nontemporal_store(v, p);
 }

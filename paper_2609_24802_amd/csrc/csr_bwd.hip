@@ -47,8 +47,8 @@ __device__ __forceinline__ void edge_pass(const EdgeT &t, int64_t row, int64_t e
         for (int r = 0; r < kUnroll; ++r) {
             const int64_t e = base + static_cast<int64_t>(r) * SL + s;
             ok[r] = e < e1;
-            c[r] = ok[r] ? ldg_stream(t.col + e) : 0;
-            wv[r] = ok[r] ? (t.w ? ldg_stream(t.w + e) : 1.0f) : 0.0f;
+            c[r] = ok[r] ? t.col[e] : 0;  // cached: neighbouring items share lines
+            wv[r] = ok[r] ? (t.w ? t.w[e] : 1.0f) : 0.0f;
         }
         Vec<K> xv[kUnroll];
 #pragma unroll

@@ -416,12 +416,15 @@ __device__ __forceinline__ void run_edges(const Trav &t, const Table<K, BUF, NT>
         for (int r = 0; r < kUnroll; ++r) {
             const int k = k0 + r * SL + s;
             ok[r] = k < n;
-            c[r] = ok[r] ? ldg_stream(colr + k) : 0;
+            // ids and weights take ordinary (cached) loads: neighbouring work
+            // items share their cache lines, which the non-temporal hint would
+            // let go back to HBM between the items
+            c[r] = ok[r] ? colr[k] : 0;
             ee[r] = 0;
             if constexpr (WM == W_DIRECT) {
-                wv[r] = ok[r] ? ldg_stream(wr + k) : 0.0f;
+                wv[r] = ok[r] ? wr[k] : 0.0f;
             } else if constexpr (WM == W_INDIRECT || WM == W_ROUTE) {
-                ee[r] = ok[r] ? ldg_stream(er + k) : 0;
+                ee[r] = ok[r] ? er[k] : 0;
                 wv[r] = ok[r] ? (t.w ? t.w[ee[r]] : 1.0f) : 0.0f;
             } else {
                 wv[r] = ok[r] ? 1.0f : 0.0f;
