@@ -282,3 +282,69 @@ def tiga_mp_dense_fwd(pos: torch.Tensor, q: torch.Tensor, eps: float, y=None, ws
     _check(lib.tiga_mp_dense_fwd(n, _ptr(pos), _ptr(q), float(eps), REDUCE_SUM, _ptr(y), _ptr(ws), ws.numel(),
                                  _stream()))
     return y
+
+
+# ------------------------------------------------------------ autograd wrappers
+#
+# The paper's Torch interop (the fused operator as a differentiable function):
+# the forward calls the fused entry point, the backward its vector-Jacobian
+# product.  The sum saves x and w (dx needs w, dw needs x); max also saves the
+# forward's argmax, which routes its gradients.  The relation is a topology
+# snapshot: it is not differentiated.
+
+
+class CsrAggregate(torch.autograd.Function):
+    """y = reduce_{e in row i} w[e] * x[col[e]] over a stored CSR relation."""
+
+    @staticmethod
+    def forward(ctx, x, w, rel, reducer, rev):
+        y, arg = tiga_mp_csr_fwd(rel, x, w, reducer=reducer)
+        ctx.rel, ctx.reducer, ctx.rev = rel, reducer, rev
+        ctx.save_for_backward(x, w, arg)
+        if arg is not None:
+            ctx.mark_non_differentiable(arg)
+        return y, arg
+
+    @staticmethod
+    def backward(ctx, gy, _garg):
+        x, w, arg = ctx.saved_tensors
+        want_dx = ctx.needs_input_grad[0]
+        want_dw = w is not None and ctx.needs_input_grad[1]
+        if not (want_dx or want_dw):
+            return None, None, None, None, None
+        dx, dw = tiga_mp_csr_bwd(ctx.rel, gy.contiguous(), x, w, reducer=ctx.reducer, argmax=arg, rev=ctx.rev,
+                                 want_dx=want_dx, want_dw=want_dw)
+        return dx, dw, None, None, None
+
+
+def csr_aggregate(rel: Csr, x: torch.Tensor, w: torch.Tensor | None = None, reducer: int = REDUCE_SUM,
+                  rev: CsrT | None = None):
+    """Differentiable fused aggregation; returns (y, argmax or None).  With `rev` (the reverse incidence)
+    the backward is the deterministic single traversal, without it dx accumulates by atomics."""
+    return CsrAggregate.apply(x, w, rel, reducer, rev)
+
+
+class RadiusAggregate(torch.autograd.Function):
+    """y_i = sum_{j != i, |p_j - p_i| < r} exp(-|p_j - p_i|^2 / sigma^2) x_j (membership not differentiated)."""
+
+    @staticmethod
+    def forward(ctx, pos, x, radius, sigma):
+        y, _ = tiga_mp_radius_fwd(pos, x, radius, sigma, want_count=False)
+        ctx.radius, ctx.sigma = radius, sigma
+        ctx.save_for_backward(pos, x)
+        return y
+
+    @staticmethod
+    def backward(ctx, gy):
+        pos, x = ctx.saved_tensors
+        want_dpos, want_dx = ctx.needs_input_grad[0], ctx.needs_input_grad[1]
+        if not (want_dpos or want_dx):
+            return None, None, None, None
+        dx, dpos = tiga_mp_radius_bwd(pos, x, gy.contiguous(), ctx.radius, ctx.sigma, want_dx=want_dx,
+                                      want_dpos=want_dpos)
+        return dpos, dx, None, None
+
+
+def radius_aggregate(pos: torch.Tensor, x: torch.Tensor, radius: float, sigma: float) -> torch.Tensor:
+    """Differentiable fused aggregation over the generated radius relation."""
+    return RadiusAggregate.apply(pos, x, radius, sigma)

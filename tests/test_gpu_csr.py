@@ -321,3 +321,26 @@ def test_config5_billion_edges_sampled(lib):
     rhs = (outw[:, None] * xd.double()).sum(0)
     scale = (outw[:, None] * xd.double().abs()).sum(0)
     assert torch.all((lhs - rhs).abs() <= 1e-5 * scale)
+
+
+@pytest.mark.parametrize("reducer,use_rev", [(0, False), (0, True), (1, True)])
+def test_autograd_wrapper(lib, reducer, use_rev):
+    """csr_aggregate's backward returns exactly the direct VJP call's gradients."""
+    F = 16
+    deg = mixed_degrees(500, 31)
+    row_ptr, col, x, w, dy = make_graph(deg, 450, F, seed=31)
+    rel = lib.Csr(dev(row_ptr), dev(col), 450)
+    rev = lib.tiga_csr_transpose(rel) if use_rev else None
+    xt = dev(x).requires_grad_(True)
+    wt = dev(w).requires_grad_(True)
+    y, arg = lib.csr_aggregate(rel, xt, wt, reducer=reducer, rev=rev)
+    y.backward(dev(dy))
+    ref_y, ref_arg = lib.tiga_mp_csr_fwd(rel, dev(x), dev(w), reducer=reducer)
+    assert torch.equal(y.detach(), ref_y)
+    dx, dw = lib.tiga_mp_csr_bwd(rel, dev(dy), dev(x), dev(w), reducer=reducer, argmax=ref_arg, rev=rev)
+    if use_rev:  # deterministic: identical bits
+        assert torch.equal(xt.grad, dx) and torch.equal(wt.grad, dw)
+    rdx, rdxa, rdw, rdwa = (oracle.csr_sum_bwd(row_ptr, col, x, w, dy, 450) if reducer == 0 else
+                            oracle.csr_max_bwd(row_ptr, col, x, w, host(ref_arg), dy, 450))
+    assert_terms_close(host(xt.grad), rdx, rdxa, what="autograd dx")
+    assert_terms_close(host(wt.grad), rdw, rdwa, what="autograd dw")

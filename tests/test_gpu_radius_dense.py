@@ -205,3 +205,21 @@ def test_config4_full_size_sampled(lib):
     pts = np.unique(np.random.default_rng(6).integers(0, 65536, 1500))
     ry, rya = oracle.dense_fwd(g["pos"], g["q"], g["eps"], pts=pts)
     assert_terms_close(host(y)[pts], ry, rya, what="config 4 y")
+
+
+def test_radius_autograd_wrapper(lib):
+    """radius_aggregate's backward returns the direct VJP call's gradients."""
+    n, F = 2500, 8
+    pos = cloud("uniform", n, 41)
+    x = synth.normal_f32(n * F, (89, n)).reshape(n, F)
+    dy = synth.normal_f32(n * F, (90, n)).reshape(n, F)
+    r, s = np.float32(0.07), np.float32(0.035)
+    pt = dev(pos).requires_grad_(True)
+    xt = dev(x).requires_grad_(True)
+    y = lib.radius_aggregate(pt, xt, r, s)
+    y.backward(dev(dy))
+    dx, dp = lib.tiga_mp_radius_bwd(dev(pos), dev(x), dev(dy), r, s)
+    assert torch.equal(xt.grad, dx) and torch.equal(pt.grad, dp)
+    rdx, rdxa, rdp, rdpa = oracle.radius_bwd(pos, x, dy, r, s)
+    assert_terms_close(host(xt.grad), rdx, rdxa, what="autograd radius dx")
+    assert_terms_close(host(pt.grad), rdp, rdpa, what="autograd radius dpos")
