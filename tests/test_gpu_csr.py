@@ -344,3 +344,34 @@ def test_autograd_wrapper(lib, reducer, use_rev):
                             oracle.csr_max_bwd(row_ptr, col, x, w, host(ref_arg), dy, 450))
     assert_terms_close(host(xt.grad), rdx, rdxa, what="autograd dx")
     assert_terms_close(host(wt.grad), rdw, rdwa, what="autograd dw")
+
+
+def test_sum_forward_all_positive_long_rows(lib):
+    """All-positive messages make sum|terms| equal |y|, so the 1e-5 bound is a
+    true relative-error bound; rows of 2e5 and 1e6 edges are split into many
+    chunks and merged."""
+    F = 16
+    deg = mixed_degrees(400, 51, big=(200_000, 1_000_000))
+    row_ptr, col, _, _, _ = make_graph(deg, 50_000, F, seed=51)
+    rng = np.random.default_rng(52)
+    x = rng.random((50_000, F)).astype(np.float32) + np.float32(0.5)
+    w = rng.random(col.size).astype(np.float32) + np.float32(0.5)
+    rel, y, _ = run_fwd(lib, row_ptr, col, x, w, 50_000, lib.REDUCE_SUM)
+    ry, rya = oracle.csr_sum_fwd(row_ptr, col, x, w)
+    assert np.allclose(rya, np.abs(ry))
+    assert_terms_close(y, ry, rya, what="all-positive sum")
+
+
+def test_forward_bit_identical_across_runs(lib):
+    """Sum and max forwards are deterministic: split rows merge in a fixed order."""
+    F = 32
+    deg = mixed_degrees(2000, 53, big=(150_000, 40_000))
+    row_ptr, col, x, w, _ = make_graph(deg, 3000, F, seed=53)
+    rel = lib.Csr(dev(row_ptr), dev(col), 3000)
+    xd, wd = dev(x), dev(w)
+    for red in (lib.REDUCE_SUM, lib.REDUCE_MAX):
+        a, aa = lib.tiga_mp_csr_fwd(rel, xd, wd, reducer=red)
+        b, bb = lib.tiga_mp_csr_fwd(rel, xd, wd, reducer=red)
+        assert torch.equal(a, b)
+        if red == lib.REDUCE_MAX:
+            assert torch.equal(aa, bb)
