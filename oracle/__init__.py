@@ -54,6 +54,10 @@ def _load():
                 "tiga_oracle_radius_bwd": (C.c_int, [i64, i32, vp, vp, vp, f32, f32, i64, vp, vp, vp, vp, vp]),
                 "tiga_oracle_radius_neighbors": (C.c_int, [i64, vp, f32, i64, vp, vp, vp, vp]),
                 "tiga_oracle_dense_fwd": (None, [i64, vp, vp, f32, i64, vp, vp, vp]),
+                "tiga_oracle_f16_to_double": (C.c_double, [C.c_uint16]),
+                "tiga_oracle_bf16_to_double": (C.c_double, [C.c_uint16]),
+                "tiga_oracle_attention_fwd": (C.c_int, [i64, i32, i32, C.c_int, vp, vp, vp, C.c_double,
+                                                        C.c_int, i64, vp, vp, vp, vp]),
             }
             for name, (res, args) in sig.items():
                 fn = getattr(lib, name)
@@ -191,3 +195,32 @@ def dense_fwd(pos, q, eps, pts=None):
     ya = np.empty((npts, 3), np.float64)
     _load().tiga_oracle_dense_fwd(n, _p(pos), _p(q), float(eps), npts, _p(pts), _p(y), _p(ya))
     return y, ya
+
+
+_ATTN_DTYPES = {"f16": 0, "bf16": 1}
+_ATTN_RELATIONS = {"triangular": 0, "dense": 1}
+
+
+def half_to_double(bits, dtype):
+    """Exact widening of 16-bit patterns (binary16 or bfloat16) to float64, one call per value."""
+    fn = _load().tiga_oracle_f16_to_double if dtype == "f16" else _load().tiga_oracle_bf16_to_double
+    bits = np.asarray(bits, np.uint16).reshape(-1)
+    return np.array([fn(int(b)) for b in bits], np.float64)
+
+
+def attention_fwd(q, k, v, scale, dtype="f16", relation="triangular", pts=None):
+    """Online-softmax attention over a triangular (causal, diagonal included) or dense relation.
+
+    q, k, v: uint16 bit patterns [H, n, D] (head-major).  Returns (y, yabs, lse): y and yabs fp64
+    [npts, H, D] (yabs = sum_j p_ij |v_jd| with normalized weights p), lse fp64 [npts, H]."""
+    q, k, v = (np.ascontiguousarray(a).view(np.uint16) for a in (q, k, v))
+    H, n, D = q.shape
+    pts, npts = _rows(pts, n)
+    y = np.empty((npts, H, D), np.float64)
+    ya = np.empty((npts, H, D), np.float64)
+    lse = np.empty((npts, H), np.float64)
+    rc = _load().tiga_oracle_attention_fwd(n, H, D, _ATTN_DTYPES[dtype], _p(q), _p(k), _p(v), float(scale),
+                                           _ATTN_RELATIONS[relation], npts, _p(pts), _p(y), _p(ya), _p(lse))
+    if rc != 0:
+        raise ValueError("oracle attention: unknown dtype or relation")
+    return y, ya, lse

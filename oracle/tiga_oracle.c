@@ -533,3 +533,94 @@ void tiga_oracle_dense_fwd(int64_t n, const float *pos, const float *q, float ep
         }
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Online-softmax reducer over an implicit triangular or dense relation      */
+/* (Section 4.8, online softmax; appendix "Causal attention as message       */
+/* passing")                                                                 */
+/* ------------------------------------------------------------------------ */
+
+/* IEEE 754 binary16: sign bit, 5 exponent bits (bias 15), 10 fraction bits.
+ * Every value is exactly representable in double. */
+double tiga_oracle_f16_to_double(uint16_t h) {
+    int s = h >> 15, e = (h >> 10) & 31, f = h & 1023;
+    double v;
+    if (e == 0)
+        v = ldexp((double)f, -24);            /* subnormal: f * 2^-24 */
+    else if (e == 31)
+        v = f ? NAN : INFINITY;
+    else
+        v = ldexp((double)(1024 + f), e - 25); /* (1 + f / 2^10) * 2^(e - 15) */
+    return s ? -v : v;
+}
+
+/* bfloat16: the upper 16 bits of an IEEE 754 binary32. */
+double tiga_oracle_bf16_to_double(uint16_t b) {
+    uint32_t u = (uint32_t)b << 16;
+    float x;
+    memcpy(&x, &u, sizeof x);
+    return (double)x;
+}
+
+/* Attention as message passing, one head at a time.  Destination i supplies the
+ * query q_i, source j the key k_j and value v_j; the relation is
+ *   triangular (relation 0):  N(i) = {0, ..., i}   (the diagonal is included)
+ *   dense      (relation 1):  N(i) = {0, ..., n-1}
+ * the message is the pair (score s_ij = scale * <q_i, k_j>, value v_j), and the
+ * online-softmax reducer finalizes to
+ *   y_i = sum_{j in N(i)} exp(s_ij) v_j / sum_{j in N(i)} exp(s_ij).
+ * The sums are evaluated after subtracting the row maximum of the scores, which
+ * changes nothing mathematically.  Inputs are [H][n][D] bit patterns (dtype 0 =
+ * binary16, 1 = bfloat16), widened exactly to double; all arithmetic is fp64.
+ * For each requested query row pts[k] (all rows if pts == NULL) and head h:
+ *   y   [k][h][d] = y_i,
+ *   yabs[k][h][d] = sum_j p_ij |v_jd| with p_ij the normalized weights,
+ *   lse [k][h]    = log sum_{j in N(i)} exp(s_ij).
+ * yabs and lse may be NULL.  Returns 0, or -1 for an unknown dtype/relation. */
+int tiga_oracle_attention_fwd(int64_t n, int32_t H, int32_t D, int dtype, const uint16_t *q,
+                              const uint16_t *k, const uint16_t *v, double scale, int relation,
+                              int64_t npts, const int64_t *pts, double *y, double *yabs, double *lse) {
+    if ((dtype != 0 && dtype != 1) || (relation != 0 && relation != 1)) return -1;
+    double (*cvt)(uint16_t) = dtype == 0 ? tiga_oracle_f16_to_double : tiga_oracle_bf16_to_double;
+    int64_t t;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (t = 0; t < npts * H; ++t) {
+        int64_t kk = t / H, h = t % H;
+        int64_t i = pts ? pts[kk] : kk;
+        int64_t last = relation == 0 ? i : n - 1;       /* N(i) = {0, ..., last} */
+        const uint16_t *qi = q + (h * n + i) * D;
+        double *out = y + (kk * H + h) * D;
+        double *mag = yabs ? yabs + (kk * H + h) * D : NULL;
+        double mx = -INFINITY, den = 0.0;
+        for (int64_t j = 0; j <= last; ++j) {          /* pass 1: the row maximum */
+            const uint16_t *kj = k + (h * n + j) * D;
+            double s = 0.0;
+            for (int d = 0; d < D; ++d) s += cvt(qi[d]) * cvt(kj[d]);
+            s *= scale;
+            if (s > mx) mx = s;
+        }
+        for (int d = 0; d < D; ++d) {
+            out[d] = 0.0;
+            if (mag) mag[d] = 0.0;
+        }
+        for (int64_t j = 0; j <= last; ++j) {          /* pass 2: weights and sums */
+            const uint16_t *kj = k + (h * n + j) * D;
+            const uint16_t *vj = v + (h * n + j) * D;
+            double s = 0.0;
+            for (int d = 0; d < D; ++d) s += cvt(qi[d]) * cvt(kj[d]);
+            s *= scale;
+            double p = exp(s - mx);
+            den += p;
+            for (int d = 0; d < D; ++d) {
+                out[d] += p * cvt(vj[d]);
+                if (mag) mag[d] += p * fabs(cvt(vj[d]));
+            }
+        }
+        for (int d = 0; d < D; ++d) {
+            out[d] /= den;
+            if (mag) mag[d] /= den;
+        }
+        if (lse) lse[kk * H + h] = mx + log(den);
+    }
+    return 0;
+}

@@ -216,3 +216,31 @@ def binary_grid_points(n: int, bits: int, key: tuple, span: int | None = None) -
     span = span if span is not None else (1 << bits)
     k = _rng(*key, 0).integers(0, span, size=(n, 3))
     return (k.astype(np.float64) * 2.0 ** -bits).astype(np.float32)
+
+
+def f32_to_half_bits(a: np.ndarray, dtype: str) -> np.ndarray:
+    """Round fp32 values to binary16 ("f16") or bfloat16 ("bf16") with round-to-nearest-even and
+    return the 16-bit patterns (uint16).  Input preparation only: finite inputs."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    if dtype == "f16":
+        return a.astype(np.float16).view(np.uint16)
+    if dtype == "bf16":
+        u = a.view(np.uint32).astype(np.uint64)
+        u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+        return u.astype(np.uint16)
+    raise ValueError(dtype)
+
+
+def attention_inputs(n: int, heads: int, width: int, dtype: str = "f16", cfg: int = 6, sigma: float = 1.0):
+    """Head-major [heads, n, width] query, key and value bit patterns, each drawn as sigma * N(0, 1)
+    in fp32 and rounded to `dtype`; scale = width ** -0.5 (the causal-attention example of the
+    appendix draws torch.randn in head-major storage and uses this scale)."""
+    out = {}
+    for a, name in enumerate(("q", "k", "v")):
+        x = normal_f32(heads * n * width, (cfg, a, n, heads, width))
+        if sigma != 1.0:
+            x *= np.float32(sigma)
+        out[name] = f32_to_half_bits(x, dtype).reshape(heads, n, width)
+    out["scale"] = np.float32(width ** -0.5)
+    out["dtype"] = dtype
+    return out
