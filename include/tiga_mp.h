@@ -228,6 +228,40 @@ size_t tiga_mp_dense_workspace(int64_t n);
 int tiga_mp_dense_fwd(int64_t n, const float *pos, const float *q, float eps, int reducer,
                       float *y, void *ws, size_t ws_bytes, void *stream);
 
+/* ------------------------------- online-softmax reducer (streaming attention) */
+
+/* 16-bit input types of the attention path. */
+enum tiga_dtype { TIGA_DT_F16 = 0 /* IEEE binary16 */, TIGA_DT_BF16 = 1 /* bfloat16 */ };
+
+/* Implicit relations of the attention path (no edge array). */
+enum tiga_relation {
+    TIGA_REL_TRIANGULAR = 0, /* N(i) = {0, ..., i}: causal, the diagonal included */
+    TIGA_REL_DENSE = 1       /* N(i) = {0, ..., n-1} */
+};
+
+/* Online-softmax reducer over an implicit triangular or dense relation: the
+ * streaming attention forward (appendix "Causal attention as message
+ * passing"; reducer state of Section 4.8: running maximum, mass and
+ * accumulator, combined by rescaling into a common maximum).  Per head h and
+ * destination i, with the message (score, value) of source j:
+ *   s_ij = scale * <q_i, k_j>,
+ *   y_i  = sum_{j in N(i)} exp(s_ij) v_j / sum_{j in N(i)} exp(s_ij),
+ *   lse_i = log sum_{j in N(i)} exp(s_ij).
+ * No score or weight array is stored.
+ *   q, k, v: [heads, n, width] head-major, 16-bit (dtype), 16-byte aligned
+ *            (a permuted view of a contiguous (heads, n, width) allocation
+ *            is the paper's logical (n, heads, width) tensor).
+ *   y:       [heads, n, width] of dtype, overwritten (rounded to nearest even).
+ *   lse:     fp32 [heads, n] or NULL.
+ * Scores, weights and sums are fp32 (products of the 16-bit inputs are exact);
+ * the normalized weights enter the value product rounded to dtype.  Every row
+ * is nonempty under both relations.  Requires width 64 or 128
+ * (TIGA_EUNSUPPORTED otherwise), n < 2^31, heads * n < 2^40, scale finite and
+ * > 0.  n == 0 or heads == 0 enqueues nothing.  Needs no workspace.
+ * Errors: TIGA_EINVAL, TIGA_EUNSUPPORTED, TIGA_EDEVICE. */
+int tiga_mp_attention_fwd(int64_t n, int32_t heads, int32_t width, int dtype, const void *q, const void *k,
+                          const void *v, float scale, int relation, void *y, float *lse, void *stream);
+
 /* ------------------------------------------------------------- profiling */
 
 /* Profiling aid.  Arms the calling thread so that its next entry-point call

@@ -21,6 +21,8 @@ LIB_PATH = os.path.join(_HERE, "libtiga_mp.so")
 TIGA_OK, TIGA_EINVAL, TIGA_EGRAPH, TIGA_EUNSUPPORTED, TIGA_EWORKSPACE, TIGA_EDEVICE = 0, -1, -2, -3, -4, -5
 REDUCE_SUM, REDUCE_MAX = 0, 1
 MSG_SRC, MSG_EDGE_SCALED_SRC = 0, 1
+DT_F16, DT_BF16 = 0, 1
+REL_TRIANGULAR, REL_DENSE = 0, 1
 _STATUS = {0: "TIGA_OK", -1: "TIGA_EINVAL", -2: "TIGA_EGRAPH", -3: "TIGA_EUNSUPPORTED",
            -4: "TIGA_EWORKSPACE", -5: "TIGA_EDEVICE"}
 
@@ -67,6 +69,8 @@ _SIGS = {
     "tiga_mp_dense_workspace": (C.c_size_t, [C.c_int64]),
     "tiga_mp_dense_fwd": (C.c_int, [C.c_int64, C.c_void_p, C.c_void_p, C.c_float, C.c_int, C.c_void_p,
                                     C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tiga_mp_attention_fwd": (C.c_int, [C.c_int64, C.c_int32, C.c_int32, C.c_int, C.c_void_p, C.c_void_p,
+                                        C.c_void_p, C.c_float, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p]),
     "tiga_mp_set_kernel_events": (C.c_int, [C.c_void_p, C.c_void_p]),
 }
 
@@ -282,6 +286,52 @@ def tiga_mp_dense_fwd(pos: torch.Tensor, q: torch.Tensor, eps: float, y=None, ws
     _check(lib.tiga_mp_dense_fwd(n, _ptr(pos), _ptr(q), float(eps), REDUCE_SUM, _ptr(y), _ptr(ws), ws.numel(),
                                  _stream()))
     return y
+
+
+def _head_major(t, name, layout, shape=None):
+    """The [heads, n, width] storage of t: t itself ("hnd": contiguous [heads, n, width]) or, for "nhd",
+    the (n, heads, width) view of a contiguous (heads, n, width) allocation permuted back."""
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype not in (torch.float16, torch.bfloat16):
+        raise TypeError(f"{name} must be float16 or bfloat16, got {t.dtype}")
+    if t.dim() != 3:
+        raise ValueError(f"{name} must have 3 dimensions")
+    if layout == "nhd":
+        t = t.permute(1, 0, 2)
+    elif layout != "hnd":
+        raise ValueError(f"unknown layout {layout!r}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be head-major storage (layout {layout!r})")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has head-major shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t
+
+
+def tiga_mp_attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, scale: float | None = None,
+                          relation: str = "triangular", want_lse: bool = False, layout: str = "hnd"):
+    """Online-softmax attention over the triangular (causal, diagonal included) or dense relation.
+
+    q, k, v: float16 or bfloat16, head-major [heads, n, width] (layout "hnd") or the (n, heads, width)
+    view of head-major storage (layout "nhd").  scale defaults to width ** -0.5.  Returns y in the
+    layout of q (and lse fp32 [heads, n] when want_lse)."""
+    lib = load()
+    qh = _head_major(q, "q", layout)
+    H, n, D = qh.shape
+    kh = _head_major(k, "k", layout, (H, n, D))
+    vh = _head_major(v, "v", layout, (H, n, D))
+    if kh.dtype != qh.dtype or vh.dtype != qh.dtype:
+        raise TypeError("q, k and v must share one dtype")
+    dt = DT_F16 if qh.dtype == torch.float16 else DT_BF16
+    rel = {"triangular": REL_TRIANGULAR, "dense": REL_DENSE}[relation]
+    if scale is None:
+        scale = D ** -0.5
+    yh = torch.empty(H, n, D, dtype=qh.dtype, device=qh.device)
+    lse = torch.empty(H, n, dtype=torch.float32, device=qh.device) if want_lse else None
+    _check(lib.tiga_mp_attention_fwd(n, H, D, dt, _ptr(qh), _ptr(kh), _ptr(vh), float(scale), rel, _ptr(yh),
+                                     _ptr(lse), _stream()))
+    y = yh.permute(1, 0, 2) if layout == "nhd" else yh
+    return (y, lse) if want_lse else y
 
 
 # ------------------------------------------------------------ autograd wrappers

@@ -124,3 +124,32 @@ def test_workspace_queries_monotone(clib):
     assert 0 < small < large
     assert clib.tiga_mp_radius_workspace(1000, 32) < clib.tiga_mp_radius_workspace(100000, 32)
     assert clib.tiga_mp_dense_workspace(65536) > 65536 * 16
+
+
+def test_attention_errors(clib):
+    from paper_2609_24802_amd import binding as b
+    fake = C.c_void_p(0x10000)
+    odd = C.c_void_p(0x10008)
+
+    def call(n=100, heads=2, width=64, dt=b.DT_F16, q=fake, k=fake, v=fake, scale=0.125, rel=b.REL_TRIANGULAR,
+             y=fake, lse=None):
+        return clib.tiga_mp_attention_fwd(n, heads, width, dt, q, k, v, scale, rel, y, lse, None)
+
+    assert call(width=96) == b.TIGA_EUNSUPPORTED
+    assert call(width=256) == b.TIGA_EUNSUPPORTED
+    assert call(n=1 << 31) == b.TIGA_EUNSUPPORTED
+    assert call(n=1 << 30, heads=1 << 10) == b.TIGA_EUNSUPPORTED
+    assert call(n=-1) == b.TIGA_EINVAL
+    assert call(dt=7) == b.TIGA_EINVAL
+    assert call(rel=5) == b.TIGA_EINVAL
+    assert call(scale=0.0) == b.TIGA_EINVAL
+    assert call(scale=-1.0) == b.TIGA_EINVAL
+    assert call(scale=float("inf")) == b.TIGA_EINVAL
+    assert call(scale=float("nan")) == b.TIGA_EINVAL
+    assert call(v=None) == b.TIGA_EINVAL
+    assert call(y=odd) == b.TIGA_EINVAL
+    assert call(k=odd) == b.TIGA_EINVAL
+    assert b"16-byte" in clib.tiga_last_error()
+    # empty problems are valid no-ops
+    assert call(n=0, q=None, k=None, v=None, y=None) == b.TIGA_OK
+    assert call(heads=0, q=None, k=None, v=None, y=None) == b.TIGA_OK
