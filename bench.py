@@ -47,9 +47,10 @@ def parse():
     p.add_argument("--no-ceilings", action="store_true", help="skip the hardware-ceiling probe")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--check-rows", type=int, default=400)
-    p.add_argument("--profile-pass", nargs="?", const="csr", choices=["csr", "radius", "dense"],
+    p.add_argument("--profile-pass", nargs="?", const="csr", choices=["csr", "radius", "dense", "attention"],
                    help="for rocprofv3 counter runs: csr = a 4 GiB plain copy (calibration) then 3 headline steps; "
-                        "radius / dense = 3 forward calls on the radius (1M points) / dense (65536 points) workload")
+                        "radius / dense / attention = 3 forward calls on the radius (1M points) / dense (65536 points) / "
+                        "attention (16 heads x 16384 tokens x 128, binary16, triangular) workload")
     p.add_argument("--paths-only", action="store_true", help="only the per-path figures (for kernel traces)")
     p.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                    help="print the markdown summary of three rocprofv3 runs (kernel trace, FETCH_SIZE, WRITE_SIZE)")
@@ -63,6 +64,10 @@ def parse():
 PROFILE_MD = os.path.join(ROOT, "profiles", "gather_reduce_csr_powerlaw_1b_f16.md")
 VALU_LANE_OPS_PER_S = 256 * 4 * 16 * 2.4e9  # CUs * SIMDs * lanes per cycle * clock
 VALU_INSTR_PER_PAIR = 12
+MFMA16_PEAK_TFLOPS = 2500.0  # dense fp16 / bf16 MFMA peak
+# (tokens, heads, width, dtype, relation); the first is the profiled attention workload
+ATTENTION_CASES = [(16384, 16, 128, "f16", "triangular"), (16384, 16, 64, "f16", "triangular"),
+                   (16384, 16, 128, "bf16", "dense")]
 KERNEL_KEY = "gather_reduce_kernel"
 COPY_BYTES = 1 << 32
 
@@ -373,6 +378,23 @@ def paths(args, torch, tb, synth):
                                   tflops_20_per_pair=tf, frac_valu=tf / VALU_PEAK_TFLOPS,
                                   valu_issue_floor_ms=floor_ms)
     log(f"dense: {rr['step_ms']:.3f} ms ({tf:.1f} TFLOP/s)")
+    del pd, qd
+
+    # online-softmax reducer over the implicit triangular / dense relation (streaming attention forward):
+    # 4 * width flops per admitted (query, key) pair (two products of 2 * width), against the dense
+    # 16-bit MFMA peak
+    for (nt, H, D, dt, rel) in ATTENTION_CASES:
+        inp = synth.attention_inputs(nt, H, D, dt)
+        tdt = torch.float16 if dt == "f16" else torch.bfloat16
+        q, kk, v = (dev(inp[a].view(np.int16)).view(tdt) for a in ("q", "k", "v"))
+        rr = time_steps(torch, tb, lambda: tb.tiga_mp_attention_fwd(q, kk, v, None, rel), steps, warm)
+        k = float(np.mean(rr["kernel_ms"]))
+        pairs = nt * (nt + 1) // 2 if rel == "triangular" else nt * nt
+        tf = 4 * D * H * pairs / (k * 1e-3) / 1e12
+        name = f"attention_{rel}_{nt}_h{H}_d{D}_{dt}"
+        res[name] = dict(ms=rr["step_ms"], kernel_ms=k, pairs=pairs * H, tflops=tf, frac_mfma=tf / MFMA16_PEAK_TFLOPS)
+        log(f"{name}: {k:.3f} ms ({tf:.1f} TFLOP/s)")
+        del q, kk, v
     return res
 
 
@@ -385,6 +407,15 @@ def profile_pass(args, torch, tb, synth):
         pd, xd = dev(g["pos"]), dev(g["x"])
         for _ in range(3):
             tb.tiga_mp_radius_fwd(pd, xd, g["radius"], g["sigma"])
+        torch.cuda.synchronize()
+        log("profile pass done")
+        return
+    if args.profile_pass == "attention":
+        nt, H, D, dt, rel = ATTENTION_CASES[0]
+        inp = synth.attention_inputs(nt, H, D, dt)
+        q, kk, v = (dev(inp[a].view(np.int16)).view(torch.float16) for a in ("q", "k", "v"))
+        for _ in range(3):
+            tb.tiga_mp_attention_fwd(q, kk, v, None, rel)
         torch.cuda.synchronize()
         log("profile pass done")
         return

@@ -81,6 +81,7 @@ struct Geo {
     static constexpr int RPT = kBN * D / 8 / kThreads;   // 16-byte K chunks per thread per tile
     static constexpr int CPR = D / 8;                    // 16-byte chunks per row
     static constexpr int KPT = kBN / (kThreads / CPR);   // V keys per thread per tile
+    static constexpr int NKG = kBN / KPT;                // V key groups per tile
     static_assert(RPT >= 1 && KPT >= 1 && (KPT == 2 || KPT == 4), "tile shape");
     static constexpr int LDS_K = kBN * KS;               // per buffer, 16-bit units
     static constexpr int LDS_V = D * VS;
@@ -98,21 +99,22 @@ __device__ __forceinline__ void stage_load(u4 (&kr)[Geo<D>::RPT], u4 (&vr)[Geo<D
                                            const u4 *__restrict__ kh, const u4 *__restrict__ vh, int64_t k0,
                                            int64_t n, int tid) {
     using G = Geo<D>;
-    const u4 z = u4{0u, 0u, 0u, 0u};
+    // Keys past n read the last row instead: their scores are masked to -inf, so their weights
+    // are exactly 0 and the (finite) row contributes nothing.
+    const int last = static_cast<int>(n - 1 - k0);     // tile-relative index of key n-1
 #pragma unroll
     for (int r = 0; r < G::RPT; ++r) {
         const int idx = tid + r * kThreads;
-        const int64_t key = k0 + idx / G::CPR;
-        // keys past n become zero rows (the load itself reads the last valid row)
-        const u4 t = kh[(key < n ? key : n - 1) * G::CPR + idx % G::CPR];
-        kr[r] = key < n ? t : z;
+        const int key = idx / G::CPR < last ? idx / G::CPR : last;
+        kr[r] = kh[(k0 + key) * G::CPR + idx % G::CPR];
     }
-    const int dg = tid % G::CPR, kg = tid / G::CPR;
+    // consecutive threads take consecutive key groups, so that one transposed row of the LDS
+    // store is written by neighbouring lanes (contiguous, no bank conflicts)
+    const int kg = tid % G::NKG, dg = tid / G::NKG;
 #pragma unroll
     for (int r = 0; r < G::KPT; ++r) {
-        const int64_t key = k0 + kg * G::KPT + r;
-        const u4 t = vh[(key < n ? key : n - 1) * G::CPR + dg];
-        vr[r] = key < n ? t : z;
+        const int key = kg * G::KPT + r < last ? kg * G::KPT + r : last;
+        vr[r] = vh[(k0 + key) * G::CPR + dg];
     }
 }
 
@@ -125,7 +127,7 @@ __device__ __forceinline__ void stage_store(const u4 (&kr)[Geo<D>::RPT], const u
         const int idx = tid + r * kThreads;
         *reinterpret_cast<u4 *>(ks + (idx / G::CPR) * G::KS + (idx % G::CPR) * 8) = kr[r];
     }
-    const int dg = tid % G::CPR, kg = tid / G::CPR;
+    const int kg = tid % G::NKG, dg = tid / G::NKG;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         uint16_t *dst = vt + (dg * 8 + j) * G::VS + kg * G::KPT;
@@ -152,7 +154,7 @@ __device__ __forceinline__ void task_of(int ntq, bool causal, int &head, int &qt
 }
 
 template <class T, int D, bool CAUSAL>
-__global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const u4 *__restrict__ q, const u4 *__restrict__ k,
+__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restrict__ q, const u4 *__restrict__ k,
                                                             const u4 *__restrict__ v, int64_t n, int ntq,
                                                             float c, uint16_t *__restrict__ y, float *__restrict__ lse) {
     using G = Geo<D>;
@@ -223,16 +225,19 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const u4 *__restrict
             // ---- relation: keys past n, and (triangular) keys after the query
             const bool edge = k0 + kBN > n || (CAUSAL && k0 + kBN - 1 > qw0);
             if (edge) {
+                // in tile-relative 32-bit units: key kb*16 + 4g + i is admissible iff it is below
+                // nk = n - k0 and (triangular) not after the query at offset qw0 - k0 + 16 qb + col
+                const int nk = static_cast<int>(n - k0 < kBN ? n - k0 : kBN);
+                const int qr = static_cast<int>(CAUSAL ? qw0 - k0 : 0) + col;
 #pragma unroll
                 for (int qb = 0; qb < 2; ++qb) {
-                    const int64_t qi = qw0 + qb * 16 + col;
+                    const int lim = CAUSAL ? (qr + qb * 16 + 1 < nk ? qr + qb * 16 + 1 : nk) : nk;
 #pragma unroll
                     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
-                            const int64_t kj = k0 + kb * 16 + g * 4 + i;
-                            const bool ok = kj < n && (!CAUSAL || kj <= qi);
-                            s[kb][qb][i] = ok ? s[kb][qb][i] : -__builtin_inff();
+                            const int kj = kb * 16 + g * 4 + i;
+                            s[kb][qb][i] = kj < lim ? s[kb][qb][i] : -__builtin_inff();
                         }
                 }
             }
