@@ -254,7 +254,10 @@ enum tiga_relation {
  *   y:       [heads, n, width] of dtype, overwritten (rounded to nearest even).
  *   lse:     fp32 [heads, n] or NULL.
  * Scores, weights and sums are fp32 (products of the 16-bit inputs are exact);
- * the normalized weights enter the value product rounded to dtype.  Every row
+ * the weights enter both the value product and the mass rounded to dtype, so
+ * y is an exactly normalized combination of the values and lse carries up to
+ * one unit roundoff of dtype (2^-11 binary16, 2^-8 bfloat16) of absolute
+ * error from that rounding.  Every row
  * is nonempty under both relations.  Requires width 64 or 128
  * (TIGA_EUNSUPPORTED otherwise), n < 2^31, heads * n < 2^40, scale finite and
  * > 0.  n == 0 or heads == 0 enqueues nothing.  Needs no workspace.

@@ -21,6 +21,9 @@
 //    8g + j are therefore bound to keys {4g + j} (j < 4) of the first and {16 + 4g + j - 4} (j >= 4)
 //    of the second 16-key block, and the V^T operand reads its keys in the same order; a
 //    contraction does not depend on the order of its terms.
+//  - The mass l is summed by the matrix core too: an all-ones A operand against the weights'
+//    B operand gives, in every row, the sum over the chunk's keys for each query, from the same
+//    rounded weights as the numerator (so y is an exactly normalized combination of the values).
 //  - Scores are kept in the log2 domain (scale * log2 e folded into one multiply-add), and the
 //    accumulator is rescaled only when a tile raises some query's maximum by more than 8 (a
 //    factor 256): any reference point m gives the same y = sum 2^(t - m) v / sum 2^(t - m), and
@@ -62,6 +65,7 @@ struct F16 {
     static __device__ __forceinline__ uint32_t pack(float a, float b) {
         return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2{a, b}), h2));
     }
+    static __device__ __forceinline__ u4 ones() { return u4{0x3c003c00u, 0x3c003c00u, 0x3c003c00u, 0x3c003c00u}; }
 };
 struct BF16 {
     static __device__ __forceinline__ f4 mma(u4 a, u4 b, f4 c) {
@@ -70,12 +74,13 @@ struct BF16 {
     static __device__ __forceinline__ uint32_t pack(float a, float b) {
         return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2{a, b}), b2));
     }
+    static __device__ __forceinline__ u4 ones() { return u4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u}; }
 };
 
 template <int D>
 struct Geo {
     static constexpr int KS = D + 8;                     // K row stride in LDS (16-bit units)
-    static constexpr int VS = kBN + 8;                   // V^T row stride in LDS
+    static constexpr int VS = kBN + 4;                   // V^T row stride in LDS
     static constexpr int CH = D / 32;                    // 32-deep chunks of the score product
     static constexpr int DB = D / 16;                    // 16-wide blocks of the output
     static constexpr int RPT = kBN * D / 8 / kThreads;   // 16-byte K chunks per thread per tile
@@ -99,22 +104,32 @@ __device__ __forceinline__ void stage_load(u4 (&kr)[Geo<D>::RPT], u4 (&vr)[Geo<D
                                            const u4 *__restrict__ kh, const u4 *__restrict__ vh, int64_t k0,
                                            int64_t n, int tid) {
     using G = Geo<D>;
-    // Keys past n read the last row instead: their scores are masked to -inf, so their weights
-    // are exactly 0 and the (finite) row contributes nothing.
-    const int last = static_cast<int>(n - 1 - k0);     // tile-relative index of key n-1
-#pragma unroll
-    for (int r = 0; r < G::RPT; ++r) {
-        const int idx = tid + r * kThreads;
-        const int key = idx / G::CPR < last ? idx / G::CPR : last;
-        kr[r] = kh[(k0 + key) * G::CPR + idx % G::CPR];
-    }
-    // consecutive threads take consecutive key groups, so that one transposed row of the LDS
+    // one uniform tile base and per-thread 32-bit offsets
+    const u4 *kt = kh + k0 * G::CPR;
+    const u4 *vtl = vh + k0 * G::CPR;
+    // consecutive threads take consecutive V key groups, so that one transposed row of the LDS
     // store is written by neighbouring lanes (contiguous, no bank conflicts)
     const int kg = tid % G::NKG, dg = tid / G::NKG;
+    if (k0 + kBN <= n) {
 #pragma unroll
-    for (int r = 0; r < G::KPT; ++r) {
-        const int key = kg * G::KPT + r < last ? kg * G::KPT + r : last;
-        vr[r] = vh[(k0 + key) * G::CPR + dg];
+        for (int r = 0; r < G::RPT; ++r) kr[r] = kt[tid + r * kThreads];
+#pragma unroll
+        for (int r = 0; r < G::KPT; ++r) vr[r] = vtl[(kg * G::KPT + r) * G::CPR + dg];
+    } else {
+        // keys past n read the last row instead: their scores are masked to -inf, so their
+        // weights are exactly 0 and the (finite) row contributes nothing
+        const int last = static_cast<int>(n - 1 - k0);     // tile-relative index of key n-1
+#pragma unroll
+        for (int r = 0; r < G::RPT; ++r) {
+            const int idx = tid + r * kThreads;
+            const int key = idx / G::CPR < last ? idx / G::CPR : last;
+            kr[r] = kt[key * G::CPR + idx % G::CPR];
+        }
+#pragma unroll
+        for (int r = 0; r < G::KPT; ++r) {
+            const int key = kg * G::KPT + r < last ? kg * G::KPT + r : last;
+            vr[r] = vtl[key * G::CPR + dg];
+        }
     }
 }
 
@@ -188,7 +203,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restr
     for (int db = 0; db < G::DB; ++db)
         for (int qb = 0; qb < 2; ++qb) o[db][qb] = f4{0.0f, 0.0f, 0.0f, 0.0f};
     float m[2] = {-__builtin_inff(), -__builtin_inff()};
-    float l[2] = {0.0f, 0.0f};
+    // mass: an all-ones A operand sums P^T over the keys of a chunk for every query column, so
+    // the denominator uses the same rounded weights as the numerator
+    f4 l[2] = {f4{0.0f, 0.0f, 0.0f, 0.0f}, f4{0.0f, 0.0f, 0.0f, 0.0f}};
+    const u4 ones = T::ones();
 
     const int64_t kend = CAUSAL ? (q0 + kBM < n ? q0 + kBM : n) : n;  // keys this block needs
     const int ntk = static_cast<int>((kend + kBN - 1) / kBN);
@@ -267,7 +285,6 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restr
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         p[kb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][qb][i], c, -m[qb]));
-                        l[qb] += p[kb][i];
                     }
 #pragma unroll
                 for (int kc = 0; kc < 2; ++kc) {
@@ -290,6 +307,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restr
                     for (int qb = 0; qb < 2; ++qb) o[db][qb] = T::mma(a, pb[kc][qb], o[db][qb]);
                 }
             }
+#pragma unroll
+            for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb) l[qb] = T::mma(ones, pb[kc][qb], l[qb]);
         }
         stage_store<D>(kr, vr, lds + (buf ^ 1) * G::LDS_K, lds + 2 * G::LDS_K + (buf ^ 1) * G::LDS_V, tid);
         __syncthreads();
@@ -298,9 +319,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restr
     // ---- finalize: total mass over the four lanes of a query, divide, store
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-        float lt = l[qb];
-        lt += __shfl_xor(lt, 16, kWave);
-        lt += __shfl_xor(lt, 32, kWave);
+        const float lt = l[qb][0];          // every row of the mass block holds the full sum
         const float inv = 1.0f / lt;
         const int64_t qi = qw0 + qb * 16 + col;
         if (qi < n) {
