@@ -54,6 +54,7 @@ def _load():
                 "tiga_oracle_radius_bwd": (C.c_int, [i64, i32, vp, vp, vp, f32, f32, i64, vp, vp, vp, vp, vp]),
                 "tiga_oracle_radius_neighbors": (C.c_int, [i64, vp, f32, i64, vp, vp, vp, vp]),
                 "tiga_oracle_dense_fwd": (None, [i64, vp, vp, f32, i64, vp, vp, vp]),
+                "tiga_oracle_knn": (C.c_int, [i64, i32, vp, vp, i32, i64, vp, vp, vp, vp]),
                 "tiga_oracle_f16_to_double": (C.c_double, [C.c_uint16]),
                 "tiga_oracle_bf16_to_double": (C.c_double, [C.c_uint16]),
                 "tiga_oracle_attention_fwd": (C.c_int, [i64, i32, i32, C.c_int, vp, vp, vp, C.c_double,
@@ -224,3 +225,18 @@ def attention_fwd(q, k, v, scale, dtype="f16", relation="triangular", pts=None):
     if rc != 0:
         raise ValueError("oracle attention: unknown dtype or relation")
     return y, ya, lse
+
+
+def knn(pos, x, k, pts=None):
+    """Exact kNN (self excluded, key (d2, index)); returns (nbr int32 [npts, k], y fp64 [npts, F], yabs)."""
+    pos = _c(pos, np.float32).reshape(-1, 3)
+    n = pos.shape[0]
+    x = None if x is None else _c(x, np.float32).reshape(n, -1)
+    F = 0 if x is None else x.shape[1]
+    pts, npts = _rows(pts, n)
+    nbr = np.empty((npts, k), np.int32)
+    y = np.empty((npts, F), np.float64)
+    ya = np.empty((npts, F), np.float64)
+    if _load().tiga_oracle_knn(n, F, _p(pos), _p(x), int(k), npts, _p(pts), _p(nbr), _p(y), _p(ya)):
+        raise MemoryError("oracle kNN: allocation failed")
+    return nbr, y, ya

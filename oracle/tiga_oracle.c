@@ -624,3 +624,77 @@ int tiga_oracle_attention_fwd(int64_t n, int32_t H, int32_t D, int dtype, const 
     }
     return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Generated exact kNN relation (Section 4.9, generated relations; the      */
+/* exact-kNN workload of Section 7)                                         */
+/* ------------------------------------------------------------------------ */
+
+/* Squared distance in fp32 from direct differences, no contraction:
+ *   d2 = fl(fl(fl(dx*dx) + fl(dy*dy)) + fl(dz*dz)),  dx = fl(p_j.x - p_i.x), ... */
+static float knn_d2(const float *pi, const float *pj) {
+    float dx = pj[0] - pi[0], dy = pj[1] - pi[1], dz = pj[2] - pi[2];
+    float sx = dx * dx, sy = dy * dy, sz = dz * dz;
+    float s = sx + sy;
+    return s + sz;
+}
+
+/* Exact k nearest neighbours over one point set, self excluded.  Source j is
+ * ranked by the key (d2_ij, j) in lexicographic order (a distance tie keeps the
+ * lower index); a key with a non-finite d2 is never selected.  S_i holds the k
+ * smallest keys (fewer if fewer sources have a finite d2).  For each requested
+ * query pts[k'] (all points if pts == NULL):
+ *   nbr [k'][t] = the t-th selected source in key order, -1 past |S_i|  (may be NULL)
+ *   y   [k'][f] = sum_{j in S_i} x[j][f]       (fp64; x == NULL or F == 0 skips y)
+ *   yabs[k'][f] = sum_{j in S_i} |x[j][f]|     (may be NULL)
+ * Returns 0, or -1 if a scratch allocation fails. */
+int tiga_oracle_knn(int64_t n, int32_t F, const float *pos, const float *x, int32_t k, int64_t npts,
+                    const int64_t *pts, int32_t *nbr, double *y, double *yabs) {
+    int fail = 0;
+    int64_t q;
+#pragma omp parallel for schedule(dynamic, 16) reduction(| : fail)
+    for (q = 0; q < npts; ++q) {
+        int64_t i = pts ? pts[q] : q;
+        float *bd = (float *)malloc(sizeof(float) * (size_t)(k > 0 ? k : 1));
+        int64_t *bj = (int64_t *)malloc(sizeof(int64_t) * (size_t)(k > 0 ? k : 1));
+        if (!bd || !bj) {
+            free(bd);
+            free(bj);
+            fail = 1;
+            continue;
+        }
+        int cnt = 0;
+        for (int64_t j = 0; j < n && k > 0; ++j) {
+            if (j == i) continue;
+            float d2 = knn_d2(pos + i * 3, pos + j * 3);
+            if (!isfinite(d2)) continue;
+            /* j grows, so among equal distances the retained (lower) index stays first:
+             * the new key goes after every retained key with d2 <= its own */
+            if (cnt == k && !(d2 < bd[k - 1])) continue;
+            int at = cnt < k ? cnt : k - 1;
+            while (at > 0 && d2 < bd[at - 1]) {
+                bd[at] = bd[at - 1];
+                bj[at] = bj[at - 1];
+                --at;
+            }
+            bd[at] = d2;
+            bj[at] = j;
+            if (cnt < k) ++cnt;
+        }
+        if (nbr)
+            for (int t = 0; t < k; ++t) nbr[q * k + t] = t < cnt ? (int32_t)bj[t] : -1;
+        if (y && x)
+            for (int f = 0; f < F; ++f) {
+                double acc = 0.0, mag = 0.0;
+                for (int t = 0; t < cnt; ++t) {
+                    acc += (double)x[bj[t] * F + f];
+                    mag += fabs((double)x[bj[t] * F + f]);
+                }
+                y[q * F + f] = acc;
+                if (yabs) yabs[q * F + f] = mag;
+            }
+        free(bd);
+        free(bj);
+    }
+    return fail ? -1 : 0;
+}

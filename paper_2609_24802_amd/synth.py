@@ -244,3 +244,11 @@ def attention_inputs(n: int, heads: int, width: int, dtype: str = "f16", cfg: in
     out["scale"] = np.float32(width ** -0.5)
     out["dtype"] = dtype
     return out
+
+
+def knn_inputs(n: int, feat: int = 1, cfg: int = 7):
+    """Points uniform in [0, 1)^3 and N(0, 1) features [n, feat]: the exact-kNN workload of the
+    evaluation (a scalar neighbour sum, k = 16, 1,024 to 131,072 points)."""
+    pos = uniform_f32(n * 3, 0.0, 1.0, (cfg, 0, n)).reshape(n, 3)
+    x = normal_f32(n * feat, (cfg, 1, n, feat)).reshape(n, feat)
+    return dict(pos=pos, x=x, k=16)
