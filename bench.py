@@ -47,10 +47,11 @@ def parse():
     p.add_argument("--no-ceilings", action="store_true", help="skip the hardware-ceiling probe")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--check-rows", type=int, default=400)
-    p.add_argument("--profile-pass", nargs="?", const="csr", choices=["csr", "radius", "dense", "attention"],
+    p.add_argument("--profile-pass", nargs="?", const="csr", choices=["csr", "radius", "dense", "attention", "knn"],
                    help="for rocprofv3 counter runs: csr = a 4 GiB plain copy (calibration) then 3 headline steps; "
                         "radius / dense / attention = 3 forward calls on the radius (1M points) / dense (65536 points) / "
-                        "attention (16 heads x 16384 tokens x 128, binary16, triangular) workload")
+                        "attention (16 heads x 16384 tokens x 128, binary16, triangular) workload; knn = 3 calls on "
+                        "131072 uniform points, k = 16")
     p.add_argument("--paths-only", action="store_true", help="only the per-path figures (for kernel traces)")
     p.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                    help="print the markdown summary of three rocprofv3 runs (kernel trace, FETCH_SIZE, WRITE_SIZE)")
@@ -65,6 +66,8 @@ PROFILE_MD = os.path.join(ROOT, "profiles", "gather_reduce_csr_powerlaw_1b_f16.m
 VALU_LANE_OPS_PER_S = 256 * 4 * 16 * 2.4e9  # CUs * SIMDs * lanes per cycle * clock
 VALU_INSTR_PER_PAIR = 12
 MFMA16_PEAK_TFLOPS = 2500.0  # dense fp16 / bf16 MFMA peak
+# exact kNN workload sizes (the largest is profiled)
+KNN_SIZES = [1024, 16384, 131072]
 # (tokens, heads, width, dtype, relation); the first is the profiled attention workload
 ATTENTION_CASES = [(16384, 16, 128, "f16", "triangular"), (16384, 16, 64, "f16", "triangular"),
                    (16384, 16, 128, "bf16", "dense")]
@@ -380,6 +383,19 @@ def paths(args, torch, tb, synth):
     log(f"dense: {rr['step_ms']:.3f} ms ({tf:.1f} TFLOP/s)")
     del pd, qd
 
+    # exact kNN relation with the neighbour sum (k = 16, scalar features): the build (curve order, tile
+    # boxes) plus the select-and-sum kernel; pairs = n (n - 1) ordered pairs the relation decides over
+    for nk in KNN_SIZES:
+        g = synth.knn_inputs(nk)
+        pd, xd = dev(g["pos"]), dev(g["x"])
+        ws = tb._workspace(tb.load().tiga_mp_knn_workspace(nk), pd.device)
+        rr = time_steps(torch, tb, lambda: tb.tiga_mp_knn_fwd(pd, xd, g["k"], ws=ws), steps, warm)
+        k = float(np.mean(rr["kernel_ms"]))
+        res[f"knn_{nk}_k16_f1"] = dict(ms=rr["step_ms"], select_kernel_ms=k,
+                                        gpairs_per_s=nk * (nk - 1) / rr["step_ms"] / 1e6)
+        log(f"knn {nk}: {rr['step_ms']:.3f} ms (select {k:.3f} ms)")
+        del pd, xd, ws
+
     # online-softmax reducer over the implicit triangular / dense relation (streaming attention forward):
     # 4 * width flops per admitted (query, key) pair (two products of 2 * width), against the dense
     # 16-bit MFMA peak
@@ -407,6 +423,14 @@ def profile_pass(args, torch, tb, synth):
         pd, xd = dev(g["pos"]), dev(g["x"])
         for _ in range(3):
             tb.tiga_mp_radius_fwd(pd, xd, g["radius"], g["sigma"])
+        torch.cuda.synchronize()
+        log("profile pass done")
+        return
+    if args.profile_pass == "knn":
+        g = synth.knn_inputs(KNN_SIZES[-1])
+        pd, xd = dev(g["pos"]), dev(g["x"])
+        for _ in range(3):
+            tb.tiga_mp_knn_fwd(pd, xd, g["k"])
         torch.cuda.synchronize()
         log("profile pass done")
         return

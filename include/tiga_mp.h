@@ -228,6 +228,32 @@ size_t tiga_mp_dense_workspace(int64_t n);
 int tiga_mp_dense_fwd(int64_t n, const float *pos, const float *q, float eps, int reducer,
                       float *y, void *ws, size_t ws_bytes, void *stream);
 
+/* ----------------------------------------------- generated exact kNN relation */
+
+/* Workspace bytes for tiga_mp_knn_fwd on n points (0 on error). */
+size_t tiga_mp_knn_workspace(int64_t n);
+
+/* Forward over the exact k-nearest-neighbour relation generated from positions
+ * (Section 4.9, generated relations: candidate tiles are scanned for each query
+ * with a padded top-k state keyed by squared distance and source index; no
+ * adjacency is stored), with the neighbour-sum message of the exact-kNN
+ * workload of Section 7:
+ *   S_i  = the k sources j != i with the smallest keys (d2_ij, j), compared
+ *          lexicographically (a distance tie keeps the lower index); a source
+ *          whose d2 is not finite is never selected, so S_i may hold fewer
+ *          than k sources;
+ *   d2   = fl(fl(fl(dx*dx) + fl(dy*dy)) + fl(dz*dz)), dx = fl(p_j.x - p_i.x), ...
+ *   y_i  = sum_{j in S_i} x_j      (fp32 sum in key order)
+ *   nbr[i][t] = the t-th selected source in key order, -1 past |S_i|.
+ * The relation is rebuilt on every call (stateless).
+ *   pos: fp32 [n, 3]; x: fp32 [n, feat] (NULL if feat == 0); y: fp32 [n, feat]
+ *   (NULL if feat == 0); nbr: int32 [n, k] or NULL.  reducer must be
+ *   TIGA_REDUCE_SUM.  Requires 0 <= k <= 32 (TIGA_EUNSUPPORTED above 32) and
+ *   n < 2^31 - 64.  Selection is exact: it equals a full scan of all pairs.
+ * Errors: TIGA_EINVAL, TIGA_EUNSUPPORTED, TIGA_EWORKSPACE, TIGA_EDEVICE. */
+int tiga_mp_knn_fwd(int64_t n, int32_t feat, const float *pos, const float *x, int32_t k, int reducer, float *y,
+                    int32_t *nbr, void *ws, size_t ws_bytes, void *stream);
+
 /* ------------------------------- online-softmax reducer (streaming attention) */
 
 /* 16-bit input types of the attention path. */

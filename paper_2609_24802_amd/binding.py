@@ -69,6 +69,9 @@ _SIGS = {
     "tiga_mp_dense_workspace": (C.c_size_t, [C.c_int64]),
     "tiga_mp_dense_fwd": (C.c_int, [C.c_int64, C.c_void_p, C.c_void_p, C.c_float, C.c_int, C.c_void_p,
                                     C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tiga_mp_knn_workspace": (C.c_size_t, [C.c_int64]),
+    "tiga_mp_knn_fwd": (C.c_int, [C.c_int64, C.c_int32, C.c_void_p, C.c_void_p, C.c_int32, C.c_int, C.c_void_p,
+                                  C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
     "tiga_mp_attention_fwd": (C.c_int, [C.c_int64, C.c_int32, C.c_int32, C.c_int, C.c_void_p, C.c_void_p,
                                         C.c_void_p, C.c_float, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p]),
     "tiga_mp_set_kernel_events": (C.c_int, [C.c_void_p, C.c_void_p]),
@@ -286,6 +289,29 @@ def tiga_mp_dense_fwd(pos: torch.Tensor, q: torch.Tensor, eps: float, y=None, ws
     _check(lib.tiga_mp_dense_fwd(n, _ptr(pos), _ptr(q), float(eps), REDUCE_SUM, _ptr(y), _ptr(ws), ws.numel(),
                                  _stream()))
     return y
+
+
+def tiga_mp_knn_fwd(pos: torch.Tensor, x: torch.Tensor | None, k: int, want_nbr: bool = False, ws=None):
+    """Exact kNN relation (self excluded, key (fp32 d2, index)) with the neighbour sum y_i = sum x_j.
+
+    pos fp32 [n, 3]; x fp32 [n, F] or None.  Returns y fp32 [n, F] (None without x), and the selected
+    indices int32 [n, k] in key order when want_nbr."""
+    lib = load()
+    n = pos.shape[0]
+    _dev(pos, torch.float32, "pos", (n, 3))
+    F = 0
+    if x is not None:
+        _dev(x, torch.float32, "x")
+        if x.dim() != 2 or x.shape[0] != n:
+            raise ValueError(f"x must be [n, F] with n = {n}")
+        F = x.shape[1]
+    y = torch.empty(n, F, dtype=torch.float32, device=pos.device) if x is not None else None
+    nbr = torch.empty(n, k, dtype=torch.int32, device=pos.device) if want_nbr else None
+    if ws is None:
+        ws = _workspace(lib.tiga_mp_knn_workspace(n), pos.device)
+    _check(lib.tiga_mp_knn_fwd(n, F, _ptr(pos), _ptr(x) if F else None, int(k), REDUCE_SUM, _ptr(y) if F else None,
+                               _ptr(nbr), _ptr(ws), ws.numel(), _stream()))
+    return (y, nbr) if want_nbr else y
 
 
 def _head_major(t, name, layout, shape=None):

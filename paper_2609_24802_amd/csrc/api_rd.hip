@@ -1,5 +1,6 @@
 // C ABI of the generated radius relation and the dense all-pairs relation.
 #include "dense.hpp"
+#include "knn.hpp"
 #include "radius.hpp"
 
 using namespace tiga;
@@ -94,6 +95,26 @@ int tiga_mp_dense_fwd(int64_t n, const float *pos, const float *q, float eps, in
     if (!q || !y) return fail(TIGA_EINVAL, "q and y are required");
     if (int rc = check_ws(ws, ws_bytes, dense::workspace_bytes(n))) return rc;
     return dense::forward(n, pos, q, eps, y, ws, static_cast<hipStream_t>(stream));
+}
+
+size_t tiga_mp_knn_workspace(int64_t n) {
+    if (n < 0) return 0;
+    return knn::workspace_bytes(n);
+}
+
+int tiga_mp_knn_fwd(int64_t n, int32_t feat, const float *pos, const float *x, int32_t k, int reducer, float *y,
+                    int32_t *nbr, void *ws, size_t ws_bytes, void *stream) {
+    EntryScope scope;
+    if (int rc = check_points(n, pos)) return rc;
+    if (reducer == TIGA_REDUCE_MAX) return fail(TIGA_EUNSUPPORTED, "the kNN relation supports the sum reducer only");
+    if (reducer != TIGA_REDUCE_SUM) return fail(TIGA_EINVAL, "unknown reducer %d", reducer);
+    if (k < 0) return fail(TIGA_EINVAL, "k must be >= 0 (got %d)", k);
+    if (k > knn::kMaxK) return fail(TIGA_EUNSUPPORTED, "k = %d exceeds the supported %d", k, knn::kMaxK);
+    if (feat < 0) return fail(TIGA_EINVAL, "feat must be >= 0");
+    if (n == 0) return TIGA_OK;
+    if (feat > 0 && (!x || !y)) return fail(TIGA_EINVAL, "x and y are required when feat > 0");
+    if (int rc = check_ws(ws, ws_bytes, knn::workspace_bytes(n))) return rc;
+    return knn::forward(n, feat, pos, x, k, y, nbr, ws, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

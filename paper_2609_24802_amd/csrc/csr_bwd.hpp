@@ -31,7 +31,8 @@ int launch_validate(const tiga_csr *rel, hipStream_t stream);
 
 // Stable sort of n keys in [0, key_limit): sorted keys to keys_out, the input
 // position of each to idx_out (ascending within equal keys), and
-// ptr[j] = first sorted position with key >= j for j in [0, key_limit].
+// ptr[j] = first sorted position with key >= j for j in [0, key_limit] (ptr may be null:
+// then only the sort runs).
 size_t sort_keys_ws_bytes(int64_t n);
 int launch_sort_keys(const int32_t *keys, int64_t n, int64_t key_limit, int32_t *keys_out, int32_t *idx_out,
                      int64_t *ptr, void *ws, hipStream_t stream);

@@ -332,6 +332,7 @@ int launch_sort_keys(const int32_t *keys, int64_t n, int64_t key_limit, int32_t 
     const int32_t *sorted = nullptr;
     if (n > 0)
         if (int rc = radix_sort(keys, nullptr, n, key_limit, keys_out, idx_out, nullptr, s, &sorted, stream)) return rc;
+    if (!ptr) return TIGA_OK;
     return ptr_from_sorted(n > 0 ? sorted : keys_out, n, key_limit, ptr, stream);
 }
 

@@ -153,3 +153,17 @@ def test_attention_errors(clib):
     # empty problems are valid no-ops
     assert call(n=0, q=None, k=None, v=None, y=None) == b.TIGA_OK
     assert call(heads=0, q=None, k=None, v=None, y=None) == b.TIGA_OK
+
+
+def test_knn_errors(clib):
+    from paper_2609_24802_amd import binding as b
+    fake = C.c_void_p(0x10000)
+    big = 1 << 40
+    assert clib.tiga_mp_knn_fwd(100, 1, fake, fake, 33, b.REDUCE_SUM, fake, None, fake, big, None) == b.TIGA_EUNSUPPORTED
+    assert clib.tiga_mp_knn_fwd(100, 1, fake, fake, -1, b.REDUCE_SUM, fake, None, fake, big, None) == b.TIGA_EINVAL
+    assert clib.tiga_mp_knn_fwd(100, 1, fake, fake, 16, b.REDUCE_MAX, fake, None, fake, big, None) == b.TIGA_EUNSUPPORTED
+    assert clib.tiga_mp_knn_fwd(100, 1, fake, None, 16, b.REDUCE_SUM, fake, None, fake, big, None) == b.TIGA_EINVAL
+    assert clib.tiga_mp_knn_fwd(100, 1, fake, fake, 16, b.REDUCE_SUM, fake, None, fake, 8, None) == b.TIGA_EWORKSPACE
+    assert clib.tiga_mp_knn_fwd(-1, 1, fake, fake, 16, b.REDUCE_SUM, fake, None, fake, big, None) == b.TIGA_EINVAL
+    assert clib.tiga_mp_knn_fwd(0, 1, None, None, 16, b.REDUCE_SUM, None, None, None, 0, None) == b.TIGA_OK
+    assert clib.tiga_mp_knn_workspace(1000) < clib.tiga_mp_knn_workspace(100000)

@@ -1,0 +1,102 @@
+"""GPU parity of the exact kNN relation against the oracle.
+
+Neighbour lists are bit-exact (both sides rank by the same fp32 squared distance and the source
+index); neighbour sums are within 1e-5 * sum|terms| (fp32 sums of at most 32 terms)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_24802_amd import synth
+from tests.parity import assert_terms_close
+
+pytestmark = pytest.mark.gpu
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def cloud(kind, n, seed):
+    rng = np.random.default_rng(seed)
+    if kind == "uniform":
+        return synth.uniform_f32(n * 3, 0.0, 1.0, (95, n, seed)).reshape(n, 3)
+    if kind == "line":        # integer points on a line: distance ties everywhere
+        p = np.zeros((n, 3), np.float32)
+        p[:, 0] = rng.permutation(n)
+        return p
+    if kind == "grid":        # binary-grid coordinates, many equal distances and duplicates
+        return synth.binary_grid_points(n, 3, (96, seed), span=6)
+    if kind == "cluster":     # a dense clump, coincident copies, a sparse background
+        p = rng.random((n, 3)).astype(np.float32)
+        p[: n // 3] = (0.3 + 0.002 * rng.random((n // 3, 3))).astype(np.float32)
+        p[n // 3: n // 3 + 12] = p[5]
+        return p
+    if kind == "flat":        # a plane
+        p = rng.random((n, 3)).astype(np.float32)
+        p[:, 2] = 0.5
+        return p
+    raise ValueError(kind)
+
+
+def check(lib, pos, F, k, pts=None, seed=0):
+    n = pos.shape[0]
+    x = synth.normal_f32(max(n * F, 1), (97, n, F, seed))[: n * F].reshape(n, F) if F else None
+    y, nbr = lib.tiga_mp_knn_fwd(dev(pos), dev(x) if F else None, k, want_nbr=True)
+    torch.cuda.synchronize()
+    nbr = nbr.cpu().numpy()
+    rnbr, ry, rya = oracle.knn(pos, x, k, pts=pts)
+    got = nbr if pts is None else nbr[pts]
+    if not np.array_equal(got, rnbr):
+        bad = np.argwhere((got != rnbr).any(1))[:, 0]
+        i = bad[0]
+        raise AssertionError(f"{len(bad)} rows differ; first {i}: got {got[i]} want {rnbr[i]}")
+    if F:
+        yy = y.cpu().numpy()
+        yy = yy if pts is None else yy[pts]
+        assert_terms_close(yy, ry, rya, what="kNN neighbour sum")
+
+
+@pytest.mark.parametrize("kind,n,k,F", [
+    ("uniform", 1, 0, 1), ("uniform", 2, 1, 1), ("uniform", 3, 4, 2), ("uniform", 17, 16, 1),
+    ("uniform", 64, 16, 3), ("uniform", 65, 8, 1), ("uniform", 200, 32, 1), ("uniform", 1000, 16, 16),
+    ("uniform", 4097, 17, 1), ("uniform", 3000, 1, 1), ("uniform", 2500, 2, 4), ("uniform", 2048, 5, 1),
+    ("line", 500, 16, 1), ("line", 129, 31, 2), ("grid", 3000, 32, 1), ("grid", 1500, 16, 3),
+    ("cluster", 2000, 16, 1), ("cluster", 777, 9, 8), ("flat", 1800, 16, 1)])
+def test_knn_against_oracle(lib, kind, n, k, F):
+    check(lib, cloud(kind, n, n + k), F, k, seed=k)
+
+
+def test_knn_all_rows_16k(lib):
+    """Every row of a 16,384-point cloud: the tile skipping must never drop a neighbour."""
+    g = synth.knn_inputs(16384)
+    check(lib, g["pos"], 1, 16)
+
+
+def test_knn_non_finite_points(lib):
+    pos = cloud("uniform", 700, 3).copy()
+    pos[10, 0] = np.nan
+    pos[20, 2] = np.inf
+    pos[30, 1] = -np.inf
+    check(lib, pos, 2, 16)
+
+
+def test_knn_more_neighbours_requested_than_exist(lib):
+    check(lib, cloud("uniform", 5, 4), 1, 8)
+    check(lib, cloud("uniform", 33, 4), 1, 32)
+
+
+def test_knn_without_features_and_repeatable(lib):
+    pos = cloud("cluster", 1200, 8)
+    _, a = lib.tiga_mp_knn_fwd(dev(pos), None, 16, want_nbr=True)
+    _, b = lib.tiga_mp_knn_fwd(dev(pos), None, 16, want_nbr=True)
+    assert torch.equal(a, b)
+    check(lib, pos, 0, 16)
+
+
+def test_knn_full_size_sampled(lib):
+    """The measured workload (131,072 uniform points, k = 16, scalar features) on sampled rows."""
+    g = synth.knn_inputs(131072)
+    rng = np.random.default_rng(2)
+    pts = np.unique(np.concatenate([[0, 1, 131071], rng.integers(0, 131072, 253)]))
+    check(lib, g["pos"], 1, 16, pts=pts)
