@@ -9,8 +9,8 @@
 // MI355X design:
 //  - Build: points are ordered along a 30-bit Morton curve (box of the finite coordinates, radix
 //    sort) into records (x, y, z, original index), cut into tiles of 64; each tile gets the box of
-//    its finite members.  A wavefront owns one tile of queries, so its 64 queries are compact in
-//    space.
+//    its finite members, and each group of 32 tiles a box too.  A block of 4 wavefronts owns one
+//    tile of queries, compact in space.
 //  - A key is one 64-bit integer, (bits of d2) << 32 | index: d2 >= 0, so the float bits order
 //    like the values, and one unsigned compare gives the lexicographic order with the index as the
 //    tie-break.  Keys of non-finite distances are >= the bits of +inf and never enter the state.
@@ -40,6 +40,7 @@ constexpr int kBits = 10;                                 // Morton bits per axi
 constexpr uint64_t kNone = 0x7f80000000000000ull;         // key (+inf, 0): above every finite key
 constexpr int kPartials = 1024;
 constexpr int kGroup = 32;                                // tiles per group (the coarse skip level)
+constexpr int kSplit = 4;                                 // wavefronts sharing one tile of queries
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
@@ -243,14 +244,39 @@ __device__ __forceinline__ float box_gap2(f4 p, f4 lo, f4 hi) {
 
 constexpr float kSkipMargin = 1.0f - 1e-6f;   // > 9 roundings of 2^-24
 
+// The KP smallest keys of two ascending states A (in place) and B: min(A[t], B[KP-1-t]) keeps
+// exactly them as a bitonic sequence, which log2(KP) half-cleaner stages sort.
 template <int KP>
-__global__ __launch_bounds__(kBlock) void select_kernel(const f4 *__restrict__ rec, const f4 *__restrict__ tlo,
-                                                        const f4 *__restrict__ thi, const f4 *__restrict__ glo,
-                                                        const f4 *__restrict__ ghi, int ntile, int k, int feat,
-                                                        const float *__restrict__ x, float *__restrict__ y,
-                                                        int32_t *__restrict__ nbr) {
-    const int qt = uniform(static_cast<int>(xcd_block()) * (kBlock / kWave) + static_cast<int>(threadIdx.x) / kWave);
-    if (qt >= ntile) return;   // a whole wavefront leaves
+__device__ __forceinline__ void merge_state(uint64_t (&a)[KP], const uint64_t (&b)[KP]) {
+#pragma unroll
+    for (int t = 0; t < KP; ++t) a[t] = b[KP - 1 - t] < a[t] ? b[KP - 1 - t] : a[t];
+#pragma unroll
+    for (int h = KP / 2; h >= 1; h /= 2)
+#pragma unroll
+        for (int t = 0; t < KP; ++t)
+            if ((t & h) == 0) {
+                const uint64_t lo = a[t + h] < a[t] ? a[t + h] : a[t];
+                const uint64_t hi = a[t + h] < a[t] ? a[t] : a[t + h];
+                a[t] = lo;
+                a[t + h] = hi;
+            }
+}
+
+// One block of kSplit wavefronts per query tile.  The candidate tiles, in visiting order, are
+// dealt round-robin to the wavefronts; each keeps its own padded state, publishes every lane's
+// KP-th distance in LDS (it only decreases, so a stale read is merely less tight), and rejects a
+// candidate only if it is strictly farther than the tightest published KP-th distance of its
+// lane, because then KP keys of the union already precede it.  Wavefront 0 merges the states.
+template <int KP>
+__global__ __launch_bounds__(kSplit * kWave) void select_kernel(const f4 *__restrict__ rec, const f4 *__restrict__ tlo,
+                                                                const f4 *__restrict__ thi, const f4 *__restrict__ glo,
+                                                                const f4 *__restrict__ ghi, int ntile, int k, int feat,
+                                                                const float *__restrict__ x, float *__restrict__ y,
+                                                                int32_t *__restrict__ nbr) {
+    __shared__ float shthr[kSplit][kWave];
+    __shared__ uint64_t shkey[kSplit - 1][KP][kWave];
+    const int qt = static_cast<int>(xcd_block());
+    const int w = uniform(static_cast<int>(threadIdx.x) / kWave);
     const int lane = lane_id();
     const f4 me = rec[static_cast<int64_t>(qt) * kTile + lane];
     const int qid = __float_as_int(me.w);
@@ -261,19 +287,33 @@ __global__ __launch_bounds__(kBlock) void select_kernel(const f4 *__restrict__ r
     // this lane's retained KP-th distance (+inf until its state is full; -inf for lanes without a
     // live query, which never need a candidate)
     float thr = live ? __builtin_inff() : -__builtin_inff();
+    shthr[w][lane] = thr;
+    __syncthreads();
+    float tight = thr;   // min over the wavefronts' published values
+    auto refresh = [&]() __attribute__((always_inline)) {
+        float v = thr;
+#pragma unroll
+        for (int o = 0; o < kSplit; ++o)
+            v = fminf(v, __hip_atomic_load(&shthr[o][lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
+        tight = v;
+    };
     // a box can be skipped when no lane could take anything from it
     auto needed = [&](f4 lo, f4 hi) __attribute__((always_inline)) {
-        return __any(box_gap2(me, lo, hi) * kSkipMargin <= thr);
+        return __any(box_gap2(me, lo, hi) * kSkipMargin <= tight);
     };
 
     // scan one candidate tile (after its box test, except for the query tile itself)
     auto scan = [&](int t) __attribute__((always_inline)) {
+        refresh();
         if (t != qt && !needed(tlo[t], thi[t])) return;
         const f4 *tr = rec + static_cast<int64_t>(t) * kTile;
+        // keys above every key of distance `tight` are out (ties in distance are kept)
+        const uint64_t cap = (static_cast<uint64_t>(__float_as_uint(tight)) << 32) | 0xffffffffull;
         bool changed = false;
         for (int c0 = 0; c0 < kTile; c0 += 8) {
             uint64_t nk[8];
             bool any = false;
+            const uint64_t lim = kd[KP - 1] < cap ? kd[KP - 1] : cap;
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
                 const f4 cj = tr[c0 + u];   // uniform address: a scalar load
@@ -281,7 +321,8 @@ __global__ __launch_bounds__(kBlock) void select_kernel(const f4 *__restrict__ r
                 const float d2 = sqdist(me, cj);
                 nk[u] = (static_cast<uint64_t>(__float_as_uint(d2)) << 32) | cid;
                 if (t == qt) nk[u] = static_cast<int>(cid) == qid ? ~0ull : nk[u];   // the query itself
-                any |= nk[u] < kd[KP - 1];
+                nk[u] = nk[u] < lim ? nk[u] : ~0ull;
+                any |= nk[u] != ~0ull;
             }
             if (__any(any)) {
                 changed = true;
@@ -290,28 +331,53 @@ __global__ __launch_bounds__(kBlock) void select_kernel(const f4 *__restrict__ r
                     if (nk[u] < kd[KP - 1]) insert<KP>(kd, nk[u]);
             }
         }
-        if (changed && live && kd[KP - 1] < kNone) thr = __uint_as_float(static_cast<uint32_t>(kd[KP - 1] >> 32));
+        if (changed && live && kd[KP - 1] < kNone) {
+            thr = __uint_as_float(static_cast<uint32_t>(kd[KP - 1] >> 32));
+            __hip_atomic_store(&shthr[w][lane], thr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
     };
 
-    // the query tile, then the rest of its group outward along the curve, then the other groups
-    // nearest-first, each behind its group box test
+    // visiting order: the query tile, then the rest of its group outward along the curve, then the
+    // other groups nearest-first, each behind its group box test; position p goes to wavefront
+    // p % kSplit (positions count every tile, skipped or not, so all wavefronts agree on them)
     const int ngroup = (ntile + kGroup - 1) / kGroup;
     const int qg = qt / kGroup;
     const int g0 = qg * kGroup, g1 = g0 + kGroup < ntile ? g0 + kGroup : ntile;
-    scan(qt);
+    int p = 0;
+    if (w == 0) scan(qt);
+    ++p;
     for (int step = 1; step < 2 * kGroup; ++step) {
         const int t = (step & 1) ? qt - (step + 1) / 2 : qt + step / 2;
-        if (t >= g0 && t < g1) scan(t);
+        if (t < g0 || t >= g1) continue;
+        if (p % kSplit == w) scan(t);
+        ++p;
     }
     for (int step = 1; step < 2 * ngroup; ++step) {
         const int g = (step & 1) ? qg - (step + 1) / 2 : qg + step / 2;
         if (g < 0 || g >= ngroup) continue;
+        const int t0 = g * kGroup, t1 = t0 + kGroup < ntile ? t0 + kGroup : ntile;
+        const int pg = p;
+        p += t1 - t0;
+        refresh();
         if (!needed(glo[g], ghi[g])) continue;
-        const int t1 = (g + 1) * kGroup < ntile ? (g + 1) * kGroup : ntile;
-        for (int t = g * kGroup; t < t1; ++t) scan(t);
+        // this wavefront's tiles of the group: positions pg + (t - t0) congruent to w
+        for (int t = t0 + ((w - pg) % kSplit + kSplit) % kSplit; t < t1; t += kSplit) scan(t);
     }
 
-    if (qid < 0) return;
+    // merge the states into wavefront 0
+    if (w > 0)
+#pragma unroll
+        for (int t = 0; t < KP; ++t) shkey[w - 1][t][lane] = kd[t];
+    __syncthreads();
+    if (w != 0 || qid < 0) return;
+#pragma unroll
+    for (int o = 0; o < kSplit - 1; ++o) {
+        uint64_t other[KP];
+#pragma unroll
+        for (int t = 0; t < KP; ++t) other[t] = shkey[o][t][lane];
+        merge_state<KP>(kd, other);
+    }
+
     // the first k entries of the padded state, in key order (-1: fewer than k finite candidates)
     int32_t sel[KP];
 #pragma unroll
@@ -334,10 +400,8 @@ __global__ __launch_bounds__(kBlock) void select_kernel(const f4 *__restrict__ r
 template <int KP>
 int launch_select(const Ws &w, int64_t ntile, int k, int feat, const float *x, float *y, int32_t *nbr,
                   hipStream_t stream) {
-    const int waves_per_block = kBlock / kWave;
-    const unsigned blocks = static_cast<unsigned>(ceil_div(ntile, waves_per_block));
     prof_before(stream);
-    hipLaunchKernelGGL(select_kernel<KP>, dim3(blocks), dim3(kBlock), 0, stream, w.rec, w.tlo, w.thi, w.glo, w.ghi,
+    hipLaunchKernelGGL(select_kernel<KP>, dim3(static_cast<unsigned>(ntile)), dim3(kSplit * kWave), 0, stream, w.rec, w.tlo, w.thi, w.glo, w.ghi,
                        static_cast<int>(ntile), k, feat, x, y, nbr);
     prof_after(stream);
     return check_launch("kNN select");
@@ -356,17 +420,19 @@ int forward(int64_t n, int32_t feat, const float *pos, const float *x, int32_t k
     Carve c(ws);
     Ws w = carve(c, n);
     const int64_t ntile = ceil_div(n, kTile);
-    const int np = static_cast<int>(ceil_div(n, kBlock) < kPartials ? ceil_div(n, kBlock) : kPartials);
-    hipLaunchKernelGGL(box_partial_kernel, dim3(np), dim3(kBlock), 0, stream, pos, n, w.part);
-    if (int rc = check_launch("kNN box")) return rc;
-    hipLaunchKernelGGL(box_final_kernel, dim3(1), dim3(kWave), 0, stream, w.part, np, w.box);
-    if (int rc = check_launch("kNN box")) return rc;
-    hipLaunchKernelGGL(morton_kernel, dim3(static_cast<unsigned>(ceil_div(n, kBlock))), dim3(kBlock), 0, stream, pos,
-                       n, w.box, w.key);
-    if (int rc = check_launch("kNN keys")) return rc;
-    if (int rc = csr::launch_sort_keys(w.key, n, int64_t{1} << (3 * kBits), w.key_sorted, w.perm, nullptr, w.sort,
-                                       stream))
-        return rc;
+    {
+        const int np = static_cast<int>(ceil_div(n, kBlock) < kPartials ? ceil_div(n, kBlock) : kPartials);
+        hipLaunchKernelGGL(box_partial_kernel, dim3(np), dim3(kBlock), 0, stream, pos, n, w.part);
+        if (int rc = check_launch("kNN box")) return rc;
+        hipLaunchKernelGGL(box_final_kernel, dim3(1), dim3(kWave), 0, stream, w.part, np, w.box);
+        if (int rc = check_launch("kNN box")) return rc;
+        hipLaunchKernelGGL(morton_kernel, dim3(static_cast<unsigned>(ceil_div(n, kBlock))), dim3(kBlock), 0, stream,
+                           pos, n, w.box, w.key);
+        if (int rc = check_launch("kNN keys")) return rc;
+        if (int rc = csr::launch_sort_keys(w.key, n, int64_t{1} << (3 * kBits), w.key_sorted, w.perm, nullptr, w.sort,
+                                           stream))
+            return rc;
+    }
     hipLaunchKernelGGL(records_kernel, dim3(static_cast<unsigned>(ceil_div(ntile * kTile, kBlock))), dim3(kBlock), 0,
                        stream, pos, w.perm, n, ntile * kTile, w.rec);
     if (int rc = check_launch("kNN records")) return rc;
