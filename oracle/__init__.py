@@ -54,6 +54,8 @@ def _load():
                 "tiga_oracle_radius_bwd": (C.c_int, [i64, i32, vp, vp, vp, f32, f32, i64, vp, vp, vp, vp, vp]),
                 "tiga_oracle_radius_neighbors": (C.c_int, [i64, vp, f32, i64, vp, vp, vp, vp]),
                 "tiga_oracle_dense_fwd": (None, [i64, vp, vp, f32, i64, vp, vp, vp]),
+                "tiga_oracle_edgenn": (None, [i64, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                              vp, vp, vp, vp]),
                 "tiga_oracle_knn": (C.c_int, [i64, i32, vp, vp, i32, i64, vp, vp, vp, vp]),
                 "tiga_oracle_f16_to_double": (C.c_double, [C.c_uint16]),
                 "tiga_oracle_bf16_to_double": (C.c_double, [C.c_uint16]),
@@ -240,3 +242,25 @@ def knn(pos, x, k, pts=None):
     if _load().tiga_oracle_knn(n, F, _p(pos), _p(x), int(k), npts, _p(pts), _p(nbr), _p(y), _p(ya)):
         raise MemoryError("oracle kNN: allocation failed")
     return nbr, y, ya
+
+
+def edgenn(pos, x, ptr, idx, W1, b1, W2, b2, dy=None):
+    """Edge-local MLP message summed per destination over the relation (ptr, idx); with dy also the
+    gradients of <dy, y>.  Returns dict(y, dx, dp, dW1, db1, dW2, db2) in fp64."""
+    pos, x = _c(pos, np.float32).reshape(-1, 3), _c(x, np.float32)
+    n = pos.shape[0]
+    x = x.reshape(n, -1)
+    F = x.shape[1]
+    W1, b1, W2, b2 = (_c(a, np.float32) for a in (W1, b1, W2, b2))
+    H, O = W1.shape[0], W2.shape[0]
+    assert W1.shape == (H, 3 + F) and b1.shape == (H,) and W2.shape == (O, H) and b2.shape == (O,)
+    ptr, idx = _c(ptr, np.int64), _c(idx, np.int32)
+    dy = _c(dy, np.float32)
+    out = dict(y=np.empty((n, O)))
+    if dy is not None:
+        out.update(dx=np.empty((n, F)), dp=np.empty((n, 3)), dW1=np.empty((H, 3 + F)), db1=np.empty(H),
+                   dW2=np.empty((O, H)), db2=np.empty(O))
+    g = lambda k: _p(out.get(k))
+    _load().tiga_oracle_edgenn(n, F, H, O, _p(pos), _p(x), _p(ptr), _p(idx), _p(W1), _p(b1), _p(W2), _p(b2),
+                               _p(dy), g("y"), g("dx"), g("dp"), g("dW1"), g("db1"), g("dW2"), g("db2"))
+    return out

@@ -698,3 +698,88 @@ int tiga_oracle_knn(int64_t n, int32_t F, const float *pos, const float *x, int3
     }
     return fail ? -1 : 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Edge-local MLP message over a given relation (appendix "A differentiable */
+/* EdgeNN example"; Section 5 for the vector-Jacobian product)              */
+/* ------------------------------------------------------------------------ */
+
+/* For the destination-major relation (ptr, idx) -- row i lists the sources j of
+ * destination i -- with the message
+ *   in_ij = [p_j - p_i ; x_j]                       (3 + F values, fp64)
+ *   a_ij  = W1 in_ij + b1,  r_ij = max(a_ij, 0)     (H values)
+ *   m_ij  = W2 r_ij + b2                            (O values; the final bias is
+ *                                                    part of every message)
+ *   y_i   = sum_{j in row i} m_ij                   (an empty row gives 0)
+ * W1 is [H][3 + F], b1 [H], W2 [O][H], b2 [O], all fp32 row-major; y is fp64
+ * [n][O].  If dy ([n][O], fp32) is given, the gradients of L = sum_i <dy_i, y_i>
+ * with the relation held fixed are formed as well (fp64, each may be NULL):
+ *   dm = dy_i;  dW2 += dm r^T;  db2 += dm;  da = (W2^T dm) * [a > 0];
+ *   dW1 += da in^T;  db1 += da;  din = W1^T da;
+ *   dp_j += din[0..3);  dp_i -= din[0..3);  dx_j += din[3..3+F).
+ * The derivative of max(a, 0) at a = 0 is taken as 0.  Serial over destinations
+ * in ascending order. */
+void tiga_oracle_edgenn(int64_t n, int32_t F, int32_t H, int32_t O, const float *pos, const float *x,
+                        const int64_t *ptr, const int32_t *idx, const float *W1, const float *b1,
+                        const float *W2, const float *b2, const float *dy, double *y, double *dx,
+                        double *dp, double *dW1, double *db1, double *dW2, double *db2) {
+    const int32_t D = 3 + F;
+    double *in = (double *)malloc(sizeof(double) * (size_t)D);
+    double *a = (double *)malloc(sizeof(double) * (size_t)H);
+    double *da = (double *)malloc(sizeof(double) * (size_t)H);
+    if (y) memset(y, 0, sizeof(double) * (size_t)(n * O));
+    if (dx) memset(dx, 0, sizeof(double) * (size_t)(n * F));
+    if (dp) memset(dp, 0, sizeof(double) * (size_t)(n * 3));
+    if (dW1) memset(dW1, 0, sizeof(double) * (size_t)(H * D));
+    if (db1) memset(db1, 0, sizeof(double) * (size_t)H);
+    if (dW2) memset(dW2, 0, sizeof(double) * (size_t)(O * H));
+    if (db2) memset(db2, 0, sizeof(double) * (size_t)O);
+    for (int64_t i = 0; i < n; ++i) {
+        for (int64_t e = ptr[i]; e < ptr[i + 1]; ++e) {
+            const int64_t j = idx[e];
+            for (int c = 0; c < 3; ++c) in[c] = (double)pos[j * 3 + c] - (double)pos[i * 3 + c];
+            for (int c = 0; c < F; ++c) in[3 + c] = (double)x[j * F + c];
+            for (int h = 0; h < H; ++h) {
+                double s = (double)b1[h];
+                for (int c = 0; c < D; ++c) s += (double)W1[h * D + c] * in[c];
+                a[h] = s;
+            }
+            if (y)
+                for (int o = 0; o < O; ++o) {
+                    double s = (double)b2[o];
+                    for (int h = 0; h < H; ++h) s += (double)W2[o * H + h] * (a[h] > 0.0 ? a[h] : 0.0);
+                    y[i * O + o] += s;
+                }
+            if (!dy) continue;
+            const float *dm = dy + i * O;
+            for (int o = 0; o < O; ++o) {
+                if (dW2)
+                    for (int h = 0; h < H; ++h) dW2[o * H + h] += (double)dm[o] * (a[h] > 0.0 ? a[h] : 0.0);
+                if (db2) db2[o] += (double)dm[o];
+            }
+            for (int h = 0; h < H; ++h) {
+                double s = 0.0;
+                for (int o = 0; o < O; ++o) s += (double)W2[o * H + h] * (double)dm[o];
+                da[h] = a[h] > 0.0 ? s : 0.0;
+                if (db1) db1[h] += da[h];
+                if (dW1)
+                    for (int c = 0; c < D; ++c) dW1[h * D + c] += da[h] * in[c];
+            }
+            for (int c = 0; c < D; ++c) {
+                double s = 0.0;
+                for (int h = 0; h < H; ++h) s += (double)W1[h * D + c] * da[h];
+                if (c < 3) {
+                    if (dp) {
+                        dp[j * 3 + c] += s;
+                        dp[i * 3 + c] -= s;
+                    }
+                } else if (dx) {
+                    dx[j * F + (c - 3)] += s;
+                }
+            }
+        }
+    }
+    free(in);
+    free(a);
+    free(da);
+}

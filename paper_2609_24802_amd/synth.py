@@ -252,3 +252,37 @@ def knn_inputs(n: int, feat: int = 1, cfg: int = 7):
     pos = uniform_f32(n * 3, 0.0, 1.0, (cfg, 0, n)).reshape(n, 3)
     x = normal_f32(n * feat, (cfg, 1, n, feat)).reshape(n, feat)
     return dict(pos=pos, x=x, k=16)
+
+
+def surface_points(n: int, key: tuple, axes=(0.5, 0.45, 0.40)) -> np.ndarray:
+    """Points on an ellipsoid surface (directions uniform on the sphere, scaled by the semi-axes),
+    centred and divided by the largest bounding-box extent: a closed-surface cloud standing in for
+    a scanned surface mesh's vertices."""
+    d = normal_f32(n * 3, key).reshape(n, 3).astype(np.float64)
+    d /= np.linalg.norm(d, axis=1, keepdims=True)
+    p = d * np.asarray(axes, np.float64)
+    p -= 0.5 * (p.min(0) + p.max(0))
+    p /= (p.max(0) - p.min(0)).max()
+    return p.astype(np.float32)
+
+
+def mlp_params(fan_in: int, hidden: int, out: int, key: tuple):
+    """Weights of Linear(fan_in, hidden) -> ReLU -> Linear(hidden, out), each entry uniform in
+    +-1/sqrt(fan in) of its layer (the usual untrained initialization)."""
+    b1 = 1.0 / math.sqrt(fan_in)
+    b2 = 1.0 / math.sqrt(hidden)
+    return dict(W1=uniform_f32(hidden * fan_in, -b1, b1, key + (0,)).reshape(hidden, fan_in),
+                b1=uniform_f32(hidden, -b1, b1, key + (1,)),
+                W2=uniform_f32(out * hidden, -b2, b2, key + (2,)).reshape(out, hidden),
+                b2=uniform_f32(out, -b2, b2, key + (3,)))
+
+
+def edgenn_inputs(n: int = 35947, feat: int = 8, hidden: int = 32, out: int = 3, radius: float = 0.015, cfg: int = 8):
+    """The differentiated edge-MLP workload: surface points (35,947 of them, the size of the scanned
+    surface the evaluation uses), radius 0.015, N(0, 1) features of width 8 or 32, an untrained
+    MLP (3 + feat) -> hidden -> out, and an N(0, 1) output cotangent."""
+    pos = surface_points(n, (cfg, 0, n))
+    x = normal_f32(n * feat, (cfg, 1, n, feat)).reshape(n, feat)
+    prm = mlp_params(3 + feat, hidden, out, (cfg, 2, feat, hidden, out))
+    dy = normal_f32(n * out, (cfg, 3, n, out)).reshape(n, out)
+    return dict(pos=pos, x=x, radius=np.float32(radius), dy=dy, **prm)
