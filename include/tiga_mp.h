@@ -254,6 +254,41 @@ size_t tiga_mp_knn_workspace(int64_t n);
 int tiga_mp_knn_fwd(int64_t n, int32_t feat, const float *pos, const float *x, int32_t k, int reducer, float *y,
                     int32_t *nbr, void *ws, size_t ws_bytes, void *stream);
 
+/* -------------------------------- edge-local MLP message on the radius relation */
+
+/* Workspace bytes for tiga_mp_edgenn_fwd / _bwd (0 on error). */
+size_t tiga_mp_edgenn_workspace(int64_t n, int32_t feat, int32_t hidden, int32_t out);
+
+/* Edge-local neural-network message summed over the generated radius relation
+ * (appendix "A differentiable EdgeNN example"; the relation as in
+ * tiga_mp_radius_fwd: j != i and the fp32 squared distance strictly below
+ * fl(radius*radius)):
+ *   in_ij = [p_j - p_i ; x_j]  (3 + feat values; fp32 differences)
+ *   y_i   = sum_{j in N(i)} ( W2 max(W1 in_ij + b1, 0) + b2 )
+ * (the final bias is part of every message; an empty row gives 0).  No edge,
+ * message or hidden activation is stored.
+ *   pos fp32 [n, 3]; x fp32 [n, feat] (NULL if feat == 0);
+ *   W1 [hidden, 3 + feat], b1 [hidden], W2 [out, hidden], b2 [out] fp32
+ *   row-major; y fp32 [n, out], overwritten.
+ * Requires 0 <= feat <= 64, 1 <= hidden <= 64, 1 <= out <= 8
+ * (TIGA_EUNSUPPORTED beyond), radius finite and > 0, n < 2^31 - 64.
+ * Errors: TIGA_EINVAL, TIGA_EUNSUPPORTED, TIGA_EWORKSPACE, TIGA_EDEVICE. */
+int tiga_mp_edgenn_fwd(int64_t n, int32_t feat, int32_t hidden, int32_t out, const float *pos, const float *x,
+                       float radius, const float *W1, const float *b1, const float *W2, const float *b2, float *y,
+                       void *ws, size_t ws_bytes, void *stream);
+
+/* Vector-Jacobian product of tiga_mp_edgenn_fwd with the relation held fixed
+ * (Section 5: radius membership is discrete and not differentiated); hidden
+ * activations are recomputed, never stored.  For L = sum_i <dy_i, y_i>:
+ *   dx [n, feat], dpos [n, 3], dW1 [hidden, 3 + feat], db1 [hidden],
+ *   dW2 [out, hidden], db2 [out]   (fp32; each may be NULL; overwritten).
+ * The derivative of max(a, 0) at a = 0 is 0.  Deterministic: fixed
+ * summation orders for every output.  Arguments and errors as the forward. */
+int tiga_mp_edgenn_bwd(int64_t n, int32_t feat, int32_t hidden, int32_t out, const float *pos, const float *x,
+                       float radius, const float *W1, const float *b1, const float *W2, const float *b2,
+                       const float *dy, float *dx, float *dpos, float *dW1, float *db1, float *dW2, float *db2,
+                       void *ws, size_t ws_bytes, void *stream);
+
 /* ------------------------------- online-softmax reducer (streaming attention) */
 
 /* 16-bit input types of the attention path. */

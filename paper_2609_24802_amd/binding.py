@@ -69,6 +69,14 @@ _SIGS = {
     "tiga_mp_dense_workspace": (C.c_size_t, [C.c_int64]),
     "tiga_mp_dense_fwd": (C.c_int, [C.c_int64, C.c_void_p, C.c_void_p, C.c_float, C.c_int, C.c_void_p,
                                     C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tiga_mp_edgenn_workspace": (C.c_size_t, [C.c_int64, C.c_int32, C.c_int32, C.c_int32]),
+    "tiga_mp_edgenn_fwd": (C.c_int, [C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_float,
+                                     C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                     C.c_size_t, C.c_void_p]),
+    "tiga_mp_edgenn_bwd": (C.c_int, [C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_float,
+                                     C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                     C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                     C.c_size_t, C.c_void_p]),
     "tiga_mp_knn_workspace": (C.c_size_t, [C.c_int64]),
     "tiga_mp_knn_fwd": (C.c_int, [C.c_int64, C.c_int32, C.c_void_p, C.c_void_p, C.c_int32, C.c_int, C.c_void_p,
                                   C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
@@ -291,6 +299,49 @@ def tiga_mp_dense_fwd(pos: torch.Tensor, q: torch.Tensor, eps: float, y=None, ws
     return y
 
 
+def _edgenn_args(pos, x, W1, b1, W2, b2):
+    n = pos.shape[0]
+    _dev(pos, torch.float32, "pos", (n, 3))
+    H, D = W1.shape
+    F = D - 3
+    O = W2.shape[0]
+    _dev(W1, torch.float32, "W1", (H, D))
+    _dev(b1, torch.float32, "b1", (H,))
+    _dev(W2, torch.float32, "W2", (O, H))
+    _dev(b2, torch.float32, "b2", (O,))
+    if F > 0:
+        _dev(x, torch.float32, "x", (n, F))
+    return n, F, H, O
+
+
+def tiga_mp_edgenn_fwd(pos, x, radius, W1, b1, W2, b2, ws=None):
+    """y_i = sum over the radius relation of W2 relu(W1 [p_j - p_i; x_j] + b1) + b2; returns y fp32 [n, out]."""
+    lib = load()
+    n, F, H, O = _edgenn_args(pos, x, W1, b1, W2, b2)
+    y = torch.empty(n, O, dtype=torch.float32, device=pos.device)
+    if ws is None:
+        ws = _workspace(lib.tiga_mp_edgenn_workspace(n, F, H, O), pos.device)
+    _check(lib.tiga_mp_edgenn_fwd(n, F, H, O, _ptr(pos), _ptr(x) if F else None, float(radius), _ptr(W1), _ptr(b1),
+                                  _ptr(W2), _ptr(b2), _ptr(y), _ptr(ws), ws.numel(), _stream()))
+    return y
+
+
+def tiga_mp_edgenn_bwd(pos, x, radius, W1, b1, W2, b2, dy, want=("dx", "dpos", "dW1", "db1", "dW2", "db2"), ws=None):
+    """The VJP of tiga_mp_edgenn_fwd for the cotangent dy [n, out]; returns a dict of the wanted gradients."""
+    lib = load()
+    n, F, H, O = _edgenn_args(pos, x, W1, b1, W2, b2)
+    _dev(dy, torch.float32, "dy", (n, O))
+    shapes = dict(dx=(n, F), dpos=(n, 3), dW1=(H, 3 + F), db1=(H,), dW2=(O, H), db2=(O,))
+    out = {k: torch.empty(*shapes[k], dtype=torch.float32, device=pos.device) for k in want if shapes[k][-1] > 0}
+    if ws is None:
+        ws = _workspace(lib.tiga_mp_edgenn_workspace(n, F, H, O), pos.device)
+    g = lambda k: _ptr(out.get(k))
+    _check(lib.tiga_mp_edgenn_bwd(n, F, H, O, _ptr(pos), _ptr(x) if F else None, float(radius), _ptr(W1), _ptr(b1),
+                                  _ptr(W2), _ptr(b2), _ptr(dy), g("dx"), g("dpos"), g("dW1"), g("db1"), g("dW2"),
+                                  g("db2"), _ptr(ws), ws.numel(), _stream()))
+    return out
+
+
 def tiga_mp_knn_fwd(pos: torch.Tensor, x: torch.Tensor | None, k: int, want_nbr: bool = False, ws=None):
     """Exact kNN relation (self excluded, key (fp32 d2, index)) with the neighbour sum y_i = sum x_j.
 
@@ -424,3 +475,23 @@ class RadiusAggregate(torch.autograd.Function):
 def radius_aggregate(pos: torch.Tensor, x: torch.Tensor, radius: float, sigma: float) -> torch.Tensor:
     """Differentiable fused aggregation over the generated radius relation."""
     return RadiusAggregate.apply(pos, x, radius, sigma)
+
+
+class EdgeMLP(torch.autograd.Function):
+    """y = sum over the radius relation of W2 relu(W1 [p_j - p_i; x_j] + b1) + b2 (membership fixed)."""
+
+    @staticmethod
+    def forward(ctx, pos, x, W1, b1, W2, b2, radius):
+        ctx.radius = radius
+        ctx.save_for_backward(pos, x, W1, b1, W2, b2)
+        return tiga_mp_edgenn_fwd(pos, x, radius, W1, b1, W2, b2)
+
+    @staticmethod
+    def backward(ctx, dy):
+        pos, x, W1, b1, W2, b2 = ctx.saved_tensors
+        g = tiga_mp_edgenn_bwd(pos, x, ctx.radius, W1, b1, W2, b2, dy.contiguous())
+        return g["dpos"], g.get("dx"), g["dW1"], g["db1"], g["dW2"], g["db2"], None
+
+
+def edge_mlp(pos, x, W1, b1, W2, b2, radius):
+    return EdgeMLP.apply(pos, x, W1, b1, W2, b2, radius)

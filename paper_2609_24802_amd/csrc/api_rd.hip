@@ -1,5 +1,6 @@
 // C ABI of the generated radius relation and the dense all-pairs relation.
 #include "dense.hpp"
+#include "edgenn.hpp"
 #include "knn.hpp"
 #include "radius.hpp"
 
@@ -95,6 +96,62 @@ int tiga_mp_dense_fwd(int64_t n, const float *pos, const float *q, float eps, in
     if (!q || !y) return fail(TIGA_EINVAL, "q and y are required");
     if (int rc = check_ws(ws, ws_bytes, dense::workspace_bytes(n))) return rc;
     return dense::forward(n, pos, q, eps, y, ws, static_cast<hipStream_t>(stream));
+}
+
+namespace {
+
+int check_net(int32_t feat, int32_t hidden, int32_t out) {
+    if (feat < 0 || hidden < 1 || out < 1) return fail(TIGA_EINVAL, "need feat >= 0, hidden >= 1, out >= 1");
+    if (feat > edgenn::kMaxFeat || hidden > edgenn::kMaxHidden || out > edgenn::kMaxOut)
+        return fail(TIGA_EUNSUPPORTED, "edge MLP widths feat %d, hidden %d, out %d exceed %d, %d, %d", feat, hidden,
+                    out, edgenn::kMaxFeat, edgenn::kMaxHidden, edgenn::kMaxOut);
+    return TIGA_OK;
+}
+
+}  // namespace
+
+size_t tiga_mp_edgenn_workspace(int64_t n, int32_t feat, int32_t hidden, int32_t out) {
+    if (n < 0 || feat < 0 || hidden < 1 || out < 1) return 0;
+    return edgenn::workspace_bytes(n, edgenn::Net{feat, hidden, out, nullptr, nullptr, nullptr, nullptr});
+}
+
+int tiga_mp_edgenn_fwd(int64_t n, int32_t feat, int32_t hidden, int32_t out, const float *pos, const float *x,
+                       float radius, const float *W1, const float *b1, const float *W2, const float *b2, float *y,
+                       void *ws, size_t ws_bytes, void *stream) {
+    EntryScope scope;
+    if (int rc = check_points(n, pos)) return rc;
+    if (int rc = check_net(feat, hidden, out)) return rc;
+    if (int rc = check_radius(radius, 1.0f)) return rc;
+    if (n == 0) return TIGA_OK;
+    if (!W1 || !b1 || !W2 || !b2 || !y || (feat > 0 && !x)) return fail(TIGA_EINVAL, "a required array is NULL");
+    const edgenn::Net net{feat, hidden, out, W1, b1, W2, b2};
+    if (int rc = check_ws(ws, ws_bytes, edgenn::workspace_bytes(n, net))) return rc;
+    return edgenn::forward(n, pos, x, radius, net, y, ws, static_cast<hipStream_t>(stream));
+}
+
+int tiga_mp_edgenn_bwd(int64_t n, int32_t feat, int32_t hidden, int32_t out, const float *pos, const float *x,
+                       float radius, const float *W1, const float *b1, const float *W2, const float *b2,
+                       const float *dy, float *dx, float *dpos, float *dW1, float *db1, float *dW2, float *db2,
+                       void *ws, size_t ws_bytes, void *stream) {
+    EntryScope scope;
+    if (int rc = check_points(n, pos)) return rc;
+    if (int rc = check_net(feat, hidden, out)) return rc;
+    if (int rc = check_radius(radius, 1.0f)) return rc;
+    if (n == 0) {
+        // no messages: the parameter gradients are zero
+        hipStream_t s = static_cast<hipStream_t>(stream);
+        const int64_t D = 3 + feat;
+        if (dW1) if (int rc = fill_u32(dW1, 0u, hidden * D, s)) return rc;
+        if (db1) if (int rc = fill_u32(db1, 0u, hidden, s)) return rc;
+        if (dW2) if (int rc = fill_u32(dW2, 0u, static_cast<int64_t>(out) * hidden, s)) return rc;
+        if (db2) if (int rc = fill_u32(db2, 0u, out, s)) return rc;
+        return TIGA_OK;
+    }
+    if (!W1 || !b1 || !W2 || !b2 || !dy || (feat > 0 && !x)) return fail(TIGA_EINVAL, "a required array is NULL");
+    const edgenn::Net net{feat, hidden, out, W1, b1, W2, b2};
+    if (int rc = check_ws(ws, ws_bytes, edgenn::workspace_bytes(n, net))) return rc;
+    return edgenn::backward(n, pos, x, radius, net, dy, edgenn::Grads{dx, dpos, dW1, db1, dW2, db2}, ws,
+                            static_cast<hipStream_t>(stream));
 }
 
 size_t tiga_mp_knn_workspace(int64_t n) {

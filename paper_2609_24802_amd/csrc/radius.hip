@@ -12,6 +12,7 @@
 // in memory).
 #include "csr_bwd.hpp"
 #include "radius.hpp"
+#include "radius_cells.hpp"
 
 namespace tiga {
 namespace radius {
@@ -23,12 +24,6 @@ namespace {
 
 constexpr int kBlock = 256;
 
-struct Params {
-    double lo[3];
-    double inv_h;
-    int dim[3];
-    int ncell;
-};
 
 __global__ __launch_bounds__(kBlock) void bbox_partial_kernel(const float *__restrict__ pos, int64_t n,
                                                               float *__restrict__ part) {
@@ -148,13 +143,6 @@ __global__ __launch_bounds__(kBlock) void grid_params_kernel(const float *__rest
 
 // Cell coordinate along axis a, clamped to [0, dim - 1] before conversion
 // (NaN and -inf go to 0, +inf to the last cell).
-__device__ __forceinline__ int cell_axis(const Params &p, int a, float v) {
-    double t = floor((static_cast<double>(v) - p.lo[a]) * p.inv_h);
-    if (!(t >= 0.0)) t = 0.0;
-    const double top = static_cast<double>(p.dim[a] - 1);
-    if (t > top) t = top;
-    return static_cast<int>(t);
-}
 
 // Cell id of every point (z-major, x fastest).
 __global__ __launch_bounds__(kBlock) void cell_key_kernel(const float *__restrict__ pos, int64_t n,
@@ -181,40 +169,7 @@ __global__ __launch_bounds__(kBlock) void gather_records_kernel(const int32_t *_
 }
 
 
-// Exact membership test: direct fp32 differences, products and sums, each
-// rounded once (no contraction), strict comparison with fp32(r*r).
-__device__ __forceinline__ bool accept(float4 pi, float4 pj, float r2, float &d2) {
-#pragma clang fp contract(off)
-    const float dx = pj.x - pi.x;
-    const float dy = pj.y - pi.y;
-    const float dz = pj.z - pi.z;
-    const float sx = dx * dx;
-    const float sy = dy * dy;
-    const float sz = dz * dz;
-    d2 = (sx + sy) + sz;
-    return d2 < r2;
-}
 
-// Visit the candidate runs of the point with record `pi`.
-template <class F>
-__device__ __forceinline__ void for_candidates(const Params &p, const int64_t *__restrict__ start, float4 pi,
-                                               F &&body) {
-    const int cx = cell_axis(p, 0, pi.x);
-    const int cy = cell_axis(p, 1, pi.y);
-    const int cz = cell_axis(p, 2, pi.z);
-    const int x0 = cx > 0 ? cx - 1 : 0;
-    const int x1 = cx + 1 < p.dim[0] ? cx + 1 : p.dim[0] - 1;
-    for (int z = cz - 1; z <= cz + 1; ++z) {
-        if (z < 0 || z >= p.dim[2]) continue;
-        for (int y = cy - 1; y <= cy + 1; ++y) {
-            if (y < 0 || y >= p.dim[1]) continue;
-            const int rowc = (z * p.dim[1] + y) * p.dim[0];
-            const int64_t b = start[rowc + x0];
-            const int64_t e = start[rowc + x1 + 1];
-            for (int64_t t = b; t < e; ++t) body(t);
-        }
-    }
-}
 
 // ---------------------------------------------------------------------------
 // Consume: one wavefront per destination cell.
@@ -842,6 +797,22 @@ int backward(int64_t n, int32_t feat, const float *pos, const float *x, float ra
         TIGA_B(1);
     }
 #undef TIGA_B
+}
+
+size_t cells_ws_bytes(int64_t n) {
+    Carve c(nullptr);
+    carve(c, n);
+    return c.bytes();
+}
+
+int build_cells(int64_t n, const float *pos, float radius, void *ws, Cells &out, hipStream_t stream) {
+    Carve c(ws);
+    Ws w = carve(c, n);
+    if (int rc = build(n, pos, radius, w, stream)) return rc;
+    out.prm = w.prm;
+    out.start = w.start;
+    out.rec = w.rec;
+    return TIGA_OK;
 }
 
 int neighbors(int64_t n, const float *pos, float radius, int32_t *count, int64_t *nbr_ptr, int32_t *nbr_idx,

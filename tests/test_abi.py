@@ -167,3 +167,21 @@ def test_knn_errors(clib):
     assert clib.tiga_mp_knn_fwd(-1, 1, fake, fake, 16, b.REDUCE_SUM, fake, None, fake, big, None) == b.TIGA_EINVAL
     assert clib.tiga_mp_knn_fwd(0, 1, None, None, 16, b.REDUCE_SUM, None, None, None, 0, None) == b.TIGA_OK
     assert clib.tiga_mp_knn_workspace(1000) < clib.tiga_mp_knn_workspace(100000)
+
+
+def test_edgenn_errors(clib):
+    from paper_2609_24802_amd import binding as b
+    f = C.c_void_p(0x10000)
+    big = 1 << 40
+    call = lambda n=100, F=8, H=32, O=3, r=0.1, ws=f, wsb=big: clib.tiga_mp_edgenn_fwd(
+        n, F, H, O, f, f, r, f, f, f, f, f, ws, wsb, None)
+    assert call(F=65) == b.TIGA_EUNSUPPORTED
+    assert call(H=65) == b.TIGA_EUNSUPPORTED
+    assert call(O=9) == b.TIGA_EUNSUPPORTED
+    assert call(H=0) == b.TIGA_EINVAL
+    assert call(r=0.0) == b.TIGA_EINVAL
+    assert call(wsb=8) == b.TIGA_EWORKSPACE
+    assert call(n=0, ws=None, wsb=0) == b.TIGA_OK
+    assert clib.tiga_mp_edgenn_bwd(100, 8, 32, 3, f, f, 0.1, f, f, f, f, None, f, f, f, f, f, f, f, big,
+                                   None) == b.TIGA_EINVAL   # dy is required
+    assert clib.tiga_mp_edgenn_workspace(1000, 8, 32, 3) < clib.tiga_mp_edgenn_workspace(100000, 8, 32, 3)
