@@ -47,11 +47,12 @@ def parse():
     p.add_argument("--no-ceilings", action="store_true", help="skip the hardware-ceiling probe")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--check-rows", type=int, default=400)
-    p.add_argument("--profile-pass", nargs="?", const="csr", choices=["csr", "radius", "dense", "attention", "knn"],
+    p.add_argument("--profile-pass", nargs="?", const="csr", choices=["csr", "radius", "dense", "attention", "knn", "edgenn"],
                    help="for rocprofv3 counter runs: csr = a 4 GiB plain copy (calibration) then 3 headline steps; "
                         "radius / dense / attention = 3 forward calls on the radius (1M points) / dense (65536 points) / "
                         "attention (16 heads x 16384 tokens x 128, binary16, triangular) workload; knn = 3 calls on "
-                        "131072 uniform points, k = 16")
+                        "131072 uniform points, k = 16; edgenn = 3 forward + backward calls of the edge MLP on 35947 "
+                        "surface points (feat 8)")
     p.add_argument("--paths-only", action="store_true", help="only the per-path figures (for kernel traces)")
     p.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                    help="print the markdown summary of three rocprofv3 runs (kernel trace, FETCH_SIZE, WRITE_SIZE)")
@@ -66,6 +67,8 @@ PROFILE_MD = os.path.join(ROOT, "profiles", "gather_reduce_csr_powerlaw_1b_f16.m
 VALU_LANE_OPS_PER_S = 256 * 4 * 16 * 2.4e9  # CUs * SIMDs * lanes per cycle * clock
 VALU_INSTR_PER_PAIR = 12
 MFMA16_PEAK_TFLOPS = 2500.0  # dense fp16 / bf16 MFMA peak
+# input widths of the edge-MLP workload (the first is profiled)
+EDGENN_FEATS = [8, 32]
 # exact kNN workload sizes (the largest is profiled)
 KNN_SIZES = [1024, 16384, 131072]
 # (tokens, heads, width, dtype, relation); the first is the profiled attention workload
@@ -383,6 +386,22 @@ def paths(args, torch, tb, synth):
     log(f"dense: {rr['step_ms']:.3f} ms ({tf:.1f} TFLOP/s)")
     del pd, qd
 
+    # edge-local MLP message on the radius relation (35,947 surface points, r = 0.015, hidden 32, 3
+    # outputs): forward and its VJP (all six gradients), each rebuilding the relation
+    for F in EDGENN_FEATS:
+        g = synth.edgenn_inputs(feat=F)
+        pd, xd, dyd = dev(g["pos"]), dev(g["x"]), dev(g["dy"])
+        W = [dev(g[k]) for k in ("W1", "b1", "W2", "b2")]
+        nn_, H, O = pd.shape[0], W[0].shape[0], W[2].shape[0]
+        ws = tb._workspace(tb.load().tiga_mp_edgenn_workspace(nn_, F, H, O), pd.device)
+        rf = time_steps(torch, tb, lambda: tb.tiga_mp_edgenn_fwd(pd, xd, g["radius"], *W, ws=ws), steps, warm)
+        rb = time_steps(torch, tb, lambda: tb.tiga_mp_edgenn_bwd(pd, xd, g["radius"], *W, dyd, ws=ws), steps, warm)
+        res[f"edgenn_surface_{nn_}_f{F}_h{H}_o{O}"] = dict(
+            fwd_ms=rf["step_ms"], fwd_kernel_ms=float(np.mean(rf["kernel_ms"])), bwd_ms=rb["step_ms"],
+            bwd_kernel_ms=float(np.mean(rb["kernel_ms"])), total_ms=rf["step_ms"] + rb["step_ms"])
+        log(f"edgenn F={F}: fwd {rf['step_ms']:.3f} ms, bwd {rb['step_ms']:.3f} ms")
+        del pd, xd, dyd, W, ws
+
     # exact kNN relation with the neighbour sum (k = 16, scalar features): the build (curve order, tile
     # boxes) plus the select-and-sum kernel; pairs = n (n - 1) ordered pairs the relation decides over
     for nk in KNN_SIZES:
@@ -423,6 +442,16 @@ def profile_pass(args, torch, tb, synth):
         pd, xd = dev(g["pos"]), dev(g["x"])
         for _ in range(3):
             tb.tiga_mp_radius_fwd(pd, xd, g["radius"], g["sigma"])
+        torch.cuda.synchronize()
+        log("profile pass done")
+        return
+    if args.profile_pass == "edgenn":
+        g = synth.edgenn_inputs(feat=EDGENN_FEATS[0])
+        pd, xd, dyd = dev(g["pos"]), dev(g["x"]), dev(g["dy"])
+        W = [dev(g[k]) for k in ("W1", "b1", "W2", "b2")]
+        for _ in range(3):
+            tb.tiga_mp_edgenn_fwd(pd, xd, g["radius"], *W)
+            tb.tiga_mp_edgenn_bwd(pd, xd, g["radius"], *W, dyd)
         torch.cuda.synchronize()
         log("profile pass done")
         return

@@ -234,13 +234,27 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(const Params *__restrict__ 
         for (int o = 0; o < O; ++o) pw[H * D + H + O * H + o] = gb2[o];
 }
 
-// Sum the per-wavefront partials (in wavefront order) into the parameter gradients.
-__global__ __launch_bounds__(kBlock) void reduce_params_kernel(const float *__restrict__ part, int64_t nw, int64_t P,
-                                                               Net net, Grads g) {
+// Sum the per-wavefront partials into the parameter gradients in two fixed-order stages: each of
+// kGroups groups of wavefronts per parameter (consecutive wavefronts, in order), then the groups.
+constexpr int kGroups = 32;
+
+__global__ __launch_bounds__(kWave) void reduce_groups_kernel(const float *__restrict__ part, int64_t nw, int64_t P,
+                                                              float *__restrict__ grp) {
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * kWave + threadIdx.x;
+    if (q >= P) return;
+    const int64_t per = (nw + kGroups - 1) / kGroups;
+    const int64_t w0 = blockIdx.y * per, w1 = w0 + per < nw ? w0 + per : nw;
+    float s = 0.0f;
+    for (int64_t w = w0; w < w1; ++w) s += part[w * P + q];
+    grp[static_cast<int64_t>(blockIdx.y) * P + q] = s;
+}
+
+__global__ __launch_bounds__(kBlock) void reduce_params_kernel(const float *__restrict__ grp, int64_t P, Net net,
+                                                               Grads g) {
     const int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
     if (q >= P) return;
     float s = 0.0f;
-    for (int64_t w = 0; w < nw; ++w) s += part[w * P + q];
+    for (int gi = 0; gi < kGroups; ++gi) s += grp[gi * P + q];
     const int64_t D = 3 + net.feat, H = net.hidden, O = net.out;
     if (q < H * D) {
         if (g.dW1) g.dW1[q] = s;
@@ -269,7 +283,7 @@ int launch_fwd(int64_t n, const Cells &cl, float r2, const float *x, const Net &
 
 template <int HP, int FP>
 int launch_bwd(int64_t n, const Cells &cl, float r2, const float *x, const Net &net, const float *dy, const Grads &g,
-               float *part, hipStream_t stream) {
+               float *part, float *grp, hipStream_t stream) {
     const int blocks = grid_blocks(n);
     const int64_t P = param_count(net);
     const bool params = g.dW1 || g.db1 || g.dW2 || g.db2;
@@ -279,8 +293,11 @@ int launch_bwd(int64_t n, const Cells &cl, float r2, const float *x, const Net &
     prof_after(stream);
     if (int rc = check_launch("edge MLP backward")) return rc;
     if (!params) return TIGA_OK;
+    hipLaunchKernelGGL(reduce_groups_kernel, dim3(static_cast<unsigned>(ceil_div(P, kWave)), kGroups), dim3(kWave), 0,
+                       stream, part, static_cast<int64_t>(blocks) * (kBlock / kWave), P, grp);
+    if (int rc = check_launch("edge MLP parameter reduction")) return rc;
     hipLaunchKernelGGL(reduce_params_kernel, dim3(static_cast<unsigned>(ceil_div(P, kBlock))), dim3(kBlock), 0,
-                       stream, part, static_cast<int64_t>(blocks) * (kBlock / kWave), P, net, g);
+                       stream, grp, P, net, g);
     return check_launch("edge MLP parameter reduction");
 }
 
@@ -307,6 +324,7 @@ size_t workspace_bytes(int64_t n, const Net &net) {
     Carve c(nullptr);
     c.take<char>(radius::cells_ws_bytes(n));
     c.take<float>(static_cast<size_t>(kMaxWaves) * param_count(net));
+    c.take<float>(static_cast<size_t>(kGroups) * param_count(net));
     return c.bytes();
 }
 
@@ -327,11 +345,12 @@ int backward(int64_t n, const float *pos, const float *x, float radius, const Ne
     Carve c(ws);
     void *cws = c.take<char>(radius::cells_ws_bytes(n));
     float *part = c.take<float>(static_cast<size_t>(kMaxWaves) * param_count(net));
+    float *grp = c.take<float>(static_cast<size_t>(kGroups) * param_count(net));
     Cells cl;
     if (int rc = radius::build_cells(n, pos, radius, cws, cl, stream)) return rc;
     const float r2 = radius * radius;
     return dispatch(net, [&](auto hp, auto fp) {
-        return launch_bwd<decltype(hp)::value, decltype(fp)::value>(n, cl, r2, x, net, dy, g, part, stream);
+        return launch_bwd<decltype(hp)::value, decltype(fp)::value>(n, cl, r2, x, net, dy, g, part, grp, stream);
     });
 }
 
