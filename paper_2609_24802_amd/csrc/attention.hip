@@ -92,6 +92,16 @@ struct Geo {
     static constexpr int LDS_V = D * VS;
 };
 
+// Maximum over the four lanes l, l^16, l^32, l^48 (the lanes that share a query column), with
+// the gfx950 lane swaps (VALU, no LDS round trip): each swap returns, per lane, its own value and
+// its partner's.
+__device__ __forceinline__ float max_over_column(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 __device__ __forceinline__ uint32_t lo16(uint32_t a, uint32_t b) { return (a & 0xffffu) | (b << 16); }
 __device__ __forceinline__ uint32_t hi16(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
 
@@ -268,8 +278,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restr
                 for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) mt = fmaxf(mt, s[kb][qb][i]);
-                mt = fmaxf(mt, __shfl_xor(mt, 16, kWave));
-                mt = fmaxf(mt, __shfl_xor(mt, 32, kWave));
+                mt = max_over_column(mt);
                 mt *= c;
                 if (__any(mt > m[qb] + kLazy)) {
                     const float mn = fmaxf(m[qb], mt);
