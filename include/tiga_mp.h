@@ -133,6 +133,30 @@ int tiga_mp_csr_fwd(const tiga_csr *rel, int32_t feat, const float *x_src, int m
                     const float *w_edge, int reducer, float *y, int32_t *argmax,
                     void *ws, size_t ws_bytes, void *stream);
 
+/* Workspace bytes for tiga_mp_csr_fwd_paged with pages of at most page_edges
+ * edges (0 on error).  Independent of the relation's size. */
+size_t tiga_mp_csr_fwd_paged_workspace(int32_t feat, int reducer, int64_t page_edges);
+
+/* tiga_mp_csr_fwd for a relation kept in HOST memory (Section 6, storage and
+ * memory: the relation stays in a persistent store, one destination-row page
+ * at a time is staged, and the kernel runs with a bounded device working set;
+ * the output stays in device memory).
+ *   rel_host: row_ptr and col_idx are HOST pointers (pinned memory lets the
+ *             copies run asynchronously); w_host likewise (or NULL, see msg).
+ *   x_src, y, argmax: DEVICE pointers, as in tiga_mp_csr_fwd.
+ * Pages hold whole destination rows and at most page_edges edges; each page's
+ * slices are copied on `stream` into the workspace and reduced there, so the
+ * device working set is fixed by page_edges.  Results equal tiga_mp_csr_fwd's
+ * (argmax holds global edge positions).  The host reads rel_host->row_ptr
+ * during the call (to cut pages and to reject a row longer than page_edges
+ * with TIGA_EUNSUPPORTED, or a row_ptr that does not run from 0 to num_edges
+ * without decreasing with TIGA_EGRAPH); the host arrays must stay valid until
+ * the stream has run the copies.
+ * Errors: as tiga_mp_csr_fwd, plus TIGA_EGRAPH. */
+int tiga_mp_csr_fwd_paged(const tiga_csr *rel_host, int32_t feat, const float *x_src, int msg,
+                          const float *w_host, int reducer, float *y, int32_t *argmax, int64_t page_edges,
+                          void *ws, size_t ws_bytes, void *stream);
+
 /* Workspace bytes for tiga_mp_csr_bwd (0 on error). */
 size_t tiga_mp_csr_bwd_workspace(const tiga_csr *rel, int32_t feat, int reducer);
 

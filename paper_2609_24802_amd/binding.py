@@ -69,6 +69,9 @@ _SIGS = {
     "tiga_mp_dense_workspace": (C.c_size_t, [C.c_int64]),
     "tiga_mp_dense_fwd": (C.c_int, [C.c_int64, C.c_void_p, C.c_void_p, C.c_float, C.c_int, C.c_void_p,
                                     C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tiga_mp_csr_fwd_paged_workspace": (C.c_size_t, [C.c_int32, C.c_int, C.c_int64]),
+    "tiga_mp_csr_fwd_paged": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_int, C.c_void_p, C.c_int, C.c_void_p,
+                                        C.c_void_p, C.c_int64, C.c_void_p, C.c_size_t, C.c_void_p]),
     "tiga_mp_edgenn_workspace": (C.c_size_t, [C.c_int64, C.c_int32, C.c_int32, C.c_int32]),
     "tiga_mp_edgenn_fwd": (C.c_int, [C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_float,
                                      C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
@@ -194,6 +197,53 @@ def tiga_mp_csr_fwd(rel: Csr, x: torch.Tensor, w: torch.Tensor | None = None, re
         ws = _workspace(need, x.device)
     _check(lib.tiga_mp_csr_fwd(rel.ref, feat, _ptr(x), msg, _ptr(w), reducer, _ptr(y), _ptr(argmax),
                                _ptr(ws), ws.numel(), _stream()))
+    return y, argmax
+
+
+def _host(t, dtype, name, n=None):
+    if not isinstance(t, torch.Tensor) or t.is_cuda:
+        raise TypeError(f"{name} must be a host (CPU) tensor")
+    if t.dtype != dtype or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous {dtype} host tensor")
+    if n is not None and t.numel() != n:
+        raise ValueError(f"{name} has {t.numel()} entries, expected {n}")
+    return t
+
+
+class HostCsr:
+    """A destination-major CSR relation kept in host memory (pin it for asynchronous copies)."""
+
+    def __init__(self, row_ptr: torch.Tensor, col_idx: torch.Tensor, num_src: int):
+        self.row_ptr = _host(row_ptr, torch.int64, "row_ptr")
+        self.col_idx = _host(col_idx, torch.int32, "col_idx")
+        self.num_dst = row_ptr.numel() - 1
+        self.num_src = int(num_src)
+        self.num_edges = col_idx.numel()
+        self._c = _Csr(self.num_dst, self.num_src, self.num_edges, self.row_ptr.data_ptr(),
+                       self.col_idx.data_ptr() if self.num_edges else None)
+
+    @property
+    def ref(self):
+        return C.byref(self._c)
+
+
+def tiga_mp_csr_fwd_paged(rel: HostCsr, x: torch.Tensor, w: torch.Tensor | None = None, reducer: int = REDUCE_SUM,
+                          page_edges: int = 1 << 24, ws=None):
+    """tiga_mp_csr_fwd with the relation (and w) in host memory, staged in pages of whole rows with at most
+    page_edges edges; x and the outputs on the device.  Returns (y, argmax or None)."""
+    lib = load()
+    feat = x.shape[1]
+    _dev(x, torch.float32, "x", (rel.num_src, feat))
+    msg = MSG_SRC
+    if w is not None:
+        _host(w, torch.float32, "w", rel.num_edges)
+        msg = MSG_EDGE_SCALED_SRC
+    y = torch.empty(rel.num_dst, feat, dtype=torch.float32, device=x.device)
+    argmax = torch.empty(rel.num_dst, feat, dtype=torch.int32, device=x.device) if reducer == REDUCE_MAX else None
+    if ws is None:
+        ws = _workspace(lib.tiga_mp_csr_fwd_paged_workspace(feat, reducer, int(page_edges)), x.device)
+    _check(lib.tiga_mp_csr_fwd_paged(rel.ref, feat, _ptr(x), msg, _ptr(w), reducer, _ptr(y), _ptr(argmax),
+                                     int(page_edges), _ptr(ws), ws.numel(), _stream()))
     return y, argmax
 
 

@@ -53,6 +53,41 @@ int check_common(const tiga_csr *rel, int32_t feat, int msg, const float *w_edge
 
 extern "C" {
 
+size_t tiga_mp_csr_fwd_paged_workspace(int32_t feat, int reducer, int64_t page_edges) {
+    if (feat < 1 || page_edges < 1 || page_edges > INT32_MAX) return 0;
+    if (reducer != TIGA_REDUCE_SUM && reducer != TIGA_REDUCE_MAX) return 0;
+    return paged_ws_bytes(page_edges, feat, reducer == TIGA_REDUCE_MAX);
+}
+
+int tiga_mp_csr_fwd_paged(const tiga_csr *rel_host, int32_t feat, const float *x_src, int msg, const float *w_host,
+                          int reducer, float *y, int32_t *argmax, int64_t page_edges, void *ws, size_t ws_bytes,
+                          void *stream) {
+    EntryScope scope;
+    if (int rc = check_common(rel_host, feat, msg, w_host, reducer)) return rc;
+    if (page_edges < 1 || page_edges > INT32_MAX) return fail(TIGA_EINVAL, "page_edges must be in [1, 2^31)");
+    if (rel_host->num_dst == 0) return TIGA_OK;
+    if (!y) return fail(TIGA_EINVAL, "y is NULL");
+    if (rel_host->num_edges > 0 && !x_src) return fail(TIGA_EINVAL, "x_src is NULL");
+    if (reducer == TIGA_REDUCE_MAX && !argmax) return fail(TIGA_EINVAL, "argmax is required for the max reducer");
+    if (reducer == TIGA_REDUCE_SUM && argmax) return fail(TIGA_EINVAL, "argmax must be NULL for the sum reducer");
+    // host-side metadata checks: the relation's ends, and no row longer than a page
+    const int64_t *rp = rel_host->row_ptr;
+    if (rp[0] != 0 || rp[rel_host->num_dst] != rel_host->num_edges)
+        return fail(TIGA_EGRAPH, "row_ptr must start at 0 and end at num_edges");
+    for (int64_t i = 0; i < rel_host->num_dst; ++i) {
+        const int64_t d = rp[i + 1] - rp[i];
+        if (d < 0) return fail(TIGA_EGRAPH, "row_ptr decreases at row %lld", (long long)i);
+        if (d > page_edges)
+            return fail(TIGA_EUNSUPPORTED, "row %lld has %lld edges, more than page_edges %lld", (long long)i,
+                        (long long)d, (long long)page_edges);
+    }
+    const size_t need = paged_ws_bytes(page_edges, feat, reducer == TIGA_REDUCE_MAX);
+    if (int rc = check_ws(ws, ws_bytes, need)) return rc;
+    return launch_paged_fwd(rel_host, feat, x_src, msg == TIGA_MSG_EDGE_SCALED_SRC ? w_host : nullptr,
+                            reducer == TIGA_REDUCE_MAX ? RED_MAX : RED_SUM, y, argmax, page_edges, ws,
+                            static_cast<hipStream_t>(stream));
+}
+
 size_t tiga_mp_csr_fwd_workspace(const tiga_csr *rel, int32_t feat, int reducer) {
     if (!rel || feat < 1 || rel->num_dst < 0 || rel->num_edges < 0) return 0;
     if (reducer != TIGA_REDUCE_SUM && reducer != TIGA_REDUCE_MAX) return 0;

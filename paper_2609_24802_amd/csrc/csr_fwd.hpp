@@ -32,5 +32,11 @@ struct EdgeGrad {
 int launch_traversal(const Trav &t, int64_t table_rows, int64_t nedges, const Layout &lay, int red, int wm, void *ws,
                      float *out, int32_t *out_arg, hipStream_t stream, const EdgeGrad &eg = EdgeGrad{});
 
+// Paged forward: rel's row_ptr and col_idx and w_host live in host memory; pages of whole rows
+// with at most page_edges edges are staged through the workspace (see csr_paged.hip).
+size_t paged_ws_bytes(int64_t page_edges, int64_t feat, bool with_arg);
+int launch_paged_fwd(const tiga_csr *rel, int32_t feat, const float *x_src, const float *w_host, int red, float *y,
+                     int32_t *argmax, int64_t page_edges, void *ws, hipStream_t stream);
+
 }  // namespace csr
 }  // namespace tiga

@@ -185,3 +185,27 @@ def test_edgenn_errors(clib):
     assert clib.tiga_mp_edgenn_bwd(100, 8, 32, 3, f, f, 0.1, f, f, f, f, None, f, f, f, f, f, f, f, big,
                                    None) == b.TIGA_EINVAL   # dy is required
     assert clib.tiga_mp_edgenn_workspace(1000, 8, 32, 3) < clib.tiga_mp_edgenn_workspace(100000, 8, 32, 3)
+
+
+def test_csr_paged_host_checks(clib):
+    """The paged forward reads row_ptr on the host: bad metadata and too-long rows are rejected there."""
+    import numpy as np
+    from paper_2609_24802_amd import binding as b
+    from paper_2609_24802_amd.binding import _Csr
+    fake = C.c_void_p(0x10000)
+    rp = np.array([0, 3, 3, 10], np.int64)
+    col = np.zeros(10, np.int32)
+    rel = _Csr(3, 5, 10, rp.ctypes.data, col.ctypes.data)
+    need = clib.tiga_mp_csr_fwd_paged_workspace(4, b.REDUCE_SUM, 8)
+    assert need > 0
+    rc = clib.tiga_mp_csr_fwd_paged(C.byref(rel), 4, fake, b.MSG_SRC, None, b.REDUCE_SUM, fake, None, 4, fake,
+                                    1 << 40, None)
+    assert rc == b.TIGA_EUNSUPPORTED and b"more than page_edges" in clib.tiga_last_error()
+    bad = np.array([0, 3, 2, 10], np.int64)
+    rel_bad = _Csr(3, 5, 10, bad.ctypes.data, col.ctypes.data)
+    rc = clib.tiga_mp_csr_fwd_paged(C.byref(rel_bad), 4, fake, b.MSG_SRC, None, b.REDUCE_SUM, fake, None, 16, fake,
+                                    1 << 40, None)
+    assert rc == b.TIGA_EGRAPH
+    rc = clib.tiga_mp_csr_fwd_paged(C.byref(rel), 4, fake, b.MSG_SRC, None, b.REDUCE_SUM, fake, None, 0, fake,
+                                    1 << 40, None)
+    assert rc == b.TIGA_EINVAL
