@@ -67,6 +67,8 @@ PROFILE_MD = os.path.join(ROOT, "profiles", "gather_reduce_csr_powerlaw_1b_f16.m
 VALU_LANE_OPS_PER_S = 256 * 4 * 16 * 2.4e9  # CUs * SIMDs * lanes per cycle * clock
 VALU_INSTR_PER_PAIR = 12
 MFMA16_PEAK_TFLOPS = 2500.0  # dense fp16 / bf16 MFMA peak
+# edges per page of the paged CSR forward on the headline graph
+PAGE_EDGES = 1 << 26
 # input widths of the edge-MLP workload (the first is profiled)
 EDGENN_FEATS = [8, 32]
 # exact kNN workload sizes (the largest is profiled)
@@ -265,10 +267,31 @@ def headline(args, torch, tb, synth, oracle):
     out = dict(E=E, n=n, F=F, step_ms=r["step_ms"], kernel_ms=kernel_ms, bytes_alg=bytes_alg,
                achieved=achieved, parity_ok=parity_ok, kernel_ms_all=r["kernel_ms"])
 
+    if not args.no_paths:
+        # the paged forward on the same graph: relation and weights in pinned host memory, staged in
+        # pages of whole rows through a bounded device workspace (x and y stay resident)
+        del rel, wd, ws
+        torch.cuda.empty_cache()
+        t = time.time()
+        rel_h = tb.HostCsr(torch.from_numpy(rp).pin_memory(), torch.from_numpy(col).pin_memory(), n)
+        w_h = torch.from_numpy(w).pin_memory()
+        log(f"relation pinned in host memory in {time.time() - t:.1f} s")
+        wsp = tb._workspace(tb.load().tiga_mp_csr_fwd_paged_workspace(F, tb.REDUCE_SUM, PAGE_EDGES), xd.device)
+        yp = {}
+        rp_ = time_steps(torch, tb, lambda: yp.update(y=tb.tiga_mp_csr_fwd_paged(
+            rel_h, xd, w_h, page_edges=PAGE_EDGES, ws=wsp)[0]), 2, 1)
+        copied = E * 8 + (n + 1) * 8 + (E // PAGE_EDGES + 1) * 8
+        out["paged"] = dict(ms=rp_["step_ms"], gedges_per_s=E / rp_["step_ms"] / 1e6, page_edges=PAGE_EDGES,
+                            device_ws_bytes=int(wsp.numel()), host_to_device_gbs=copied / rp_["step_ms"] / 1e6,
+                            equal_to_resident=bool(torch.equal(yp["y"], y)))
+        log(f"paged: {rp_['step_ms']:.1f} ms, equal to resident: {out['paged']['equal_to_resident']}")
+        del rel_h, w_h, wsp, yp
+    else:
+        del rel, wd, ws
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(args, oracle, rp, col, x, w)
-    del rel, xd, wd, y, ws
+    del xd, y
     torch.cuda.empty_cache()
     return out, cpu
 
@@ -543,6 +566,8 @@ def main():
     ceil = None if args.no_ceilings else ceilings()
     h, cpu = headline(args, torch, tb, synth, oracle)
     extra = {} if args.no_paths else paths(args, torch, tb, synth)
+    if "paged" in h:
+        extra[f"csr_paged_host_relation_{h['n']}n_{h['E']}e_f{h['F']}"] = h["paged"]
     value = h["E"] / (h["step_ms"] * 1e-3) / 1e9
     line = {
         "metric": "GEdges/s fused fwd(+bwd) and achieved HBM GB/s vs peak, 1 MI355X",
