@@ -70,7 +70,7 @@ __global__ __launch_bounds__(kBlock) void bbox_partial_kernel(const float *__res
 // One block: reduce the per-block boxes, then thread 0 picks the cell size and
 // the grid dimensions.
 __global__ __launch_bounds__(kBlock) void grid_params_kernel(const float *__restrict__ part, int nblocks, int64_t n,
-                                                             float radius, int64_t max_cells,
+                                                             float radius, int64_t max_cells, double spacing_scale,
                                                              Params *__restrict__ prm) {
     float mn[3] = {__builtin_inff(), __builtin_inff(), __builtin_inff()};
     float mx[3] = {-__builtin_inff(), -__builtin_inff(), -__builtin_inff()};
@@ -114,7 +114,7 @@ __global__ __launch_bounds__(kBlock) void grid_params_kernel(const float *__rest
     // fp32 rounding of the predicate), and not much smaller than the mean
     // point spacing; grown until the directory has at most max_cells cells
     double h = static_cast<double>(radius) * (1.0 + 1.0 / 1024.0);
-    const double spacing = cbrt(vol / static_cast<double>(n > 0 ? n : 1));
+    const double spacing = spacing_scale * cbrt(vol / static_cast<double>(n > 0 ? n : 1));
     if (spacing > h) h = spacing;
     int64_t d[3] = {1, 1, 1};
     bool fits = false;
@@ -644,9 +644,12 @@ struct Ws {
     int bbox_blocks;
 };
 
-Ws carve(Carve &c, int64_t n) {
+// cells_per_point bounds the directory (max_cells = cells_per_point * n + 64): 1 for volume
+// clouds; more for callers whose points lie on surfaces, where the volume-based spacing floor
+// overestimates the point spacing.
+Ws carve(Carve &c, int64_t n, int64_t cells_per_point = 1) {
     Ws w;
-    w.max_cells = n + 64;
+    w.max_cells = cells_per_point * n + 64;
     w.bbox_blocks = 1024;
     w.prm = c.take<Params>(1);
     w.bbox = c.take<float>(6 * w.bbox_blocks);
@@ -667,14 +670,14 @@ int blocks_for(int64_t n) {
 }
 
 // Build the cell directory and the cell-ordered records.
-int build(int64_t n, const float *pos, float radius, Ws &w, hipStream_t stream) {
+int build(int64_t n, const float *pos, float radius, Ws &w, hipStream_t stream, double spacing_scale = 1.0) {
     int nb = w.bbox_blocks;
     const int64_t need = ceil_div(n, kBlock);
     if (need < nb) nb = static_cast<int>(need);
     hipLaunchKernelGGL(bbox_partial_kernel, dim3(nb), dim3(kBlock), 0, stream, pos, n, w.bbox);
     if (int rc = check_launch("radius bbox")) return rc;
     hipLaunchKernelGGL(grid_params_kernel, dim3(1), dim3(kBlock), 0, stream, w.bbox, nb, n, radius, w.max_cells,
-                       w.prm);
+                       spacing_scale, w.prm);
     if (int rc = check_launch("radius grid")) return rc;
     // cell-ordered positions: a stable sort by cell keeps ascending point ids
     // within a cell, so every candidate order depends only on the input
@@ -799,16 +802,21 @@ int backward(int64_t n, int32_t feat, const float *pos, const float *x, float ra
 #undef TIGA_B
 }
 
+// The shared directory (edge-MLP messages): up to 8 cells per point and half the volume-based
+// spacing floor, so that surface clouds get cells near the radius.
+constexpr int64_t kSharedCellsPerPoint = 8;
+constexpr double kSharedSpacingScale = 0.5;
+
 size_t cells_ws_bytes(int64_t n) {
     Carve c(nullptr);
-    carve(c, n);
+    carve(c, n, kSharedCellsPerPoint);
     return c.bytes();
 }
 
 int build_cells(int64_t n, const float *pos, float radius, void *ws, Cells &out, hipStream_t stream) {
     Carve c(ws);
-    Ws w = carve(c, n);
-    if (int rc = build(n, pos, radius, w, stream)) return rc;
+    Ws w = carve(c, n, kSharedCellsPerPoint);
+    if (int rc = build(n, pos, radius, w, stream, kSharedSpacingScale)) return rc;
     out.prm = w.prm;
     out.start = w.start;
     out.rec = w.rec;
