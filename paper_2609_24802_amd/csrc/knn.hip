@@ -311,20 +311,27 @@ __global__ __launch_bounds__(kSplit * kWave) void select_kernel(const f4 *__rest
         const uint64_t cap = (static_cast<uint64_t>(__float_as_uint(tight)) << 32) | 0xffffffffull;
         bool changed = false;
         for (int c0 = 0; c0 < kTile; c0 += 8) {
-            uint64_t nk[8];
+            float d2[8];
             bool any = false;
-            const uint64_t lim = kd[KP - 1] < cap ? kd[KP - 1] : cap;
+            // a distance above the lane's tight bound cannot enter (ties go on to the key test)
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
-                const f4 cj = tr[c0 + u];   // uniform address: a scalar load
-                const uint32_t cid = static_cast<uint32_t>(__float_as_int(cj.w));
-                const float d2 = sqdist(me, cj);
-                nk[u] = (static_cast<uint64_t>(__float_as_uint(d2)) << 32) | cid;
+                d2[u] = sqdist(me, tr[c0 + u]);   // uniform address: a scalar load
+                any |= d2[u] <= tight;
+            }
+            if (!__any(any)) continue;
+            const uint64_t lim = kd[KP - 1] < cap ? kd[KP - 1] : cap;
+            uint64_t nk[8];
+            bool take = false;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const uint32_t cid = static_cast<uint32_t>(__float_as_int(tr[c0 + u].w));
+                nk[u] = (static_cast<uint64_t>(__float_as_uint(d2[u])) << 32) | cid;
                 if (t == qt) nk[u] = static_cast<int>(cid) == qid ? ~0ull : nk[u];   // the query itself
                 nk[u] = nk[u] < lim ? nk[u] : ~0ull;
-                any |= nk[u] != ~0ull;
+                take |= nk[u] != ~0ull;
             }
-            if (__any(any)) {
+            if (__any(take)) {
                 changed = true;
 #pragma unroll
                 for (int u = 0; u < 8; ++u)
