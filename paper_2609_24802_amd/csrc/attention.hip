@@ -79,17 +79,16 @@ struct BF16 {
 
 template <int D>
 struct Geo {
-    static constexpr int KS = D + 8;                     // K row stride in LDS (16-bit units)
-    static constexpr int VS = kBN + 4;                   // V^T row stride in LDS
+    static constexpr int CPR = D / 8;                    // 16-byte chunks per row
+    static constexpr int RB = 2 * D;                     // bytes per row
+    static constexpr int R = 256 / RB;                   // rows per 256-byte bank window (1 or 2)
+    static constexpr int NB = D / 16;                    // 32-byte blocks per row
     static constexpr int CH = D / 32;                    // 32-deep chunks of the score product
     static constexpr int DB = D / 16;                    // 16-wide blocks of the output
-    static constexpr int RPT = kBN * D / 8 / kThreads;   // 16-byte K chunks per thread per tile
-    static constexpr int CPR = D / 8;                    // 16-byte chunks per row
-    static constexpr int KPT = kBN / (kThreads / CPR);   // V keys per thread per tile
-    static constexpr int NKG = kBN / KPT;                // V key groups per tile
-    static_assert(RPT >= 1 && KPT >= 1 && (KPT == 2 || KPT == 4), "tile shape");
-    static constexpr int LDS_K = kBN * KS;               // per buffer, 16-bit units
-    static constexpr int LDS_V = D * VS;
+    static constexpr int TILE = kBN * RB;                // bytes of one K or V tile in LDS
+    static constexpr int LPW = TILE / 1024 / kWaves;     // 1-KB direct loads per wavefront, tile and operand
+    static_assert(LPW >= 1 && TILE % (1024 * kWaves) == 0, "tile shape");
+    static constexpr int LDS = 4 * TILE;                 // two buffers of (K, V)
 };
 
 // Maximum over the four lanes l, l^16, l^32, l^48 (the lanes that share a query column), with
@@ -102,69 +101,64 @@ __device__ __forceinline__ float max_over_column(float v) {
     return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
-__device__ __forceinline__ uint32_t lo16(uint32_t a, uint32_t b) { return (a & 0xffffu) | (b << 16); }
-__device__ __forceinline__ uint32_t hi16(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
-
-__device__ __forceinline__ uint32_t word(const u4 &v, int i) { return v[i]; }
-
-// Tile staging: global loads into registers (kr: K rows, vr: V rows), then stores into one LDS
-// buffer (K row-major, V transposed).
+// LDS layouts (no padding; XOR swizzles keep the operand reads free of bank conflicts):
+//  - K tile, row-major (key, width): the 16-byte chunk c of key row k sits at chunk
+//    c ^ ((k / R) % CPR).  The score product reads 16 consecutive keys at one chunk, which then
+//    fall into 16 distinct 16-byte bank groups of a 256-byte window.
+//  - V tile, row-major (key, width): the 32-byte block b of key row k sits at block
+//    b ^ ((k / R) % NB).  The transposing read of the value product takes 4 consecutive keys x
+//    16 widths per 16 lanes, 8 keys per half wavefront: 8 distinct 32-byte bank groups.
+// Both are filled by direct global -> LDS loads: lane t of a load writes bytes [16 t, 16 t + 16)
+// of a 1-KB LDS run, so each lane fetches the global chunk whose swizzled place that is.
 template <int D>
-__device__ __forceinline__ void stage_load(u4 (&kr)[Geo<D>::RPT], u4 (&vr)[Geo<D>::KPT],
-                                           const u4 *__restrict__ kh, const u4 *__restrict__ vh, int64_t k0,
-                                           int64_t n, int tid) {
+__device__ __forceinline__ int k_chunk(int k, int pc) { using G = Geo<D>; return pc ^ ((k / G::R) % G::CPR); }
+template <int D>
+__device__ __forceinline__ int v_chunk(int k, int pc) {
     using G = Geo<D>;
-    // one uniform tile base and per-thread 32-bit offsets
+    return (((pc >> 1) ^ ((k / G::R) % G::NB)) << 1) | (pc & 1);
+}
+
+// 16 bytes per lane from global memory straight into LDS: lane t writes bytes [16 t, 16 t + 16)
+// of the 1-KB run at `run` (a wavefront-uniform LDS address).
+__device__ __forceinline__ void lds_load16(const void *src, uint8_t *run) {
+    __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)run, 16, 0, 0);
+}
+
+// gfx950 transposing LDS read of 16-bit data: within each group of 16 lanes, lane i receives, in
+// slot j, element i % 4 of the 8 bytes addressed by lane 4 j + i / 4 of its group.
+__device__ __forceinline__ u2 lds_read_tr16(const uint8_t *p) {
+    typedef short s4 __attribute__((ext_vector_type(4)));
+    return __builtin_bit_cast(u2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4 *)p));
+}
+
+// Issue the direct loads of the K and V tile starting at key k0 into one LDS buffer.  ko / vo
+// hold this lane's global chunk offsets (row * CPR + chunk) for a full tile.
+template <int D>
+__device__ __forceinline__ void stage_kv(const u4 *__restrict__ kh, const u4 *__restrict__ vh, int64_t k0, int64_t n,
+                                          const int *ko, const int *vo, uint8_t *kl,
+                                          uint8_t *vl, int w, int lane) {
+    using G = Geo<D>;
     const u4 *kt = kh + k0 * G::CPR;
-    const u4 *vtl = vh + k0 * G::CPR;
-    // consecutive threads take consecutive V key groups, so that one transposed row of the LDS
-    // store is written by neighbouring lanes (contiguous, no bank conflicts)
-    const int kg = tid % G::NKG, dg = tid / G::NKG;
+    const u4 *vt = vh + k0 * G::CPR;
     if (k0 + kBN <= n) {
 #pragma unroll
-        for (int r = 0; r < G::RPT; ++r) kr[r] = kt[tid + r * kThreads];
-#pragma unroll
-        for (int r = 0; r < G::KPT; ++r) vr[r] = vtl[(kg * G::KPT + r) * G::CPR + dg];
+        for (int r = 0; r < G::LPW; ++r) {
+            const int run = (w * G::LPW + r) * 1024;
+            lds_load16(kt + ko[r], kl + run);
+            lds_load16(vt + vo[r], vl + run);
+        }
     } else {
         // keys past n read the last row instead: their scores are masked to -inf, so their
         // weights are exactly 0 and the (finite) row contributes nothing
-        const int last = static_cast<int>(n - 1 - k0);     // tile-relative index of key n-1
+        const int last = static_cast<int>(n - 1 - k0);
 #pragma unroll
-        for (int r = 0; r < G::RPT; ++r) {
-            const int idx = tid + r * kThreads;
-            const int key = idx / G::CPR < last ? idx / G::CPR : last;
-            kr[r] = kt[key * G::CPR + idx % G::CPR];
-        }
-#pragma unroll
-        for (int r = 0; r < G::KPT; ++r) {
-            const int key = kg * G::KPT + r < last ? kg * G::KPT + r : last;
-            vr[r] = vtl[key * G::CPR + dg];
-        }
-    }
-}
-
-template <int D>
-__device__ __forceinline__ void stage_store(const u4 (&kr)[Geo<D>::RPT], const u4 (&vr)[Geo<D>::KPT],
-                                            uint16_t *ks, uint16_t *vt, int tid) {
-    using G = Geo<D>;
-#pragma unroll
-    for (int r = 0; r < G::RPT; ++r) {
-        const int idx = tid + r * kThreads;
-        *reinterpret_cast<u4 *>(ks + (idx / G::CPR) * G::KS + (idx % G::CPR) * 8) = kr[r];
-    }
-    const int kg = tid % G::NKG, dg = tid / G::NKG;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        uint16_t *dst = vt + (dg * 8 + j) * G::VS + kg * G::KPT;
-        const int w = j / 2;
-        if constexpr (G::KPT == 4) {
-            u2 p;
-            p.x = (j & 1) ? hi16(word(vr[0], w), word(vr[1], w)) : lo16(word(vr[0], w), word(vr[1], w));
-            p.y = (j & 1) ? hi16(word(vr[2], w), word(vr[3], w)) : lo16(word(vr[2], w), word(vr[3], w));
-            *reinterpret_cast<u2 *>(dst) = p;
-        } else {
-            *reinterpret_cast<uint32_t *>(dst) =
-                (j & 1) ? hi16(word(vr[0], w), word(vr[1], w)) : lo16(word(vr[0], w), word(vr[1], w));
+        for (int r = 0; r < G::LPW; ++r) {
+            const int run = (w * G::LPW + r) * 1024;
+            const int k = (run + 16 * lane) / G::RB;
+            const int pc = ((run + 16 * lane) % G::RB) / 16;
+            const int key = k < last ? k : last;
+            lds_load16(kt + key * G::CPR + k_chunk<D>(k, pc), kl + run);
+            lds_load16(vt + key * G::CPR + v_chunk<D>(k, pc), vl + run);
         }
     }
 }
@@ -178,12 +172,108 @@ __device__ __forceinline__ void task_of(int ntq, bool causal, int &head, int &qt
     qt = causal ? ntq - 1 - r : r;
 }
 
+template <class T, int D>
+struct State {
+    f4 o[Geo<D>::DB][2];
+    float m[2];
+    f4 l[2];
+};
+
+// One 64-key tile: scores, relation mask, online-softmax update, value and mass products.
+// kb_ / vb_ are this lane's LDS byte addresses for the tile's K and V operands.
+template <class T, int D, bool CAUSAL>
+__device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][Geo<D>::CH], const uint8_t *kl,
+                                          const uint8_t *vl, const int *kr, const int *vr,
+                                          int64_t k0, int64_t n, int64_t qw0, float c, int col, int g, u4 ones) {
+    using G = Geo<D>;
+    // ---- S^T = K Q^T for 4 blocks of 16 keys x 2 blocks of 16 queries
+    f4 s[4][2];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+        for (int qb = 0; qb < 2; ++qb) s[kb][qb] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int ch = 0; ch < G::CH; ++ch) {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            const u4 a = *reinterpret_cast<const u4 *>(kl + kr[ch] + kb * 16 * G::RB);
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb) s[kb][qb] = T::mma(a, qreg[qb][ch], s[kb][qb]);
+        }
+    }
+    // ---- relation: keys past n, and (triangular) keys after the query
+    const bool edge = k0 + kBN > n || (CAUSAL && k0 + kBN - 1 > qw0);
+    if (edge) {
+        const int nk = static_cast<int>(n - k0 < kBN ? n - k0 : kBN);
+        const int qr = static_cast<int>(CAUSAL ? qw0 - k0 : 0) + col;
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+            const int lim = CAUSAL ? (qr + qb * 16 + 1 < nk ? qr + qb * 16 + 1 : nk) : nk;
+            // key kb*16 + 4g + i is admissible iff kb*16 + i < lim - 4g (constants on the left)
+            const int rel = lim - g * 4;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) s[kb][qb][i] = kb * 16 + i < rel ? s[kb][qb][i] : -__builtin_inff();
+        }
+    }
+    // ---- online-softmax state update (Section 4.8), log2 domain
+    u4 pb[2][2];   // [key chunk][query block]: B operands of the second product
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        float mt = s[0][qb][0];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) mt = fmaxf(mt, s[kb][qb][i]);
+        mt = max_over_column(mt);
+        mt *= c;
+        if (__any(mt > st.m[qb] + kLazy)) {
+            const float mn = fmaxf(st.m[qb], mt);
+            const float alpha = __builtin_amdgcn_exp2f(st.m[qb] - mn);
+            st.m[qb] = mn;
+            st.l[qb] *= alpha;
+#pragma unroll
+            for (int db = 0; db < G::DB; ++db) st.o[db][qb] *= alpha;
+        }
+        float p[4][4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) p[kb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][qb][i], c, -st.m[qb]));
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) {
+            pb[kc][qb].x = T::pack(p[2 * kc][0], p[2 * kc][1]);
+            pb[kc][qb].y = T::pack(p[2 * kc][2], p[2 * kc][3]);
+            pb[kc][qb].z = T::pack(p[2 * kc + 1][0], p[2 * kc + 1][1]);
+            pb[kc][qb].w = T::pack(p[2 * kc + 1][2], p[2 * kc + 1][3]);
+        }
+    }
+    // ---- O^T += V^T P^T; the V^T operand comes from the row-major V tile by transposing reads
+    //      (lane r of a 16-lane group receives width r of the four keys its group addresses)
+#pragma unroll
+    for (int db = 0; db < G::DB; ++db) {
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) {
+            const uint8_t *base = vl + vr[db] + kc * 32 * G::RB;
+            const u2 l2 = lds_read_tr16(base);
+            const u2 h2v = lds_read_tr16(base + 16 * G::RB);
+            const u4 a = u4{l2.x, l2.y, h2v.x, h2v.y};
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb) st.o[db][qb] = T::mma(a, pb[kc][qb], st.o[db][qb]);
+        }
+    }
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) st.l[qb] = T::mma(ones, pb[kc][qb], st.l[qb]);
+}
+
 template <class T, int D, bool CAUSAL>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restrict__ q, const u4 *__restrict__ k,
                                                             const u4 *__restrict__ v, int64_t n, int ntq,
                                                             float c, uint16_t *__restrict__ y, float *__restrict__ lse) {
     using G = Geo<D>;
-    __shared__ __attribute__((aligned(16))) uint16_t lds[2 * (G::LDS_K + G::LDS_V)];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[G::LDS];
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int w = uniform(tid / kWave);
@@ -208,140 +298,80 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restr
         for (int ch = 0; ch < G::CH; ++ch) qreg[qb][ch] = qh[row * G::CPR + ch * 4 + g];
     }
 
-    f4 o[G::DB][2];
+    // direct-load chunk offsets of this lane (full tiles)
+    int ko[G::LPW], vo[G::LPW];
+#pragma unroll
+    for (int r = 0; r < G::LPW; ++r) {
+        const int b = (w * G::LPW + r) * 1024 + 16 * lane;
+        const int kk = b / G::RB, pc = (b % G::RB) / 16;
+        ko[r] = kk * G::CPR + k_chunk<D>(kk, pc);
+        vo[r] = kk * G::CPR + v_chunk<D>(kk, pc);
+    }
+    // operand read addresses of this lane within a tile
+    int kr[G::CH], vr[G::DB];
+#pragma unroll
+    for (int ch = 0; ch < G::CH; ++ch) kr[ch] = col * G::RB + 16 * k_chunk<D>(col, ch * 4 + g);
+    {
+        const int s = lane & 15;
+        const int row = 4 * g + s / 4;           // key row of this lane's address (plus 16 / 32 steps)
+        const int sw = (row / G::R) % G::NB;
+#pragma unroll
+        for (int db = 0; db < G::DB; ++db) vr[db] = row * G::RB + 32 * (db ^ sw) + 8 * (s % 4);
+    }
+
+    State<T, D> st;
 #pragma unroll
     for (int db = 0; db < G::DB; ++db)
-        for (int qb = 0; qb < 2; ++qb) o[db][qb] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    float m[2] = {-__builtin_inff(), -__builtin_inff()};
+        for (int qb = 0; qb < 2; ++qb) st.o[db][qb] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    st.m[0] = st.m[1] = -__builtin_inff();
     // mass: an all-ones A operand sums P^T over the keys of a chunk for every query column, so
     // the denominator uses the same rounded weights as the numerator
-    f4 l[2] = {f4{0.0f, 0.0f, 0.0f, 0.0f}, f4{0.0f, 0.0f, 0.0f, 0.0f}};
+    st.l[0] = st.l[1] = f4{0.0f, 0.0f, 0.0f, 0.0f};
     const u4 ones = T::ones();
 
     const int64_t kend = CAUSAL ? (q0 + kBM < n ? q0 + kBM : n) : n;  // keys this block needs
     const int ntk = static_cast<int>((kend + kBN - 1) / kBN);
 
-    u4 kr[G::RPT], vr[G::KPT];
-    stage_load<D>(kr, vr, kh, vh, 0, n, tid);
-    stage_store<D>(kr, vr, lds, lds + 2 * G::LDS_K, tid);
-    __syncthreads();
-
-    for (int kt = 0; kt < ntk; ++kt) {
-        const int buf = kt & 1;
-        const int64_t k0 = static_cast<int64_t>(kt) * kBN;
-        // prefetch the next tile (the last iteration reloads its own tile into the idle buffer)
-        stage_load<D>(kr, vr, kh, vh, kt + 1 < ntk ? k0 + kBN : k0, n, tid);
-
-        const uint16_t *ks = lds + buf * G::LDS_K;
-        const uint16_t *vt = lds + 2 * G::LDS_K + buf * G::LDS_V;
-        // a wavefront whose queries all precede the tile has nothing to add from it
-        if (!CAUSAL || k0 <= qw0 + kQW - 1) {
-            // ---- S^T = K Q^T for 4 blocks of 16 keys x 2 blocks of 16 queries
-            f4 s[4][2];
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-                for (int qb = 0; qb < 2; ++qb) s[kb][qb] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-            for (int ch = 0; ch < G::CH; ++ch) {
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb) {
-                    const u4 a = *reinterpret_cast<const u4 *>(ks + (kb * 16 + col) * G::KS + ch * 32 + g * 8);
-#pragma unroll
-                    for (int qb = 0; qb < 2; ++qb) s[kb][qb] = T::mma(a, qreg[qb][ch], s[kb][qb]);
-                }
-            }
-            // ---- relation: keys past n, and (triangular) keys after the query
-            const bool edge = k0 + kBN > n || (CAUSAL && k0 + kBN - 1 > qw0);
-            if (edge) {
-                // in tile-relative 32-bit units: key kb*16 + 4g + i is admissible iff it is below
-                // nk = n - k0 and (triangular) not after the query at offset qw0 - k0 + 16 qb + col
-                const int nk = static_cast<int>(n - k0 < kBN ? n - k0 : kBN);
-                const int qr = static_cast<int>(CAUSAL ? qw0 - k0 : 0) + col;
-#pragma unroll
-                for (int qb = 0; qb < 2; ++qb) {
-                    const int lim = CAUSAL ? (qr + qb * 16 + 1 < nk ? qr + qb * 16 + 1 : nk) : nk;
-#pragma unroll
-                    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const int kj = kb * 16 + g * 4 + i;
-                            s[kb][qb][i] = kj < lim ? s[kb][qb][i] : -__builtin_inff();
-                        }
-                }
-            }
-            // ---- online-softmax state update (Section 4.8), log2 domain
-            u4 pb[2][2];   // [key chunk][query block]: B operands of the second product
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb) {
-                float mt = s[0][qb][0];
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) mt = fmaxf(mt, s[kb][qb][i]);
-                mt = max_over_column(mt);
-                mt *= c;
-                if (__any(mt > m[qb] + kLazy)) {
-                    const float mn = fmaxf(m[qb], mt);
-                    const float alpha = __builtin_amdgcn_exp2f(m[qb] - mn);
-                    m[qb] = mn;
-                    l[qb] *= alpha;
-#pragma unroll
-                    for (int db = 0; db < G::DB; ++db) o[db][qb] *= alpha;
-                }
-                float p[4][4];
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        p[kb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][qb][i], c, -m[qb]));
-                    }
-#pragma unroll
-                for (int kc = 0; kc < 2; ++kc) {
-                    pb[kc][qb].x = T::pack(p[2 * kc][0], p[2 * kc][1]);
-                    pb[kc][qb].y = T::pack(p[2 * kc][2], p[2 * kc][3]);
-                    pb[kc][qb].z = T::pack(p[2 * kc + 1][0], p[2 * kc + 1][1]);
-                    pb[kc][qb].w = T::pack(p[2 * kc + 1][2], p[2 * kc + 1][3]);
-                }
-            }
-            // ---- O^T += V^T P^T
-#pragma unroll
-            for (int db = 0; db < G::DB; ++db) {
-#pragma unroll
-                for (int kc = 0; kc < 2; ++kc) {
-                    const uint16_t *row = vt + (db * 16 + col) * G::VS + kc * 32 + g * 4;
-                    const u2 lo = *reinterpret_cast<const u2 *>(row);
-                    const u2 hi = *reinterpret_cast<const u2 *>(row + 16);
-                    const u4 a = u4{lo.x, lo.y, hi.x, hi.y};
-#pragma unroll
-                    for (int qb = 0; qb < 2; ++qb) o[db][qb] = T::mma(a, pb[kc][qb], o[db][qb]);
-                }
-            }
-#pragma unroll
-            for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-                for (int qb = 0; qb < 2; ++qb) l[qb] = T::mma(ones, pb[kc][qb], l[qb]);
-        }
-        stage_store<D>(kr, vr, lds + (buf ^ 1) * G::LDS_K, lds + 2 * G::LDS_K + (buf ^ 1) * G::LDS_V, tid);
+    // last key any query of this wavefront admits (dense: every key; kept as a run-time bound in
+    // both cases, which also keeps the two relations on one instruction schedule)
+    const int64_t klast = CAUSAL ? qw0 + kQW - 1 : n;
+    uint8_t *const l0 = lds;
+    uint8_t *const l1 = lds + 2 * G::TILE;
+    stage_kv<D>(kh, vh, 0, n, ko, vo, l0, l0 + G::TILE, w, lane);
+    for (int kt = 0; kt < ntk; kt += 2) {
+        // buffer 0 holds tile kt; prefetch tile kt + 1 into buffer 1
+        __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
+        const int64_t k0 = static_cast<int64_t>(kt) * kBN;
+        if (kt + 1 < ntk) stage_kv<D>(kh, vh, k0 + kBN, n, ko, vo, l1, l1 + G::TILE, w, lane);
+        // a wavefront whose queries all precede the tile has nothing to add from it
+        if (k0 <= klast)
+            tile_step<T, D, CAUSAL>(st, qreg, l0, l0 + G::TILE, kr, vr, k0, n, qw0, c, col, g, ones);
+        if (kt + 1 >= ntk) break;
+        __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (kt + 2 < ntk) stage_kv<D>(kh, vh, k0 + 2 * kBN, n, ko, vo, l0, l0 + G::TILE, w, lane);
+        if (k0 + kBN <= klast)
+            tile_step<T, D, CAUSAL>(st, qreg, l1, l1 + G::TILE, kr, vr, k0 + kBN, n, qw0, c, col, g, ones);
     }
 
     // ---- finalize: total mass over the four lanes of a query, divide, store
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-        const float lt = l[qb][0];          // every row of the mass block holds the full sum
+        const float lt = st.l[qb][0];       // every row of the mass block holds the full sum
         const float inv = 1.0f / lt;
         const int64_t qi = qw0 + qb * 16 + col;
         if (qi < n) {
             uint16_t *yr = y + (hb + qi) * D;
 #pragma unroll
             for (int db = 0; db < G::DB; ++db) {
-                const f4 r = o[db][qb] * inv;
+                const f4 r = st.o[db][qb] * inv;
                 u2 out;
                 out.x = T::pack(r[0], r[1]);
                 out.y = T::pack(r[2], r[3]);
                 *reinterpret_cast<u2 *>(yr + db * 16 + g * 4) = out;
             }
-            if (lse && g == 0) lse[hb + qi] = (m[qb] + __log2f(lt)) * kLn2;
+            if (lse && g == 0) lse[hb + qi] = (st.m[qb] + __log2f(lt)) * kLn2;
         }
     }
 }
