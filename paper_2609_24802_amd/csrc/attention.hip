@@ -8,13 +8,11 @@
 //
 // MI355X design (gfx950, MFMA 16x16x32 with fp32 accumulation):
 //  - A block of 4 wavefronts owns 128 consecutive queries of one head (32 per wavefront) and
-//    streams the keys in tiles of 64 through LDS, double-buffered with one barrier per tile.  K is
-//    stored row-major (key, width); V is stored transposed (width, key) as it is written, so both
-//    products read 8- or 16-byte runs.
+//    streams the keys in tiles of 64 through LDS, double-buffered with one barrier per tile.
 //  - Scores are formed transposed, S^T = K Q^T (A = K from LDS, B = Q^T held in registers), so a
-//    lane's scores all belong to one query (column = lane % 16).  The running maximum, mass and
-//    rescale are then lane-local except for one cross-lane max per tile over the four lanes that
-//    share a query.
+//    lane's scores all belong to one query (column = lane % 16).  The reference point, mass and
+//    rescale are then lane-local; only the exact path's column maximum crosses lanes (the four
+//    lanes that share a query).
 //  - The exponentiated scores feed the second product O^T += V^T P^T straight from the
 //    accumulator registers: a lane of the S^T accumulator holds keys 4g..4g+3 (g = lane / 16) of a
 //    16-key block, and the B operand of a 32-deep MFMA wants 8 keys per lane.  The key slots
@@ -24,10 +22,17 @@
 //  - The mass l is summed by the matrix core too: an all-ones A operand against the weights'
 //    B operand gives, in every row, the sum over the chunk's keys for each query, from the same
 //    rounded weights as the numerator (so y is an exactly normalized combination of the values).
-//  - Scores are kept in the log2 domain (scale * log2 e folded into one multiply-add), and the
-//    accumulator is rescaled only when a tile raises some query's maximum by more than 8 (a
-//    factor 256): any reference point m gives the same y = sum 2^(t - m) v / sum 2^(t - m), and
-//    2^(t - m) <= 256 stays far inside the range of the weights' 16-bit type.
+//  - Scores are kept in the log2 domain (scale * log2 e folded into one multiply-add).  Any
+//    reference point m gives the same y = sum 2^(t - m) v / sum 2^(t - m), so m is moved only
+//    when it must be: each tile's weights are formed against the current m and the tile's mass
+//    (from the matrix core) is checked; while it stays at most 2^12 for every query, every weight
+//    is at most 2^12, far inside the range of the weights' 16-bit type, and no maximum is taken.
+//    Otherwise (and always on the first tile, where m = -inf) the tile takes the exact path:
+//    column maximum, rescale of the accumulator and the mass, weights formed again.
+//  - K and V tiles go from global memory straight into LDS (16-byte direct loads, no staging
+//    registers), in unpadded rows with XOR swizzles that keep the operand reads free of bank
+//    conflicts; the V^T operand is read from the row-major V tile by the gfx950 transposing
+//    LDS read, so V is never transposed by the VALU.
 //  - Causal blocks are scheduled heaviest first, and each XCD takes a contiguous range of
 //    (head, query tile) tasks, so the K/V tiles of a head are shared in that XCD's L2.
 #include "attention.hpp"
@@ -42,7 +47,7 @@ constexpr int kThreads = kWaves * kWave;
 constexpr int kQW = 32;                // queries per wavefront
 constexpr int kBM = kWaves * kQW;      // queries per block
 constexpr int kBN = 64;                // keys per tile
-constexpr float kLazy = 8.0f;          // rescale threshold in the log2 domain
+constexpr float kMassCap = 4096.0f;    // largest tile mass (and so weight) of the fast path
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -179,6 +184,19 @@ struct State {
     f4 l[2];
 };
 
+// Weights 2^(c s - m) of query block qb, packed as the B operands of the value product: key
+// chunk 0 takes keys {4g..4g+3, 16+4g..16+4g+3}, chunk 1 the same keys plus 32.
+template <class T>
+__device__ __forceinline__ void weights(const f4 (&s)[4][2], int qb, float c, float m, u4 &p0, u4 &p1) {
+    float p[4][4];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) p[kb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][qb][i], c, -m));
+    p0 = u4{T::pack(p[0][0], p[0][1]), T::pack(p[0][2], p[0][3]), T::pack(p[1][0], p[1][1]), T::pack(p[1][2], p[1][3])};
+    p1 = u4{T::pack(p[2][0], p[2][1]), T::pack(p[2][2], p[2][3]), T::pack(p[3][0], p[3][1]), T::pack(p[3][2], p[3][3])};
+}
+
 // One 64-key tile: scores, relation mask, online-softmax update, value and mass products.
 // kb_ / vb_ are this lane's LDS byte addresses for the tile's K and V operands.
 template <class T, int D, bool CAUSAL>
@@ -216,38 +234,43 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
                 for (int i = 0; i < 4; ++i) s[kb][qb][i] = kb * 16 + i < rel ? s[kb][qb][i] : -__builtin_inff();
         }
     }
-    // ---- online-softmax state update (Section 4.8), log2 domain
+    // ---- online-softmax state update (Section 4.8), log2 domain.
+    // Fast path: the weights are formed against the current reference point m and the mass of
+    // the tile (an MFMA against an all-ones operand) is checked: a tile mass of at most 2^12 for
+    // every query bounds every weight by 2^12, far inside the 16-bit range.  A larger, infinite
+    // or NaN mass (the first tile, where m = -inf, always) sends the wavefront to the exact path,
+    // which takes the tile's column maximum, rescales (o, l) to the new reference point and forms
+    // the weights again before any value product uses them.
     u4 pb[2][2];   // [key chunk][query block]: B operands of the second product
+    f4 ln[2];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-        float mt = s[0][qb][0];
+        weights<T>(s, qb, c, st.m[qb], pb[0][qb], pb[1][qb]);
+        ln[qb] = T::mma(ones, pb[1][qb], T::mma(ones, pb[0][qb], st.l[qb]));
+    }
+    const bool fast = ln[0][0] - st.l[0][0] <= kMassCap && ln[1][0] - st.l[1][0] <= kMassCap;
+    if (!__all(fast)) {
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+        for (int qb = 0; qb < 2; ++qb) {
+            float mt = s[0][qb][0];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) mt = fmaxf(mt, s[kb][qb][i]);
-        mt = max_over_column(mt);
-        mt *= c;
-        if (__any(mt > st.m[qb] + kLazy)) {
-            const float mn = fmaxf(st.m[qb], mt);
-            const float alpha = __builtin_amdgcn_exp2f(st.m[qb] - mn);
-            st.m[qb] = mn;
-            st.l[qb] *= alpha;
+            for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-            for (int db = 0; db < G::DB; ++db) st.o[db][qb] *= alpha;
-        }
-        float p[4][4];
+                for (int i = 0; i < 4; ++i) mt = fmaxf(mt, s[kb][qb][i]);
+            mt = max_over_column(mt) * c;
+            if (mt > st.m[qb]) {
+                const float alpha = __builtin_amdgcn_exp2f(st.m[qb] - mt);
+                st.m[qb] = mt;
+                st.l[qb] *= alpha;
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) p[kb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][qb][i], c, -st.m[qb]));
-#pragma unroll
-        for (int kc = 0; kc < 2; ++kc) {
-            pb[kc][qb].x = T::pack(p[2 * kc][0], p[2 * kc][1]);
-            pb[kc][qb].y = T::pack(p[2 * kc][2], p[2 * kc][3]);
-            pb[kc][qb].z = T::pack(p[2 * kc + 1][0], p[2 * kc + 1][1]);
-            pb[kc][qb].w = T::pack(p[2 * kc + 1][2], p[2 * kc + 1][3]);
+                for (int db = 0; db < G::DB; ++db) st.o[db][qb] *= alpha;
+            }
+            weights<T>(s, qb, c, st.m[qb], pb[0][qb], pb[1][qb]);
+            ln[qb] = T::mma(ones, pb[1][qb], T::mma(ones, pb[0][qb], st.l[qb]));
         }
     }
+    st.l[0] = ln[0];
+    st.l[1] = ln[1];
     // ---- O^T += V^T P^T; the V^T operand comes from the row-major V tile by transposing reads
     //      (lane r of a 16-lane group receives width r of the four keys its group addresses)
 #pragma unroll
@@ -262,10 +285,6 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
             for (int qb = 0; qb < 2; ++qb) st.o[db][qb] = T::mma(a, pb[kc][qb], st.o[db][qb]);
         }
     }
-#pragma unroll
-    for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) st.l[qb] = T::mma(ones, pb[kc][qb], st.l[qb]);
 }
 
 template <class T, int D, bool CAUSAL>

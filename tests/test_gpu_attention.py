@@ -117,6 +117,25 @@ def test_rising_maximum_rescales(lib, dtype):
         compare(lib, inp, rel, what=f"rising {dtype} {rel}")
 
 
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_tile_mass_above_cap(lib, dtype):
+    """Every key of the second 64-key tile scores about 7 (log2 units) above the first tile's
+    maximum: no single weight leaves the 16-bit range, but the tile's mass (about 64 * 2^7) exceeds
+    the fast path's cap, so the reference point must still move before the value product."""
+    n, H, D = 200, 2, 64
+    rng = np.random.default_rng(12)
+    q = np.ones((H, n, D), np.float32)
+    lift = np.zeros(n, np.float32)
+    lift[64:128] = 7.0 * np.log(2.0) * 8.0 / D        # scale * <q, k> = 7 ln 2 above the first tile
+    lift[128:] = 3.5 * np.log(2.0) * 8.0 / D
+    k = lift[None, :, None] + 0.02 * rng.standard_normal((H, n, D)).astype(np.float32)
+    v = rng.standard_normal((H, n, D)).astype(np.float32)
+    inp = dict(q=synth.f32_to_half_bits(q, dtype), k=synth.f32_to_half_bits(k, dtype),
+               v=synth.f32_to_half_bits(v, dtype), scale=np.float32(D ** -0.5), dtype=dtype)
+    for rel in ("triangular", "dense"):
+        compare(lib, inp, rel, what=f"tile mass {dtype} {rel}")
+
+
 def test_paper_layout_view(lib):
     """The logical (n, heads, width) view of head-major storage gives the same bits as [heads, n, width]."""
     inp = synth.attention_inputs(333, 3, 64, "f16", cfg=62)
