@@ -130,10 +130,26 @@ __device__ __forceinline__ void lds_load16(const void *src, uint8_t *run) {
 }
 
 // gfx950 transposing LDS read of 16-bit data: within each group of 16 lanes, lane i receives, in
-// slot j, element i % 4 of the 8 bytes addressed by lane 4 j + i / 4 of its group.
-__device__ __forceinline__ u2 lds_read_tr16(const uint8_t *p) {
-    typedef short s4 __attribute__((ext_vector_type(4)));
-    return __builtin_bit_cast(u2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4 *)p));
+// slot j, element i % 4 of the 8 bytes addressed by lane 4 j + i / 4 of its group.  Issued as
+// inline assembly: the compiler cannot tell these reads from the direct loads of the next tile
+// (which write the other LDS buffer) and would otherwise wait for those loads before every tile's
+// value product.  The caller orders the data with lgkm_wait; the tile itself is complete once
+// the barrier at the top of the tile has passed.
+template <int OFF>
+__device__ __forceinline__ u2 lds_read_tr16(uint32_t addr) {
+    u2 r;
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+    return r;
+}
+// Wait until at most N LDS operations of this wavefront are outstanding (they complete in order),
+// tied to the registers the waited-for reads wrote.
+template <int N>
+__device__ __forceinline__ void lgkm_wait(u4 &a, u4 &b) {
+    asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(a), "+v"(b) : "i"(N));
+}
+// 32-bit LDS address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_addr(const uint8_t *p) {
+    return (uint32_t)(size_t)(const __attribute__((address_space(3))) uint8_t *)p;
 }
 
 // Issue the direct loads of the K and V tile starting at key k0 into one LDS buffer.  ko / vo
@@ -184,6 +200,20 @@ struct State {
     f4 l[2];
 };
 
+// V^T operands of one 16-wide output block for both 32-key chunks: 8 keys per lane, in the key
+// slot order of the weights (keys 4g..4g+3 and 16+4g..16+4g+3 of the chunk).  VOFF is the byte
+// offset of the V tile in LDS, addr this lane's address of the block within it.
+template <int D, int VOFF>
+__device__ __forceinline__ void read_vt(uint32_t addr, u4 (&a)[2]) {
+    using G = Geo<D>;
+    const u2 l0 = lds_read_tr16<VOFF>(addr);
+    const u2 h0 = lds_read_tr16<VOFF + 16 * G::RB>(addr);
+    const u2 l1 = lds_read_tr16<VOFF + 32 * G::RB>(addr);
+    const u2 h1 = lds_read_tr16<VOFF + 48 * G::RB>(addr);
+    a[0] = u4{l0.x, l0.y, h0.x, h0.y};
+    a[1] = u4{l1.x, l1.y, h1.x, h1.y};
+}
+
 // Weights 2^(c s - m) of query block qb, packed as the B operands of the value product: key
 // chunk 0 takes keys {4g..4g+3, 16+4g..16+4g+3}, chunk 1 the same keys plus 32.
 template <class T>
@@ -199,9 +229,9 @@ __device__ __forceinline__ void weights(const f4 (&s)[4][2], int qb, float c, fl
 
 // One 64-key tile: scores, relation mask, online-softmax update, value and mass products.
 // kb_ / vb_ are this lane's LDS byte addresses for the tile's K and V operands.
-template <class T, int D, bool CAUSAL>
+template <class T, int D, bool CAUSAL, int VOFF>
 __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][Geo<D>::CH], const uint8_t *kl,
-                                          const uint8_t *vl, const int *kr, const int *vr,
+                                          const int *kr, const uint32_t *vr,
                                           int64_t k0, int64_t n, int64_t qw0, float c, int col, int g, u4 ones) {
     using G = Geo<D>;
     // ---- S^T = K Q^T for 4 blocks of 16 keys x 2 blocks of 16 queries
@@ -271,19 +301,24 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
     }
     st.l[0] = ln[0];
     st.l[1] = ln[1];
-    // ---- O^T += V^T P^T; the V^T operand comes from the row-major V tile by transposing reads
-    //      (lane r of a 16-lane group receives width r of the four keys its group addresses)
+    // ---- O^T += V^T P^T; the V^T operand comes from the row-major V tile by transposing reads,
+    //      the operands of block db + 1 being read while the products of block db run
+    u4 va[2], vn[2];
+    read_vt<D, VOFF>(vr[0], va);
 #pragma unroll
     for (int db = 0; db < G::DB; ++db) {
-#pragma unroll
-        for (int kc = 0; kc < 2; ++kc) {
-            const uint8_t *base = vl + vr[db] + kc * 32 * G::RB;
-            const u2 l2 = lds_read_tr16(base);
-            const u2 h2v = lds_read_tr16(base + 16 * G::RB);
-            const u4 a = u4{l2.x, l2.y, h2v.x, h2v.y};
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb) st.o[db][qb] = T::mma(a, pb[kc][qb], st.o[db][qb]);
+        if (db + 1 < G::DB) {
+            read_vt<D, VOFF>(vr[db + 1], vn);
+            lgkm_wait<4>(va[0], va[1]);
+        } else {
+            lgkm_wait<0>(va[0], va[1]);
         }
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb) st.o[db][qb] = T::mma(va[kc], pb[kc][qb], st.o[db][qb]);
+        va[0] = vn[0];
+        va[1] = vn[1];
     }
 }
 
@@ -327,7 +362,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restr
         vo[r] = kk * G::CPR + v_chunk<D>(kk, pc);
     }
     // operand read addresses of this lane within a tile
-    int kr[G::CH], vr[G::DB];
+    int kr[G::CH];
+    uint32_t vr[G::DB];
 #pragma unroll
     for (int ch = 0; ch < G::CH; ++ch) kr[ch] = col * G::RB + 16 * k_chunk<D>(col, ch * 4 + g);
     {
@@ -335,7 +371,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restr
         const int row = 4 * g + s / 4;           // key row of this lane's address (plus 16 / 32 steps)
         const int sw = (row / G::R) % G::NB;
 #pragma unroll
-        for (int db = 0; db < G::DB; ++db) vr[db] = row * G::RB + 32 * (db ^ sw) + 8 * (s % 4);
+        for (int db = 0; db < G::DB; ++db) vr[db] = lds_addr(lds) + row * G::RB + 32 * (db ^ sw) + 8 * (s % 4);
     }
 
     State<T, D> st;
@@ -365,13 +401,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restr
         if (kt + 1 < ntk) stage_kv<D>(kh, vh, k0 + kBN, n, ko, vo, l1, l1 + G::TILE, w, lane);
         // a wavefront whose queries all precede the tile has nothing to add from it
         if (k0 <= klast)
-            tile_step<T, D, CAUSAL>(st, qreg, l0, l0 + G::TILE, kr, vr, k0, n, qw0, c, col, g, ones);
+            tile_step<T, D, CAUSAL, G::TILE>(st, qreg, l0, kr, vr, k0, n, qw0, c, col, g, ones);
         if (kt + 1 >= ntk) break;
         __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
         if (kt + 2 < ntk) stage_kv<D>(kh, vh, k0 + 2 * kBN, n, ko, vo, l0, l0 + G::TILE, w, lane);
         if (k0 + kBN <= klast)
-            tile_step<T, D, CAUSAL>(st, qreg, l1, l1 + G::TILE, kr, vr, k0 + kBN, n, qw0, c, col, g, ones);
+            tile_step<T, D, CAUSAL, 3 * G::TILE>(st, qreg, l1, kr, vr, k0 + kBN, n, qw0, c, col, g, ones);
     }
 
     // ---- finalize: total mass over the four lanes of a query, divide, store
