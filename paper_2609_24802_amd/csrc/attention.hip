@@ -147,6 +147,17 @@ template <int N>
 __device__ __forceinline__ void lgkm_wait(u4 &a, u4 &b) {
     asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(a), "+v"(b) : "i"(N));
 }
+// Plain 16-byte LDS read, issued as inline assembly like the transposing read (same reason).
+template <int OFF>
+__device__ __forceinline__ u4 lds_read_b128(uint32_t addr) {
+    u4 r;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+    return r;
+}
+template <int N>
+__device__ __forceinline__ void lgkm_wait1(u4 &a) {
+    asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(a) : "i"(N));
+}
 // 32-bit LDS address of a pointer into a __shared__ array.
 __device__ __forceinline__ uint32_t lds_addr(const uint8_t *p) {
     return (uint32_t)(size_t)(const __attribute__((address_space(3))) uint8_t *)p;
@@ -227,27 +238,41 @@ __device__ __forceinline__ void weights(const f4 (&s)[4][2], int qb, float c, fl
     p1 = u4{T::pack(p[2][0], p[2][1]), T::pack(p[2][2], p[2][3]), T::pack(p[3][0], p[3][1]), T::pack(p[3][2], p[3][3])};
 }
 
+// Step R of the score product S^T = K Q^T: K operand R (chunk R / 4, key block R % 4) is
+// consumed by the two query blocks, and the read of operand R + 4 is issued into its registers;
+// at most 4 reads are in flight.  kaddr[ch] is this lane's LDS address of chunk ch in key block 0.
+template <class T, int D, int KOFF, int R>
+__device__ __forceinline__ void score_step(f4 (&s)[4][2], u4 (&ka)[4], const u4 *qreg, const uint32_t *kaddr) {
+    using G = Geo<D>;
+    constexpr int NR = 4 * G::CH;
+    if constexpr (R < NR) {
+        constexpr int ch = R / 4, kb = R % 4, left = NR - 1 - R;
+        lgkm_wait1<(left < 3 ? left : 3)>(ka[R % 4]);
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+            s[kb][qb] = T::mma(ka[R % 4], qreg[qb * G::CH + ch], ch == 0 ? f4{0.0f, 0.0f, 0.0f, 0.0f} : s[kb][qb]);
+        if constexpr (R + 4 < NR)
+            ka[R % 4] = lds_read_b128<KOFF + (R + 4) % 4 * 16 * G::RB>(kaddr[(R + 4) / 4]);
+        score_step<T, D, KOFF, R + 1>(s, ka, qreg, kaddr);
+    }
+}
+
 // One 64-key tile: scores, relation mask, online-softmax update, value and mass products.
 // kb_ / vb_ are this lane's LDS byte addresses for the tile's K and V operands.
-template <class T, int D, bool CAUSAL, int VOFF>
-__device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][Geo<D>::CH], const uint8_t *kl,
-                                          const int *kr, const uint32_t *vr,
+template <class T, int D, bool CAUSAL, int KOFF, int VOFF>
+__device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][Geo<D>::CH], const uint32_t *kaddr,
+                                          const uint32_t *vr,
                                           int64_t k0, int64_t n, int64_t qw0, float c, int col, int g, u4 ones) {
     using G = Geo<D>;
-    // ---- S^T = K Q^T for 4 blocks of 16 keys x 2 blocks of 16 queries
+    // ---- S^T = K Q^T for 4 blocks of 16 keys x 2 blocks of 16 queries, the K operands read in a
+    //      rolling window of 4
     f4 s[4][2];
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-        for (int qb = 0; qb < 2; ++qb) s[kb][qb] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int ch = 0; ch < G::CH; ++ch) {
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-            const u4 a = *reinterpret_cast<const u4 *>(kl + kr[ch] + kb * 16 * G::RB);
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb) s[kb][qb] = T::mma(a, qreg[qb][ch], s[kb][qb]);
-        }
-    }
+    u4 ka[4];
+    ka[0] = lds_read_b128<KOFF + 0 * 16 * G::RB>(kaddr[0]);
+    ka[1] = lds_read_b128<KOFF + 1 * 16 * G::RB>(kaddr[0]);
+    ka[2] = lds_read_b128<KOFF + 2 * 16 * G::RB>(kaddr[0]);
+    ka[3] = lds_read_b128<KOFF + 3 * 16 * G::RB>(kaddr[0]);
+    score_step<T, D, KOFF, 0>(s, ka, &qreg[0][0], kaddr);
     // ---- relation: keys past n, and (triangular) keys after the query
     const bool edge = k0 + kBN > n || (CAUSAL && k0 + kBN - 1 > qw0);
     if (edge) {
@@ -362,10 +387,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restr
         vo[r] = kk * G::CPR + v_chunk<D>(kk, pc);
     }
     // operand read addresses of this lane within a tile
-    int kr[G::CH];
+    uint32_t kr[G::CH];
     uint32_t vr[G::DB];
 #pragma unroll
-    for (int ch = 0; ch < G::CH; ++ch) kr[ch] = col * G::RB + 16 * k_chunk<D>(col, ch * 4 + g);
+    for (int ch = 0; ch < G::CH; ++ch) kr[ch] = lds_addr(lds) + col * G::RB + 16 * k_chunk<D>(col, ch * 4 + g);
     {
         const int s = lane & 15;
         const int row = 4 * g + s / 4;           // key row of this lane's address (plus 16 / 32 steps)
@@ -401,13 +426,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restr
         if (kt + 1 < ntk) stage_kv<D>(kh, vh, k0 + kBN, n, ko, vo, l1, l1 + G::TILE, w, lane);
         // a wavefront whose queries all precede the tile has nothing to add from it
         if (k0 <= klast)
-            tile_step<T, D, CAUSAL, G::TILE>(st, qreg, l0, kr, vr, k0, n, qw0, c, col, g, ones);
+            tile_step<T, D, CAUSAL, 0, G::TILE>(st, qreg, kr, vr, k0, n, qw0, c, col, g, ones);
         if (kt + 1 >= ntk) break;
         __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
         if (kt + 2 < ntk) stage_kv<D>(kh, vh, k0 + 2 * kBN, n, ko, vo, l0, l0 + G::TILE, w, lane);
         if (k0 + kBN <= klast)
-            tile_step<T, D, CAUSAL, 3 * G::TILE>(st, qreg, l1, kr, vr, k0 + kBN, n, qw0, c, col, g, ones);
+            tile_step<T, D, CAUSAL, 2 * G::TILE, 3 * G::TILE>(st, qreg, kr, vr, k0 + kBN, n, qw0, c, col, g, ones);
     }
 
     // ---- finalize: total mass over the four lanes of a query, divide, store
