@@ -298,6 +298,10 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
     // the weights again before any value product uses them.
     u4 pb[2][2];   // [key chunk][query block]: B operands of the second product
     f4 ln[2];
+    // the weights are the VALU stretch of the tile: issued at raised priority, so that the
+    // other wavefront of the SIMD keeps the matrix core busy meanwhile rather than competing
+    // for the issue slots
+    __builtin_amdgcn_s_setprio(2);
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
         weights<T>(s, qb, c, st.m[qb], pb[0][qb], pb[1][qb]);
@@ -326,6 +330,7 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
     }
     st.l[0] = ln[0];
     st.l[1] = ln[1];
+    __builtin_amdgcn_s_setprio(0);
     // ---- O^T += V^T P^T; the V^T operand comes from the row-major V tile by transposing reads,
     //      the operands of block db + 1 being read while the products of block db run
     u4 va[2], vn[2];
