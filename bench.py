@@ -322,11 +322,59 @@ def cpu_baseline(args, oracle, rp, col, x, w):
                        f"fp64 accumulation, {dt:.1f} s")
 
 
+def cpu_baseline_config1(oracle, synth):
+    """The oracle on config 1 (weighted-sum forward and backward, 1,024 nodes, 8,192 edges), single-
+    threaded and on all host threads: one warmup, then the median of three calls."""
+    g = synth.csr_uniform_small()
+    rp, col, x, w, dy = g["row_ptr"], g["col"], g["x"], g["w"], g["dy"]
+
+    def once():
+        oracle.csr_sum_fwd(rp, col, x, w)
+        oracle.csr_sum_bwd(rp, col, x, w, dy, g["num_src"])
+
+    out = {}
+    for label, nt in (("single_thread", 1), ("all_threads", 0)):
+        oracle.set_threads(nt)
+        once()
+        ts = []
+        for _ in range(3):
+            t = time.perf_counter()
+            once()
+            ts.append(time.perf_counter() - t)
+        out[f"{label}_us"] = sorted(ts)[1] * 1e6
+        out[f"{label}_threads"] = oracle.threads()
+    oracle.set_threads(0)
+    out.update(kind="oracle", sample="config 1 weighted-sum forward + backward (dx, dw), fp64 accumulation")
+    log(f"cpu oracle config 1: {out['single_thread_us']:.0f} us on 1 thread, {out['all_threads_us']:.0f} us "
+        f"on {out['all_threads_threads']}")
+    return out
+
+
 def paths(args, torch, tb, synth):
     """Per-path figures on the other workloads (each timed with HIP events)."""
     res = {}
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
     steps, warm = max(5, args.steps // 2), 2
+
+    # config 1 (1,024 nodes, 8,192 uniform edges, F = 16): bound by launch latency (0.66 MB of traffic
+    # is 83 ns at the HBM peak), so the figure is microseconds per call, from HIP events and from the
+    # host clock (launch overhead included)
+    g = synth.csr_uniform_small()
+    rp1, col1 = g["row_ptr"], g["col"]
+    E1 = int(rp1[-1])
+    rel1 = tb.Csr(dev(rp1), dev(col1), g["num_dst"])
+    x1, w1, dy1 = dev(g["x"]), dev(g["w"]), dev(g["dy"])
+    rev1 = tb.tiga_csr_transpose(rel1)
+    c1 = {"sum_fwd": lambda: tb.tiga_mp_csr_fwd(rel1, x1, w1),
+          "sum_bwd_gather": lambda: tb.tiga_mp_csr_bwd(rel1, dy1, x1, w1, rev=rev1),
+          "sum_fwd_bwd": lambda: (tb.tiga_mp_csr_fwd(rel1, x1, w1), tb.tiga_mp_csr_bwd(rel1, dy1, x1, w1, rev=rev1))}
+    for key, fn in c1.items():
+        r = time_steps(torch, tb, fn, 200, 20)
+        res[f"csr_uniform_1024n_8192e_f16_{key}"] = dict(us_per_call=r["step_ms"] * 1e3,
+                                                        wall_us_per_call=r["wall_ms"] * 1e3,
+                                                        gedges_per_s=E1 / r["step_ms"] / 1e6)
+        log(f"config 1 {key}: {r['step_ms'] * 1e3:.1f} us")
+    del rel1, x1, w1, dy1, rev1
 
     g = synth.config2()
     rp, col, n = g["row_ptr"], g["col"], g["num_dst"]
@@ -568,6 +616,8 @@ def main():
     extra = {} if args.no_paths else paths(args, torch, tb, synth)
     if "paged" in h:
         extra[f"csr_paged_host_relation_{h['n']}n_{h['E']}e_f{h['F']}"] = h["paged"]
+    if not args.no_paths and not args.no_cpu:
+        extra["csr_uniform_1024n_8192e_f16_cpu_oracle"] = cpu_baseline_config1(oracle, synth)
     value = h["E"] / (h["step_ms"] * 1e-3) / 1e9
     line = {
         "metric": "GEdges/s fused fwd(+bwd) and achieved HBM GB/s vs peak, 1 MI355X",

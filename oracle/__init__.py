@@ -46,6 +46,7 @@ def _load():
             i64, i32, vp, f32 = C.c_int64, C.c_int32, C.c_void_p, C.c_float
             sig = {
                 "tiga_oracle_threads": (C.c_int, []),
+                "tiga_oracle_set_threads": (None, [C.c_int]),
                 "tiga_oracle_csr_sum_fwd": (None, [i64, vp, i32, vp, vp, vp, vp, vp, vp]),
                 "tiga_oracle_csr_max_fwd": (None, [i64, vp, i32, vp, vp, vp, vp, vp, vp]),
                 "tiga_oracle_csr_sum_bwd": (None, [i64, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
@@ -80,6 +81,11 @@ def _c(a, dtype):
 
 def threads() -> int:
     return int(_load().tiga_oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """Threads for later calls (n <= 0: all host cores again); results do not depend on it."""
+    _load().tiga_oracle_set_threads(int(n))
 
 
 def _rows(rows, n):

@@ -44,6 +44,19 @@ int tiga_oracle_threads(void) {
 #endif
 }
 
+/* Threads for the following calls: n >= 1 sets that many, n <= 0 restores the default (all host
+ * cores).  Only the timing of the baseline uses it; every result is independent of it (each
+ * output is summed by one thread in a fixed order). */
+static int default_threads = 0;
+void tiga_oracle_set_threads(int n) {
+#ifdef _OPENMP
+    if (default_threads == 0) default_threads = omp_get_max_threads();
+    omp_set_num_threads(n >= 1 ? n : default_threads);
+#else
+    (void)n;
+#endif
+}
+
 /* ------------------------------------------------------------------------ */
 /* Stored CSR relation, weighted-sum message                                 */
 /* ------------------------------------------------------------------------ */

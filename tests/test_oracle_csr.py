@@ -200,3 +200,19 @@ def test_powerlaw_generator_shapes():
     y, _ = oracle.csr_sum_fwd(rp, col, g["x"], g["w"], rows=np.arange(10))
     A = sp.csr_matrix((g["w"].astype(np.float64), col, rp), shape=(n, n))
     np.testing.assert_allclose(y, (A @ g["x"].astype(np.float64))[:10], rtol=1e-12, atol=1e-12)
+
+
+def test_results_do_not_depend_on_thread_count():
+    """Each output is summed by one thread in a fixed order, so one thread and all host threads give
+    the same bits (the baseline timing runs both)."""
+    g = synth.csr_uniform_small()
+    args = (g["row_ptr"], g["col"], g["x"], g["w"])
+    try:
+        oracle.set_threads(1)
+        one = oracle.csr_sum_fwd(*args), oracle.csr_sum_bwd(*args, g["dy"], g["num_src"])
+    finally:
+        oracle.set_threads(0)
+    many = oracle.csr_sum_fwd(*args), oracle.csr_sum_bwd(*args, g["dy"], g["num_src"])
+    for a, b in zip(one, many):
+        for u, v in zip(a, b):
+            assert np.array_equal(u, v)
