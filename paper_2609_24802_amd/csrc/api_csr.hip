@@ -110,7 +110,7 @@ int tiga_mp_csr_fwd(const tiga_csr *rel, int32_t feat, const float *x_src, int m
     Trav t{rel->row_ptr, rel->col_idx, w_edge, nullptr, x_src, rel->num_dst, lay.fu, nullptr, 0u, rel->num_edges};
     const int wm = msg == TIGA_MSG_EDGE_SCALED_SRC ? W_DIRECT : W_NONE;
     return launch_traversal(t, rel->num_src, rel->num_edges, lay, reducer == TIGA_REDUCE_MAX ? RED_MAX : RED_SUM, wm, ws, y,
-                            argmax, static_cast<hipStream_t>(stream));
+                            argmax, static_cast<hipStream_t>(stream), direct_traversal(rel->num_dst, rel->num_edges));
 }
 
 size_t tiga_mp_csr_bwd_workspace(const tiga_csr *rel, int32_t feat, int reducer) {

@@ -189,7 +189,7 @@ int launch_bwd(const BwdArgs &a, void *ws, hipStream_t stream) {
             eg.dw = a.dw;
         }
         if (int rc = launch_traversal(t, rel->num_dst, rel->num_edges, lay, RED_SUM, wm, ws, a.dx, nullptr, stream,
-                                      eg))
+                                      direct_traversal(rel->num_src, rel->num_edges), eg))
             return rc;
     }
     return TIGA_OK;

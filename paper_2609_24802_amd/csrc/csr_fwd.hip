@@ -7,6 +7,11 @@ namespace csr {
 
 namespace {
 
+// Relations at most this large take the single-launch direct traversal (no plan, no merge): their
+// time is launch latency, which the plan's three extra launches and the merge would dominate.
+constexpr int64_t kDirectEdges = int64_t{1} << 16;
+constexpr int64_t kDirectRows = int64_t{1} << 16;
+
 // Edge gradient of the backward, formed during the traversal of the reverse
 // incidence: dw[e] = <x_j, dy[dst(e)]> for the source row j being folded
 // (for max, only the units whose argmax is e are nonzero when they arrive).  Each lane holds one unit of x_j; the L lanes of an edge slot add
@@ -101,6 +106,26 @@ __global__ __launch_bounds__(kBlock) void gather_reduce_kernel(Trav t, int64_t n
     for_each_item<L>(items, chunks, t.ptr, t.nrows, body);
 }
 
+// Small relations (at most kDirectEdges edges and kDirectRows rows): no plan and no merge, one
+// launch.  Wavefront w folds rows w, w + nwaves, ... with all 64 lanes, whatever their degree (a
+// row of kDirectEdges edges is about a thousand 64-edge steps), and writes each finalized row.
+template <int K, int L, int RED, int WM, bool BUF, bool NT, bool DW>
+__global__ __launch_bounds__(kBlock) void direct_kernel(Trav t, float *__restrict__ out, int32_t *__restrict__ out_arg,
+                                                        const float *__restrict__ hx, float *__restrict__ hdw) {
+    const Table<K, BUF, NT> tab(t.table, t.fu, t.table_bytes);
+    const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t *>(t.arg), 0, (BUF && WM == W_ROUTE) ? t.table_bytes : 0u, kBufWord3);
+    GatherBody<K, L, RED, WM, BUF, NT, DW> body{t, tab, ars, out, out_arg, nullptr, nullptr, hx, hdw};
+    const int lane = lane_id();
+    const int64_t wave = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
+    const int64_t nwaves = static_cast<int64_t>(gridDim.x) * kWavesPerBlock;
+    for (int64_t row = wave; row < t.nrows; row += nwaves) {
+        const int64_t e0 = t.ptr[row];
+        const Meta m{e0, static_cast<int32_t>(t.ptr[row + 1] - e0), static_cast<int32_t>(row), -1, 1};
+        body.template run<kWave>(m, lane);
+    }
+}
+
 // Merge the partial states of split rows in chunk order: lane slot s folds
 // chunks s, s + S, ..., then the slots are combined by a fixed shuffle tree.
 template <int K, int L, int RED>
@@ -162,10 +187,25 @@ int launch_gather_reduce(const Trav &t, int64_t n_groups, const PlanWs &w, const
     return check_launch("gather-reduce");
 }
 
+template <int K, int L, int RED, int WM, bool BUF, bool NT, bool DW>
+int launch_direct(const Trav &t, float *out, int32_t *out_arg, const EdgeGrad &eg, hipStream_t stream) {
+    auto kern = direct_kernel<K, L, RED, WM, BUF, NT, DW>;
+    static const int per_cu = resident_blocks(reinterpret_cast<const void *>(kern), kBlock);
+    const int blocks = persistent_blocks(t.nrows, per_cu);
+    prof_before(stream);
+    hipLaunchKernelGGL(kern, dim3(blocks), dim3(kBlock), 0, stream, t, out, out_arg, eg.x, eg.dw);
+    prof_after(stream);
+    return check_launch("direct gather-reduce");
+}
+
 template <int K, int L, int RED, int WM, bool DW>
 int launch_traversal_t(const Trav &t, int64_t nedges, const PlanWs &w, const PlanBounds &b, float *out,
-                       int32_t *out_arg, const EdgeGrad &eg, hipStream_t stream) {
+                       int32_t *out_arg, const EdgeGrad &eg, hipStream_t stream, bool direct) {
     constexpr Geom g = make_geom(L);
+    if (direct) {
+        if (!t.table_bytes) return launch_direct<K, L, RED, WM, false, true, DW>(t, out, out_arg, eg, stream);
+        return launch_direct<K, L, RED, WM, true, false, DW>(t, out, out_arg, eg, stream);
+    }
     if (int rc = launch_plan(t.ptr, t.nrows, g, b, w, stream)) return rc;
     const int64_t n_groups = ceil_div(t.nrows, g.RPW);
     int rc;
@@ -184,15 +224,15 @@ int launch_traversal_t(const Trav &t, int64_t nedges, const PlanWs &w, const Pla
 
 template <int K, int RED, int WM, bool DW = false>
 int dispatch_lanes(int L, const Trav &t, int64_t nedges, const PlanWs &w, const PlanBounds &b, float *out,
-                   int32_t *out_arg, const EdgeGrad &eg, hipStream_t stream) {
+                   int32_t *out_arg, const EdgeGrad &eg, hipStream_t stream, bool direct) {
     switch (L) {
-        case 1: return launch_traversal_t<K, 1, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream);
-        case 2: return launch_traversal_t<K, 2, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream);
-        case 4: return launch_traversal_t<K, 4, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream);
-        case 8: return launch_traversal_t<K, 8, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream);
-        case 16: return launch_traversal_t<K, 16, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream);
-        case 32: return launch_traversal_t<K, 32, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream);
-        case 64: return launch_traversal_t<K, 64, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream);
+        case 1: return launch_traversal_t<K, 1, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream, direct);
+        case 2: return launch_traversal_t<K, 2, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream, direct);
+        case 4: return launch_traversal_t<K, 4, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream, direct);
+        case 8: return launch_traversal_t<K, 8, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream, direct);
+        case 16: return launch_traversal_t<K, 16, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream, direct);
+        case 32: return launch_traversal_t<K, 32, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream, direct);
+        case 64: return launch_traversal_t<K, 64, RED, WM, DW>(t, nedges, w, b, out, out_arg, eg, stream, direct);
         default: return fail(TIGA_EINVAL, "internal: lanes per edge %d", L);
     }
 }
@@ -220,8 +260,10 @@ size_t traversal_ws_bytes(int64_t nrows, int64_t nedges, int64_t feat, bool with
     return best;
 }
 
+bool direct_traversal(int64_t nrows, int64_t nedges) { return nedges <= kDirectEdges && nrows <= kDirectRows; }
+
 int launch_traversal(const Trav &t0, int64_t table_rows, int64_t nedges, const Layout &lay, int red, int wm, void *ws,
-                     float *out, int32_t *out_arg, hipStream_t stream, const EdgeGrad &eg) {
+                     float *out, int32_t *out_arg, hipStream_t stream, bool direct, const EdgeGrad &eg) {
     if (t0.nrows == 0) return TIGA_OK;
     Trav t = t0;
     const int64_t tb = table_rows * lay.fu * lay.K * 4;
@@ -236,15 +278,15 @@ int launch_traversal(const Trav &t0, int64_t table_rows, int64_t nedges, const L
             return fail(TIGA_EUNSUPPORTED, "internal: fused edge gradients need a routed sum over one feature block");
         if (wm == W_INDIRECT) {
             if (lay.K == 4)
-                return dispatch_lanes<4, RED_SUM, W_INDIRECT, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream);
-            return dispatch_lanes<1, RED_SUM, W_INDIRECT, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream);
+                return dispatch_lanes<4, RED_SUM, W_INDIRECT, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream, direct);
+            return dispatch_lanes<1, RED_SUM, W_INDIRECT, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream, direct);
         }
         if (lay.K == 4)
-            return dispatch_lanes<4, RED_SUM, W_ROUTE, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream);
-        return dispatch_lanes<1, RED_SUM, W_ROUTE, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream);
+            return dispatch_lanes<4, RED_SUM, W_ROUTE, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream, direct);
+        return dispatch_lanes<1, RED_SUM, W_ROUTE, true>(lay.L, t, nedges, w, b, out, out_arg, eg, stream, direct);
     }
 #define TIGA_DISPATCH(KK, RR, WW) \
-    if (lay.K == KK && red == RR && wm == WW) return dispatch_lanes<KK, RR, WW>(lay.L, t, nedges, w, b, out, out_arg, eg, stream)
+    if (lay.K == KK && red == RR && wm == WW) return dispatch_lanes<KK, RR, WW>(lay.L, t, nedges, w, b, out, out_arg, eg, stream, direct)
     TIGA_DISPATCH(4, RED_SUM, W_DIRECT);
     TIGA_DISPATCH(4, RED_SUM, W_NONE);
     TIGA_DISPATCH(4, RED_SUM, W_INDIRECT);

@@ -29,8 +29,16 @@ struct EdgeGrad {
 // `table_rows` is the row count of t.table (and t.arg); tables below 4 GiB are
 // read through buffer resources.  With eg.dw the traversal must be a sum with
 // W_INDIRECT or W_ROUTE weights over one feature block (fu <= L).
+// Whether a relation of nrows rows and nedges edges takes the single-launch direct traversal (no
+// plan, no merge).  The direct traversal folds each row with all 64 lanes of a wavefront, the
+// planned one with a lane group sized by the row's degree class, so the two differ in rounding.
+bool direct_traversal(int64_t nrows, int64_t nedges);
+
+// `direct` chooses the traversal (callers pass direct_traversal() of the relation the result must
+// agree with bit for bit: a page of a relation takes the whole relation's choice).
 int launch_traversal(const Trav &t, int64_t table_rows, int64_t nedges, const Layout &lay, int red, int wm, void *ws,
-                     float *out, int32_t *out_arg, hipStream_t stream, const EdgeGrad &eg = EdgeGrad{});
+                     float *out, int32_t *out_arg, hipStream_t stream, bool direct,
+                     const EdgeGrad &eg = EdgeGrad{});
 
 // Paged forward: rel's row_ptr and col_idx and w_host live in host memory; pages of whole rows
 // with at most page_edges edges are staged through the workspace (see csr_paged.hip).

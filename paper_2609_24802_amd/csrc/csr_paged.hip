@@ -78,7 +78,10 @@ int launch_paged_fwd(const tiga_csr *rel, int32_t feat, const float *x_src, cons
         if (int rc = check_launch("paged: rebase")) return rc;
         Trav t{p.rp, p.col, w_host ? p.w : nullptr, nullptr, x_src, rows, lay.fu, nullptr, 0u, edges};
         int32_t *arg = argmax ? argmax + r0 * feat : nullptr;
-        if (int rc = launch_traversal(t, rel->num_src, edges, lay, red, wm, p.trav, y + r0 * feat, arg, stream))
+        // every page takes the traversal the whole relation would take, so that each row is folded
+        // in the same order as by the resident forward
+        if (int rc = launch_traversal(t, rel->num_src, edges, lay, red, wm, p.trav, y + r0 * feat, arg, stream,
+                                      direct_traversal(rel->num_dst, rel->num_edges)))
             return rc;
         if (arg && e0 > 0) {
             hipLaunchKernelGGL(shift_arg_kernel, dim3(static_cast<unsigned>(ceil_div(rows * feat, kBlock))),
