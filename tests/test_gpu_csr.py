@@ -375,3 +375,34 @@ def test_forward_bit_identical_across_runs(lib):
         assert torch.equal(a, b)
         if red == lib.REDUCE_MAX:
             assert torch.equal(aa, bb)
+
+
+@pytest.mark.parametrize("num_edges", [1 << 16, (1 << 16) + 1])
+@pytest.mark.parametrize("reducer", ["sum", "max"])
+def test_direct_traversal_boundary(lib, num_edges, reducer):
+    """Relations of at most 2^16 edges (and rows) take the single-launch traversal, larger ones the
+    planned one.  Both sides of the boundary, each with a row of about 60,000 edges and empty rows:
+    forward and gather-mode backward against the oracle."""
+    n, F = 500, 16
+    rng = np.random.default_rng(num_edges)
+    deg = rng.integers(0, 23, n).astype(np.int64)
+    deg[100] = 0
+    deg[100] = num_edges - int(deg.sum())
+    assert deg[100] > 50000 and (deg == 0).any()
+    row_ptr, col, x, w, dy = make_graph(deg, 400, F, seed=int(num_edges % 97))
+    red = lib.REDUCE_SUM if reducer == "sum" else lib.REDUCE_MAX
+    rel, y, arg = run_fwd(lib, row_ptr, col, x, w, 400, red)
+    rev = lib.tiga_csr_transpose(rel)
+    if reducer == "sum":
+        ry, rya = oracle.csr_sum_fwd(row_ptr, col, x, w)
+        assert_terms_close(y, ry, rya, what=f"direct boundary sum E={num_edges}")
+        rdx, rdxa, rdw, rdwa = oracle.csr_sum_bwd(row_ptr, col, x, w, dy, 400)
+        dx, dw = lib.tiga_mp_csr_bwd(rel, dev(dy), dev(x), dev(w), rev=rev)
+    else:
+        ry, rarg = oracle.csr_max_fwd(row_ptr, col, x, w)
+        assert np.array_equal(arg, rarg)
+        assert np.array_equal(y.view(np.int32), ry.view(np.int32))
+        rdx, rdxa, rdw, rdwa = oracle.csr_max_bwd(row_ptr, col, x, w, rarg, dy, 400)
+        dx, dw = lib.tiga_mp_csr_bwd(rel, dev(dy), dev(x), dev(w), reducer=lib.REDUCE_MAX, argmax=dev(arg), rev=rev)
+    assert_terms_close(host(dx), rdx, rdxa, what=f"direct boundary {reducer} dx E={num_edges}")
+    assert_terms_close(host(dw), rdw, rdwa, what=f"direct boundary {reducer} dw E={num_edges}")
