@@ -46,7 +46,6 @@ constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * kWave;
 constexpr int kQW = 32;                // queries per wavefront
 constexpr int kBM = kWaves * kQW;      // queries per block
-constexpr int kBN = 64;                // keys per tile
 constexpr float kMassCap = 4096.0f;    // largest tile mass (and so weight) of the fast path
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -90,7 +89,10 @@ struct Geo {
     static constexpr int NB = D / 16;                    // 32-byte blocks per row
     static constexpr int CH = D / 32;                    // 32-deep chunks of the score product
     static constexpr int DB = D / 16;                    // 16-wide blocks of the output
-    static constexpr int TILE = kBN * RB;                // bytes of one K or V tile in LDS
+    static constexpr int BN = D == 64 ? 128 : 64;        // keys per tile (registers allow 128 at width 64)
+    static constexpr int KB = BN / 16;                   // 16-key blocks of the score product
+    static constexpr int KC = BN / 32;                   // 32-key chunks of the value product
+    static constexpr int TILE = BN * RB;                 // bytes of one K or V tile in LDS
     static constexpr int LPW = TILE / 1024 / kWaves;     // 1-KB direct loads per wavefront, tile and operand
     static_assert(LPW >= 1 && TILE % (1024 * kWaves) == 0, "tile shape");
     static constexpr int LDS = 4 * TILE;                 // two buffers of (K, V)
@@ -158,6 +160,10 @@ template <int N>
 __device__ __forceinline__ void lgkm_wait1(u4 &a) {
     asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(a) : "i"(N));
 }
+template <int N>
+__device__ __forceinline__ void lgkm_wait(u4 &a, u4 &b, u4 &c, u4 &d) {
+    asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) : "i"(N));
+}
 // 32-bit LDS address of a pointer into a __shared__ array.
 __device__ __forceinline__ uint32_t lds_addr(const uint8_t *p) {
     return (uint32_t)(size_t)(const __attribute__((address_space(3))) uint8_t *)p;
@@ -172,7 +178,7 @@ __device__ __forceinline__ void stage_kv(const u4 *__restrict__ kh, const u4 *__
     using G = Geo<D>;
     const u4 *kt = kh + k0 * G::CPR;
     const u4 *vt = vh + k0 * G::CPR;
-    if (k0 + kBN <= n) {
+    if (k0 + G::BN <= n) {
 #pragma unroll
         for (int r = 0; r < G::LPW; ++r) {
             const int run = (w * G::LPW + r) * 1024;
@@ -215,7 +221,7 @@ struct State {
 // slot order of the weights (keys 4g..4g+3 and 16+4g..16+4g+3 of the chunk).  VOFF is the byte
 // offset of the V tile in LDS, addr this lane's address of the block within it.
 template <int D, int VOFF>
-__device__ __forceinline__ void read_vt(uint32_t addr, u4 (&a)[2]) {
+__device__ __forceinline__ void read_vt(uint32_t addr, u4 *a) {
     using G = Geo<D>;
     const u2 l0 = lds_read_tr16<VOFF>(addr);
     const u2 h0 = lds_read_tr16<VOFF + 16 * G::RB>(addr);
@@ -223,36 +229,55 @@ __device__ __forceinline__ void read_vt(uint32_t addr, u4 (&a)[2]) {
     const u2 h1 = lds_read_tr16<VOFF + 48 * G::RB>(addr);
     a[0] = u4{l0.x, l0.y, h0.x, h0.y};
     a[1] = u4{l1.x, l1.y, h1.x, h1.y};
+    if constexpr (G::KC == 4) {
+        const u2 l2 = lds_read_tr16<VOFF + 64 * G::RB>(addr);
+        const u2 h2 = lds_read_tr16<VOFF + 80 * G::RB>(addr);
+        const u2 l3 = lds_read_tr16<VOFF + 96 * G::RB>(addr);
+        const u2 h3 = lds_read_tr16<VOFF + 112 * G::RB>(addr);
+        a[2] = u4{l2.x, l2.y, h2.x, h2.y};
+        a[3] = u4{l3.x, l3.y, h3.x, h3.y};
+    }
 }
 
 // Weights 2^(c s - m) of query block qb, packed as the B operands of the value product: key
-// chunk 0 takes keys {4g..4g+3, 16+4g..16+4g+3}, chunk 1 the same keys plus 32.
-template <class T>
-__device__ __forceinline__ void weights(const f4 (&s)[4][2], int qb, float c, float m, u4 &p0, u4 &p1) {
-    float p[4][4];
+// chunk kc takes keys 32 kc + {4g..4g+3, 16+4g..16+4g+3}.
+template <class T, int KB>
+__device__ __forceinline__ void weights(const f4 (*s)[2], int qb, float c, float m, u4 (*pb)[2]) {
+    float p[KB][4];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
+    for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) p[kb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][qb][i], c, -m));
-    p0 = u4{T::pack(p[0][0], p[0][1]), T::pack(p[0][2], p[0][3]), T::pack(p[1][0], p[1][1]), T::pack(p[1][2], p[1][3])};
-    p1 = u4{T::pack(p[2][0], p[2][1]), T::pack(p[2][2], p[2][3]), T::pack(p[3][0], p[3][1]), T::pack(p[3][2], p[3][3])};
+#pragma unroll
+    for (int kc = 0; kc < KB / 2; ++kc)
+        pb[kc][qb] = u4{T::pack(p[2 * kc][0], p[2 * kc][1]), T::pack(p[2 * kc][2], p[2 * kc][3]),
+                        T::pack(p[2 * kc + 1][0], p[2 * kc + 1][1]), T::pack(p[2 * kc + 1][2], p[2 * kc + 1][3])};
 }
 
-// Step R of the score product S^T = K Q^T: K operand R (chunk R / 4, key block R % 4) is
+// Mass of query block qb over the tile: l + the sum of its weights, by MFMAs against an all-ones
+// A operand (every row of the result holds the sum for the block's query of that column).
+template <class T, int KC>
+__device__ __forceinline__ f4 mass(const u4 (*pb)[2], int qb, u4 ones, f4 l) {
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) l = T::mma(ones, pb[kc][qb], l);
+    return l;
+}
+
+// Step R of the score product S^T = K Q^T: K operand R (chunk R / KB, key block R % KB) is
 // consumed by the two query blocks, and the read of operand R + 4 is issued into its registers;
 // at most 4 reads are in flight.  kaddr[ch] is this lane's LDS address of chunk ch in key block 0.
 template <class T, int D, int KOFF, int R>
-__device__ __forceinline__ void score_step(f4 (&s)[4][2], u4 (&ka)[4], const u4 *qreg, const uint32_t *kaddr) {
+__device__ __forceinline__ void score_step(f4 (*s)[2], u4 (&ka)[4], const u4 *qreg, const uint32_t *kaddr) {
     using G = Geo<D>;
-    constexpr int NR = 4 * G::CH;
+    constexpr int NR = G::KB * G::CH;
     if constexpr (R < NR) {
-        constexpr int ch = R / 4, kb = R % 4, left = NR - 1 - R;
+        constexpr int ch = R / G::KB, kb = R % G::KB, left = NR - 1 - R;
         lgkm_wait1<(left < 3 ? left : 3)>(ka[R % 4]);
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb)
             s[kb][qb] = T::mma(ka[R % 4], qreg[qb * G::CH + ch], ch == 0 ? f4{0.0f, 0.0f, 0.0f, 0.0f} : s[kb][qb]);
         if constexpr (R + 4 < NR)
-            ka[R % 4] = lds_read_b128<KOFF + (R + 4) % 4 * 16 * G::RB>(kaddr[(R + 4) / 4]);
+            ka[R % 4] = lds_read_b128<KOFF + (R + 4) % G::KB * 16 * G::RB>(kaddr[(R + 4) / G::KB]);
         score_step<T, D, KOFF, R + 1>(s, ka, qreg, kaddr);
     }
 }
@@ -266,7 +291,7 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
     using G = Geo<D>;
     // ---- S^T = K Q^T for 4 blocks of 16 keys x 2 blocks of 16 queries, the K operands read in a
     //      rolling window of 4
-    f4 s[4][2];
+    f4 s[G::KB][2];
     u4 ka[4];
     ka[0] = lds_read_b128<KOFF + 0 * 16 * G::RB>(kaddr[0]);
     ka[1] = lds_read_b128<KOFF + 1 * 16 * G::RB>(kaddr[0]);
@@ -274,9 +299,9 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
     ka[3] = lds_read_b128<KOFF + 3 * 16 * G::RB>(kaddr[0]);
     score_step<T, D, KOFF, 0>(s, ka, &qreg[0][0], kaddr);
     // ---- relation: keys past n, and (triangular) keys after the query
-    const bool edge = k0 + kBN > n || (CAUSAL && k0 + kBN - 1 > qw0);
+    const bool edge = k0 + G::BN > n || (CAUSAL && k0 + G::BN - 1 > qw0);
     if (edge) {
-        const int nk = static_cast<int>(n - k0 < kBN ? n - k0 : kBN);
+        const int nk = static_cast<int>(n - k0 < G::BN ? n - k0 : G::BN);
         const int qr = static_cast<int>(CAUSAL ? qw0 - k0 : 0) + col;
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
@@ -284,7 +309,7 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
             // key kb*16 + 4g + i is admissible iff kb*16 + i < lim - 4g (constants on the left)
             const int rel = lim - g * 4;
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+            for (int kb = 0; kb < G::KB; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) s[kb][qb][i] = kb * 16 + i < rel ? s[kb][qb][i] : -__builtin_inff();
         }
@@ -296,7 +321,7 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
     // or NaN mass (the first tile, where m = -inf, always) sends the wavefront to the exact path,
     // which takes the tile's column maximum, rescales (o, l) to the new reference point and forms
     // the weights again before any value product uses them.
-    u4 pb[2][2];   // [key chunk][query block]: B operands of the second product
+    u4 pb[G::KC][2];   // [key chunk][query block]: B operands of the second product
     f4 ln[2];
     // the weights are the VALU stretch of the tile: issued at raised priority, so that the
     // other wavefront of the SIMD keeps the matrix core busy meanwhile rather than competing
@@ -304,8 +329,8 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
     __builtin_amdgcn_s_setprio(2);
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-        weights<T>(s, qb, c, st.m[qb], pb[0][qb], pb[1][qb]);
-        ln[qb] = T::mma(ones, pb[1][qb], T::mma(ones, pb[0][qb], st.l[qb]));
+        weights<T, G::KB>(s, qb, c, st.m[qb], pb);
+        ln[qb] = mass<T, G::KC>(pb, qb, ones, st.l[qb]);
     }
     const bool fast = ln[0][0] - st.l[0][0] <= kMassCap && ln[1][0] - st.l[1][0] <= kMassCap;
     if (!__all(fast)) {
@@ -313,7 +338,7 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
         for (int qb = 0; qb < 2; ++qb) {
             float mt = s[0][qb][0];
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+            for (int kb = 0; kb < G::KB; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) mt = fmaxf(mt, s[kb][qb][i]);
             mt = max_over_column(mt) * c;
@@ -324,8 +349,8 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
 #pragma unroll
                 for (int db = 0; db < G::DB; ++db) st.o[db][qb] *= alpha;
             }
-            weights<T>(s, qb, c, st.m[qb], pb[0][qb], pb[1][qb]);
-            ln[qb] = T::mma(ones, pb[1][qb], T::mma(ones, pb[0][qb], st.l[qb]));
+            weights<T, G::KB>(s, qb, c, st.m[qb], pb);
+            ln[qb] = mass<T, G::KC>(pb, qb, ones, st.l[qb]);
         }
     }
     st.l[0] = ln[0];
@@ -333,22 +358,24 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
     __builtin_amdgcn_s_setprio(0);
     // ---- O^T += V^T P^T; the V^T operand comes from the row-major V tile by transposing reads,
     //      the operands of block db + 1 being read while the products of block db run
-    u4 va[2], vn[2];
+    u4 va[G::KC], vn[G::KC];
     read_vt<D, VOFF>(vr[0], va);
 #pragma unroll
     for (int db = 0; db < G::DB; ++db) {
-        if (db + 1 < G::DB) {
-            read_vt<D, VOFF>(vr[db + 1], vn);
-            lgkm_wait<4>(va[0], va[1]);
+        if (db + 1 < G::DB) read_vt<D, VOFF>(vr[db + 1], vn);
+        if constexpr (G::KC == 2) {
+            if (db + 1 < G::DB) lgkm_wait<4>(va[0], va[1]);
+            else lgkm_wait<0>(va[0], va[1]);
         } else {
-            lgkm_wait<0>(va[0], va[1]);
+            if (db + 1 < G::DB) lgkm_wait<8>(va[0], va[1], va[2], va[3]);
+            else lgkm_wait<0>(va[0], va[1], va[2], va[3]);
         }
 #pragma unroll
-        for (int kc = 0; kc < 2; ++kc)
+        for (int kc = 0; kc < G::KC; ++kc)
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb) st.o[db][qb] = T::mma(va[kc], pb[kc][qb], st.o[db][qb]);
-        va[0] = vn[0];
-        va[1] = vn[1];
+#pragma unroll
+        for (int kc = 0; kc < G::KC; ++kc) va[kc] = vn[kc];
     }
 }
 
@@ -415,7 +442,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restr
     const u4 ones = T::ones();
 
     const int64_t kend = CAUSAL ? (q0 + kBM < n ? q0 + kBM : n) : n;  // keys this block needs
-    const int ntk = static_cast<int>((kend + kBN - 1) / kBN);
+    const int ntk = static_cast<int>((kend + G::BN - 1) / G::BN);
 
     // last key any query of this wavefront admits (dense: every key; kept as a run-time bound in
     // both cases, which also keeps the two relations on one instruction schedule)
@@ -427,17 +454,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const u4 *__restr
         // buffer 0 holds tile kt; prefetch tile kt + 1 into buffer 1
         __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
-        const int64_t k0 = static_cast<int64_t>(kt) * kBN;
-        if (kt + 1 < ntk) stage_kv<D>(kh, vh, k0 + kBN, n, ko, vo, l1, l1 + G::TILE, w, lane);
+        const int64_t k0 = static_cast<int64_t>(kt) * G::BN;
+        if (kt + 1 < ntk) stage_kv<D>(kh, vh, k0 + G::BN, n, ko, vo, l1, l1 + G::TILE, w, lane);
         // a wavefront whose queries all precede the tile has nothing to add from it
         if (k0 <= klast)
             tile_step<T, D, CAUSAL, 0, G::TILE>(st, qreg, kr, vr, k0, n, qw0, c, col, g, ones);
         if (kt + 1 >= ntk) break;
         __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
-        if (kt + 2 < ntk) stage_kv<D>(kh, vh, k0 + 2 * kBN, n, ko, vo, l0, l0 + G::TILE, w, lane);
-        if (k0 + kBN <= klast)
-            tile_step<T, D, CAUSAL, 2 * G::TILE, 3 * G::TILE>(st, qreg, kr, vr, k0 + kBN, n, qw0, c, col, g, ones);
+        if (kt + 2 < ntk) stage_kv<D>(kh, vh, k0 + 2 * G::BN, n, ko, vo, l0, l0 + G::TILE, w, lane);
+        if (k0 + G::BN <= klast)
+            tile_step<T, D, CAUSAL, 2 * G::TILE, 3 * G::TILE>(st, qreg, kr, vr, k0 + G::BN, n, qw0, c, col, g, ones);
     }
 
     // ---- finalize: total mass over the four lanes of a query, divide, store
