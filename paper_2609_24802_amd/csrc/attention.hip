@@ -4,11 +4,12 @@
 // common maximum).  For head h and destination i:
 //   s_ij = scale * <q_i, k_j>,  y_i = sum_{j in N(i)} exp(s_ij) v_j / sum_{j in N(i)} exp(s_ij)
 // with N(i) = {0..i} (triangular, diagonal included) or {0..n-1} (dense).  No score or weight
-// array is stored: scores live in registers for one 64-key tile.
+// array is stored: scores live in registers for one key tile.
 //
 // MI355X design (gfx950, MFMA 16x16x32 with fp32 accumulation):
 //  - A block of 4 wavefronts owns 128 consecutive queries of one head (32 per wavefront) and
-//    streams the keys in tiles of 64 through LDS, double-buffered with one barrier per tile.
+//    streams the keys in tiles of 64 (width 128) or 128 (width 64) through LDS, double-buffered
+//    with one barrier per tile.
 //  - Scores are formed transposed, S^T = K Q^T (A = K from LDS, B = Q^T held in registers), so a
 //    lane's scores all belong to one query (column = lane % 16).  The reference point, mass and
 //    rescale are then lane-local; only the exact path's column maximum crosses lanes (the four
@@ -282,14 +283,15 @@ __device__ __forceinline__ void score_step(f4 (*s)[2], u4 (&ka)[4], const u4 *qr
     }
 }
 
-// One 64-key tile: scores, relation mask, online-softmax update, value and mass products.
-// kb_ / vb_ are this lane's LDS byte addresses for the tile's K and V operands.
+// One key tile: scores, relation mask, online-softmax update, value and mass products.
+// kaddr[ch] / vr[db] are this lane's LDS addresses of K chunk ch (key block 0) and of V^T output
+// block db within a tile; KOFF / VOFF are the byte offsets of the tile's K and V buffers.
 template <class T, int D, bool CAUSAL, int KOFF, int VOFF>
 __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][Geo<D>::CH], const uint32_t *kaddr,
                                           const uint32_t *vr,
                                           int64_t k0, int64_t n, int64_t qw0, float c, int col, int g, u4 ones) {
     using G = Geo<D>;
-    // ---- S^T = K Q^T for 4 blocks of 16 keys x 2 blocks of 16 queries, the K operands read in a
+    // ---- S^T = K Q^T for KB blocks of 16 keys x 2 blocks of 16 queries, the K operands read in a
     //      rolling window of 4
     f4 s[G::KB][2];
     u4 ka[4];
