@@ -404,6 +404,91 @@ __global__ __launch_bounds__(kSplit * kWave) void select_kernel(const f4 *__rest
     }
 }
 
+// ---- small relations: one wavefront per query, no build
+
+// At or below this many points every query scans every point and no relation is built (box,
+// Morton keys, sort, records, boxes): the build's launches and the tiled select's short dependent
+// chains cost more there than the quadratic distance work.
+constexpr int64_t kBruteMax = 16384;
+constexpr int kBruteWaves = 4;   // queries per block
+
+// 64-bit lane shift: lane t receives lane t - 1's value (lane 0 its own).
+__device__ __forceinline__ uint64_t shift_up(uint64_t v) {
+    const int src = lane_id() > 0 ? lane_id() - 1 : 0;
+    const uint32_t lo = __builtin_amdgcn_ds_bpermute(src * 4, static_cast<int>(static_cast<uint32_t>(v)));
+    const uint32_t hi = __builtin_amdgcn_ds_bpermute(src * 4, static_cast<int>(static_cast<uint32_t>(v >> 32)));
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(v)), l);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(v >> 32)), l);
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Wavefront w of block b takes query q = kBruteWaves b + w; its lanes scan the points 64 at a
+// time in input order, with the fp32 distance and the (distance, index) key of the tiled select.
+// The query's KP smallest keys are kept one per lane (lanes 0..KP-1, ascending); a step's keys
+// below the current KP-th key are found by one ballot and inserted one at a time (each lane takes
+// its left neighbour's key or the new one: the same rule as the register state of the tiled
+// select), so the list is exact whatever the order of the scan.
+template <int KP>
+__global__ __launch_bounds__(kBruteWaves * kWave) void brute_kernel(const float *__restrict__ pos, int64_t n, int k,
+                                                                    int feat, const float *__restrict__ x,
+                                                                    float *__restrict__ y, int32_t *__restrict__ nbr) {
+    const int lane = lane_id();
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * kBruteWaves + uniform(static_cast<int>(threadIdx.x) / kWave);
+    if (q >= n) return;
+    const f4 me = f4{pos[q * 3], pos[q * 3 + 1], pos[q * 3 + 2], 0.0f};   // uniform: scalar loads
+    uint64_t L = kNone;                                                      // lane t < KP: the t-th key
+    if (finite3(me.x, me.y, me.z)) {
+        uint64_t thr = kNone;                                                // the KP-th key (uniform)
+        // candidates of the next step are loaded before the current step is tested
+        int64_t j = lane;
+        f4 pj = j < n ? f4{pos[j * 3], pos[j * 3 + 1], pos[j * 3 + 2], 0.0f} : f4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int64_t c0 = 0; c0 < n; c0 += kWave) {
+            const f4 cur = pj;
+            const int64_t jc = c0 + lane;
+            j = jc + kWave;
+            if (j < n) pj = f4{pos[j * 3], pos[j * 3 + 1], pos[j * 3 + 2], 0.0f};
+            const float d2 = sqdist(me, cur);
+            uint64_t key = (static_cast<uint64_t>(__float_as_uint(d2)) << 32) | static_cast<uint32_t>(jc);
+            key = (jc >= n || jc == q) ? ~0ull : key;   // past the end, or the query itself
+            uint64_t mask = __builtin_amdgcn_ballot_w64(key < thr);
+            while (mask) {
+                const int b = __builtin_ctzll(mask);
+                mask &= mask - 1;
+                const uint64_t nk = readlane64(key, b);
+                if (nk >= thr) continue;   // the list moved below it meanwhile
+                const uint64_t left = shift_up(L);
+                const uint64_t up = lane == 0 ? nk : (nk < left ? left : nk);
+                L = lane < KP ? (nk < L ? up : L) : L;
+                thr = readlane64(L, KP - 1);
+            }
+        }
+    }
+    const bool has = lane < k && L < kNone;
+    const int32_t sel = has ? static_cast<int32_t>(static_cast<uint32_t>(L)) : -1;
+    if (nbr && lane < k) nbr[q * k + lane] = sel;
+    for (int f = 0; f < feat; ++f) {
+        float v = has ? x[static_cast<int64_t>(sel) * feat + f] : 0.0f;
+        // fixed shuffle tree over the lanes (the selected rows in key order, then zeros)
+#pragma unroll
+        for (int o = kWave / 2; o >= 1; o /= 2) v += __shfl_xor(v, o);
+        if (lane == 0) y[q * feat + f] = v;
+    }
+}
+
+template <int KP>
+int launch_brute(int64_t n, int k, int feat, const float *pos, const float *x, float *y, int32_t *nbr,
+                 hipStream_t stream) {
+    prof_before(stream);
+    hipLaunchKernelGGL(brute_kernel<KP>, dim3(static_cast<unsigned>(ceil_div(n, kBruteWaves))),
+                       dim3(kBruteWaves * kWave), 0, stream, pos, n, k, feat, x, y, nbr);
+    prof_after(stream);
+    return check_launch("kNN brute force");
+}
+
 template <int KP>
 int launch_select(const Ws &w, int64_t ntile, int k, int feat, const float *x, float *y, int32_t *nbr,
                   hipStream_t stream) {
@@ -424,6 +509,17 @@ size_t workspace_bytes(int64_t n) {
 
 int forward(int64_t n, int32_t feat, const float *pos, const float *x, int32_t k, float *y, int32_t *nbr, void *ws,
             hipStream_t stream) {
+    const int kp = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : k <= 8 ? 8 : k <= 16 ? 16 : 32;
+    if (n <= kBruteMax) {
+        switch (kp) {
+            case 1: return launch_brute<1>(n, k, feat, pos, x, y, nbr, stream);
+            case 2: return launch_brute<2>(n, k, feat, pos, x, y, nbr, stream);
+            case 4: return launch_brute<4>(n, k, feat, pos, x, y, nbr, stream);
+            case 8: return launch_brute<8>(n, k, feat, pos, x, y, nbr, stream);
+            case 16: return launch_brute<16>(n, k, feat, pos, x, y, nbr, stream);
+            default: return launch_brute<32>(n, k, feat, pos, x, y, nbr, stream);
+        }
+    }
     Carve c(ws);
     Ws w = carve(c, n);
     const int64_t ntile = ceil_div(n, kTile);
@@ -450,7 +546,6 @@ int forward(int64_t n, int32_t feat, const float *pos, const float *x, int32_t k
     hipLaunchKernelGGL(group_box_kernel, dim3(static_cast<unsigned>(ceil_div(ngroup, kBlock / kWave))), dim3(kBlock), 0,
                        stream, w.tlo, w.thi, ntile, ngroup, w.glo, w.ghi);
     if (int rc = check_launch("kNN group boxes")) return rc;
-    const int kp = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : k <= 8 ? 8 : k <= 16 ? 16 : 32;
     switch (kp) {
         case 1: return launch_select<1>(w, ntile, k, feat, x, y, nbr, stream);
         case 2: return launch_select<2>(w, ntile, k, feat, x, y, nbr, stream);

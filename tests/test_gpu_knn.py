@@ -73,6 +73,14 @@ def test_knn_all_rows_16k(lib):
     check(lib, g["pos"], 1, 16)
 
 
+def test_knn_all_rows_above_brute_force_limit(lib):
+    """Every row of a 20,000-point cloud: above 16,384 points the relation is built and the tiled
+    select runs (below, every query scans every point); both must agree with the oracle."""
+    g = synth.knn_inputs(20000)
+    check(lib, g["pos"], 1, 16)
+    check(lib, cloud("cluster", 17000, 5), 2, 9)
+
+
 def test_knn_non_finite_points(lib):
     pos = cloud("uniform", 700, 3).copy()
     pos[10, 0] = np.nan
