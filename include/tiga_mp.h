@@ -267,7 +267,8 @@ size_t tiga_mp_knn_workspace(int64_t n);
  *          whose d2 is not finite is never selected, so S_i may hold fewer
  *          than k sources;
  *   d2   = fl(fl(fl(dx*dx) + fl(dy*dy)) + fl(dz*dz)), dx = fl(p_j.x - p_i.x), ...
- *   y_i  = sum_{j in S_i} x_j      (fp32 sum in key order)
+ *   y_i  = sum_{j in S_i} x_j      (fp32; terms in key order, added sequentially
+ *          above 16,384 points and by a fixed pairwise tree at or below)
  *   nbr[i][t] = the t-th selected source in key order, -1 past |S_i|.
  * The relation is rebuilt on every call (stateless).
  *   pos: fp32 [n, 3]; x: fp32 [n, feat] (NULL if feat == 0); y: fp32 [n, feat]
