@@ -399,6 +399,30 @@ def paths(args, torch, tb, synth):
     log(f"config 1 fwd+bwd graph replay: {us:.1f} us")
     del rel1, x1, w1, dy1, rev1, graph
 
+    # the paper's own latency workloads on this path: stored CSR, weighted neighbour sum, degree 32,
+    # F = 32 at 8,192 / 32,768 / 131,072 nodes, forward; and the generated radius relation (scalar
+    # distance-weighted sum, nominal degree 32, 131,072 uniform points, rebuilt every call), forward
+    for nn in (8192, 32768, 131072):
+        g = synth.csr_fixed_degree(nn, 32, 32)
+        relp = tb.Csr(dev(g["row_ptr"]), dev(g["col"]), nn)
+        xp, wp = dev(g["x"]), dev(g["w"])
+        r = time_steps(torch, tb, lambda: tb.tiga_mp_csr_fwd(relp, xp, wp), 50, 5)
+        res[f"csr_degree32_{nn}n_f32_sum_fwd"] = dict(ms=r["step_ms"], gedges_per_s=nn * 32 / r["step_ms"] / 1e6)
+        log(f"degree-32 CSR {nn}: {r['step_ms']:.4f} ms")
+        del relp, xp, wp
+    nr = 131072
+    posr = dev(synth.uniform_f32(nr * 3, 0.0, 1.0, (10, 0)).reshape(nr, 3))
+    xr = dev(synth.normal_f32(nr, (10, 1)).reshape(nr, 1))
+    rr_ = synth.radius_for_mean_degree(nr)
+    _, cntr = tb.tiga_mp_radius_fwd(posr, xr, rr_, np.float32(rr_ / np.float32(2)))
+    pairs_r = int(cntr.long().sum().item())
+    r = time_steps(torch, tb, lambda: tb.tiga_mp_radius_fwd(posr, xr, rr_, np.float32(rr_ / np.float32(2)),
+                                                            want_count=False), 50, 5)
+    res["radius_131072_f1_fwd_with_build"] = dict(ms=r["step_ms"], accepted_pairs=pairs_r,
+                                                  gedges_per_s=pairs_r / r["step_ms"] / 1e6)
+    log(f"radius 131072 F=1: {r['step_ms']:.4f} ms")
+    del posr, xr, cntr
+
     g = synth.config2()
     rp, col, n = g["row_ptr"], g["col"], g["num_dst"]
     E = int(rp[-1])

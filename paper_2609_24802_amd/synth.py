@@ -211,6 +211,17 @@ def config4(n: int = 65_536, cfg=4):
     return dict(pos=pos, q=q, eps=np.float32(1e-2))
 
 
+def csr_fixed_degree(num_nodes: int, degree: int, feat: int, cfg: int = 9):
+    """Every destination has `degree` edges from uniform sources (the stored-CSR workload of the
+    paper's latency experiments): x ~ N(0, 1) [num_nodes, feat], w ~ U(0, 1)."""
+    E = num_nodes * degree
+    row_ptr = csr_from_degrees(np.full(num_nodes, degree, dtype=np.int64))
+    col = randint_i32(E, num_nodes, (cfg, num_nodes, 0))
+    w = uniform_f32(E, 0.0, 1.0, (cfg, num_nodes, 1))
+    x = normal_f32(num_nodes * feat, (cfg, num_nodes, 2)).reshape(num_nodes, feat)
+    return dict(row_ptr=row_ptr, col=col, w=w, x=x, num_dst=num_nodes, num_src=num_nodes)
+
+
 def binary_grid_points(n: int, bits: int, key: tuple, span: int | None = None) -> np.ndarray:
     """Points whose coordinates are multiples of 2**-bits in [0, span * 2**-bits)."""
     span = span if span is not None else (1 << bits)
