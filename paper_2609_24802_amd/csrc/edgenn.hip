@@ -274,8 +274,14 @@ int grid_blocks(int64_t n) {
 
 template <int HP, int FP>
 int launch_fwd(int64_t n, const Cells &cl, float r2, const float *x, const Net &net, float *y, hipStream_t stream) {
+    // the forward keeps no per-wavefront partials, so its grid is as large as stays resident
+    // (more wavefronts in flight hide the dependent record and row loads of each point)
+    static const int per_cu = resident_blocks(reinterpret_cast<const void *>(&fwd_kernel<HP, FP>), kBlock);
+    const int64_t cap = static_cast<int64_t>(device_cus()) * per_cu;
+    const int64_t need = ceil_div(n, kBlock / kWave);
+    const int blocks = static_cast<int>(need < cap ? need : cap);
     prof_before(stream);
-    hipLaunchKernelGGL((fwd_kernel<HP, FP>), dim3(grid_blocks(n)), dim3(kBlock), 0, stream, cl.prm, cl.start, cl.rec,
+    hipLaunchKernelGGL((fwd_kernel<HP, FP>), dim3(blocks), dim3(kBlock), 0, stream, cl.prm, cl.start, cl.rec,
                        n, r2, x, net, y);
     prof_after(stream);
     return check_launch("edge MLP forward");
