@@ -117,23 +117,26 @@ def test_rising_maximum_rescales(lib, dtype):
         compare(lib, inp, rel, what=f"rising {dtype} {rel}")
 
 
+@pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
-def test_tile_mass_above_cap(lib, dtype):
-    """Every key of the second 64-key tile scores about 7 (log2 units) above the first tile's
-    maximum: no single weight leaves the 16-bit range, but the tile's mass (about 64 * 2^7) exceeds
-    the fast path's cap, so the reference point must still move before the value product."""
-    n, H, D = 200, 2, 64
-    rng = np.random.default_rng(12)
+def test_tile_mass_above_cap(lib, dtype, D):
+    """Keys 128..255 score about 7 (log2 units) above keys 0..127: a later key tile (the kernel's
+    tiles hold 64 or 128 keys) whose weights all stay inside the 16-bit range, but whose mass
+    (at least 64 * 2^7) exceeds the fast path's cap, so the reference point must still move
+    before the value product."""
+    n, H = 300, 2
+    rng = np.random.default_rng(12 + D)
     q = np.ones((H, n, D), np.float32)
+    unit = np.float32(np.log(2.0) / np.sqrt(D))      # scale * <q, k> = ln 2 per unit of lift
     lift = np.zeros(n, np.float32)
-    lift[64:128] = 7.0 * np.log(2.0) * 8.0 / D        # scale * <q, k> = 7 ln 2 above the first tile
-    lift[128:] = 3.5 * np.log(2.0) * 8.0 / D
-    k = lift[None, :, None] + 0.02 * rng.standard_normal((H, n, D)).astype(np.float32)
+    lift[128:256] = 7.0 * unit
+    lift[256:] = 3.5 * unit
+    k = lift[None, :, None] + 0.02 * rng.standard_normal((H, n, D)).astype(np.float32) / np.sqrt(D)
     v = rng.standard_normal((H, n, D)).astype(np.float32)
     inp = dict(q=synth.f32_to_half_bits(q, dtype), k=synth.f32_to_half_bits(k, dtype),
                v=synth.f32_to_half_bits(v, dtype), scale=np.float32(D ** -0.5), dtype=dtype)
     for rel in ("triangular", "dense"):
-        compare(lib, inp, rel, what=f"tile mass {dtype} {rel}")
+        compare(lib, inp, rel, what=f"tile mass {dtype} D={D} {rel}")
 
 
 def test_paper_layout_view(lib):
