@@ -283,24 +283,19 @@ __device__ __forceinline__ void score_step(f4 (*s)[2], u4 (&ka)[4], const u4 *qr
     }
 }
 
-// One key tile: scores, relation mask, online-softmax update, value and mass products.
-// kaddr[ch] / vr[db] are this lane's LDS addresses of K chunk ch (key block 0) and of V^T output
-// block db within a tile; KOFF / VOFF are the byte offsets of the tile's K and V buffers.
-template <class T, int D, bool CAUSAL, int KOFF, int VOFF>
-__device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][Geo<D>::CH], const uint32_t *kaddr,
-                                          const uint32_t *vr,
-                                          int64_t k0, int64_t n, int64_t qw0, float c, int col, int g, u4 ones) {
+// S^T = K Q^T of one tile for KB blocks of 16 keys x 2 blocks of 16 queries (the K operands read in
+// a rolling window of 4), with the relation applied: keys past n and (triangular) keys after the
+// query get -inf.
+template <class T, int D, bool CAUSAL, int KOFF>
+__device__ __forceinline__ void scores_of(f4 (*s)[2], const u4 (&qreg)[2][Geo<D>::CH], const uint32_t *kaddr,
+                                          int64_t k0, int64_t n, int64_t qw0, int col, int g) {
     using G = Geo<D>;
-    // ---- S^T = K Q^T for KB blocks of 16 keys x 2 blocks of 16 queries, the K operands read in a
-    //      rolling window of 4
-    f4 s[G::KB][2];
     u4 ka[4];
     ka[0] = lds_read_b128<KOFF + 0 * 16 * G::RB>(kaddr[0]);
     ka[1] = lds_read_b128<KOFF + 1 * 16 * G::RB>(kaddr[0]);
     ka[2] = lds_read_b128<KOFF + 2 * 16 * G::RB>(kaddr[0]);
     ka[3] = lds_read_b128<KOFF + 3 * 16 * G::RB>(kaddr[0]);
     score_step<T, D, KOFF, 0>(s, ka, &qreg[0][0], kaddr);
-    // ---- relation: keys past n, and (triangular) keys after the query
     const bool edge = k0 + G::BN > n || (CAUSAL && k0 + G::BN - 1 > qw0);
     if (edge) {
         const int nk = static_cast<int>(n - k0 < G::BN ? n - k0 : G::BN);
@@ -316,14 +311,18 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
                 for (int i = 0; i < 4; ++i) s[kb][qb][i] = kb * 16 + i < rel ? s[kb][qb][i] : -__builtin_inff();
         }
     }
-    // ---- online-softmax state update (Section 4.8), log2 domain.
-    // Fast path: the weights are formed against the current reference point m and the mass of
-    // the tile (an MFMA against an all-ones operand) is checked: a tile mass of at most 2^12 for
-    // every query bounds every weight by 2^12, far inside the 16-bit range.  A larger, infinite
-    // or NaN mass (the first tile, where m = -inf, always) sends the wavefront to the exact path,
-    // which takes the tile's column maximum, rescales (o, l) to the new reference point and forms
-    // the weights again before any value product uses them.
-    u4 pb[G::KC][2];   // [key chunk][query block]: B operands of the second product
+}
+
+// Online-softmax state update of one tile (Section 4.8), log2 domain, producing the weights pb.
+// Fast path: the weights are formed against the current reference point m and the mass of the
+// tile (an MFMA against an all-ones operand) is checked: a tile mass of at most 2^12 for every
+// query bounds every weight by 2^12, far inside the 16-bit range.  A larger, infinite or NaN mass
+// (the first tile, where m = -inf, always) sends the wavefront to the exact path, which takes the
+// tile's column maximum, rescales (o, l) to the new reference point and forms the weights again
+// before any value product uses them.
+template <class T, int D>
+__device__ __forceinline__ void softmax_of(State<T, D> &st, const f4 (*s)[2], u4 (*pb)[2], float c, u4 ones) {
+    using G = Geo<D>;
     f4 ln[2];
     // the weights are the VALU stretch of the tile: issued at raised priority, so that the
     // other wavefront of the SIMD keeps the matrix core busy meanwhile rather than competing
@@ -358,8 +357,13 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
     st.l[0] = ln[0];
     st.l[1] = ln[1];
     __builtin_amdgcn_s_setprio(0);
-    // ---- O^T += V^T P^T; the V^T operand comes from the row-major V tile by transposing reads,
-    //      the operands of block db + 1 being read while the products of block db run
+}
+
+// O^T += V^T P^T of one tile; the V^T operand comes from the row-major V tile by transposing
+// reads, the operands of block db + 1 being read while the products of block db run.
+template <class T, int D, int VOFF>
+__device__ __forceinline__ void values_of(State<T, D> &st, const u4 (*pb)[2], const uint32_t *vr) {
+    using G = Geo<D>;
     u4 va[G::KC], vn[G::KC];
     read_vt<D, VOFF>(vr[0], va);
 #pragma unroll
@@ -379,6 +383,21 @@ __device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][G
 #pragma unroll
         for (int kc = 0; kc < G::KC; ++kc) va[kc] = vn[kc];
     }
+}
+
+// One key tile: scores, relation mask, online-softmax update, value and mass products.
+// kaddr[ch] / vr[db] are this lane's LDS addresses of K chunk ch (key block 0) and of V^T output
+// block db within a tile; KOFF / VOFF are the byte offsets of the tile's K and V buffers.
+template <class T, int D, bool CAUSAL, int KOFF, int VOFF>
+__device__ __forceinline__ void tile_step(State<T, D> &st, const u4 (&qreg)[2][Geo<D>::CH], const uint32_t *kaddr,
+                                          const uint32_t *vr,
+                                          int64_t k0, int64_t n, int64_t qw0, float c, int col, int g, u4 ones) {
+    using G = Geo<D>;
+    f4 s[G::KB][2];
+    u4 pb[G::KC][2];   // [key chunk][query block]: B operands of the second product
+    scores_of<T, D, CAUSAL, KOFF>(s, qreg, kaddr, k0, n, qw0, col, g);
+    softmax_of<T, D>(st, s, pb, c, ones);
+    values_of<T, D, VOFF>(st, pb, vr);
 }
 
 template <class T, int D, bool CAUSAL>
