@@ -51,6 +51,7 @@ struct Ws {
     void *sort;
     f4 *rec;            // [ntile * kTile] Morton-ordered (x, y, z, original index)
     f4 *tlo, *thi;      // [ntile] box of each tile's finite records
+    f4 *slo, *shi;      // [ntile * kTile / 8] box of each run of 8 records (one candidate step)
     f4 *glo, *ghi;      // [ngroup] box of each group of kGroup tiles
 };
 
@@ -66,6 +67,8 @@ Ws carve(Carve &c, int64_t n) {
     w.rec = c.take<f4>(ntile * kTile);
     w.tlo = c.take<f4>(ntile);
     w.thi = c.take<f4>(ntile);
+    w.slo = c.take<f4>(ntile * (kTile / 8));
+    w.shi = c.take<f4>(ntile * (kTile / 8));
     w.glo = c.take<f4>(ceil_div(ntile, kGroup));
     w.ghi = c.take<f4>(ceil_div(ntile, kGroup));
     return w;
@@ -174,19 +177,34 @@ __global__ __launch_bounds__(kBlock) void records_kernel(const float *__restrict
     }
 }
 
-// Box of each tile's finite records (empty tiles: lo = +inf, hi = -inf).
+// Box of each run of 8 records and of each tile, over the finite records (empty: lo = +inf,
+// hi = -inf).  The 8-record boxes are reduced first; the tile box continues from them.
 __global__ __launch_bounds__(kBlock) void tile_box_kernel(const f4 *__restrict__ rec, int64_t ntile,
-                                                          f4 *__restrict__ tlo, f4 *__restrict__ thi) {
+                                                          f4 *__restrict__ tlo, f4 *__restrict__ thi,
+                                                          f4 *__restrict__ slo, f4 *__restrict__ shi) {
     const int64_t t = static_cast<int64_t>(blockIdx.x) * (kBlock / kWave) + threadIdx.x / kWave;
     if (t >= ntile) return;
-    const f4 r = rec[t * kTile + lane_id()];
+    const int lane = lane_id();
+    const f4 r = rec[t * kTile + lane];
     const bool ok = finite3(r.x, r.y, r.z);
     const float inf = __builtin_inff();
-    const float lx = wave_min(ok ? r.x : inf), ly = wave_min(ok ? r.y : inf), lz = wave_min(ok ? r.z : inf);
-    const float hx = wave_max(ok ? r.x : -inf), hy = wave_max(ok ? r.y : -inf), hz = wave_max(ok ? r.z : -inf);
-    if (lane_id() == 0) {
-        tlo[t] = f4{lx, ly, lz, 0.0f};
-        thi[t] = f4{hx, hy, hz, 0.0f};
+    float lo[3] = {ok ? r.x : inf, ok ? r.y : inf, ok ? r.z : inf};
+    float hi[3] = {ok ? r.x : -inf, ok ? r.y : -inf, ok ? r.z : -inf};
+#pragma unroll
+    for (int m = 1; m < kWave; m <<= 1) {
+#pragma unroll
+        for (int a = 0; a < 3; ++a) {
+            lo[a] = fminf(lo[a], __shfl_xor(lo[a], m, kWave));
+            hi[a] = fmaxf(hi[a], __shfl_xor(hi[a], m, kWave));
+        }
+        if (m == 4 && lane % 8 == 0) {
+            slo[t * (kTile / 8) + lane / 8] = f4{lo[0], lo[1], lo[2], 0.0f};
+            shi[t * (kTile / 8) + lane / 8] = f4{hi[0], hi[1], hi[2], 0.0f};
+        }
+    }
+    if (lane == 0) {
+        tlo[t] = f4{lo[0], lo[1], lo[2], 0.0f};
+        thi[t] = f4{hi[0], hi[1], hi[2], 0.0f};
     }
 }
 
@@ -269,7 +287,8 @@ __device__ __forceinline__ void merge_state(uint64_t (&a)[KP], const uint64_t (&
 // lane, because then KP keys of the union already precede it.  Wavefront 0 merges the states.
 template <int KP>
 __global__ __launch_bounds__(kSplit * kWave) void select_kernel(const f4 *__restrict__ rec, const f4 *__restrict__ tlo,
-                                                                const f4 *__restrict__ thi, const f4 *__restrict__ glo,
+                                                                const f4 *__restrict__ thi, const f4 *__restrict__ slo,
+                                                                const f4 *__restrict__ shi, const f4 *__restrict__ glo,
                                                                 const f4 *__restrict__ ghi, int ntile, int k, int feat,
                                                                 const float *__restrict__ x, float *__restrict__ y,
                                                                 int32_t *__restrict__ nbr) {
@@ -311,6 +330,10 @@ __global__ __launch_bounds__(kSplit * kWave) void select_kernel(const f4 *__rest
         const uint64_t cap = (static_cast<uint64_t>(__float_as_uint(tight)) << 32) | 0xffffffffull;
         bool changed = false;
         for (int c0 = 0; c0 < kTile; c0 += 8) {
+            // a run of 8 records whose box no lane could take anything from is skipped (the
+            // query tile too: its query is excluded by index, and its runs skip like any other)
+            const int64_t sb = static_cast<int64_t>(t) * (kTile / 8) + c0 / 8;
+            if (!needed(slo[sb], shi[sb])) continue;
             float d2[8];
             bool any = false;
             // a distance above the lane's tight bound cannot enter (ties go on to the key test)
@@ -493,7 +516,7 @@ template <int KP>
 int launch_select(const Ws &w, int64_t ntile, int k, int feat, const float *x, float *y, int32_t *nbr,
                   hipStream_t stream) {
     prof_before(stream);
-    hipLaunchKernelGGL(select_kernel<KP>, dim3(static_cast<unsigned>(ntile)), dim3(kSplit * kWave), 0, stream, w.rec, w.tlo, w.thi, w.glo, w.ghi,
+    hipLaunchKernelGGL(select_kernel<KP>, dim3(static_cast<unsigned>(ntile)), dim3(kSplit * kWave), 0, stream, w.rec, w.tlo, w.thi, w.slo, w.shi, w.glo, w.ghi,
                        static_cast<int>(ntile), k, feat, x, y, nbr);
     prof_after(stream);
     return check_launch("kNN select");
@@ -540,7 +563,7 @@ int forward(int64_t n, int32_t feat, const float *pos, const float *x, int32_t k
                        stream, pos, w.perm, n, ntile * kTile, w.rec);
     if (int rc = check_launch("kNN records")) return rc;
     hipLaunchKernelGGL(tile_box_kernel, dim3(static_cast<unsigned>(ceil_div(ntile, kBlock / kWave))), dim3(kBlock), 0,
-                       stream, w.rec, ntile, w.tlo, w.thi);
+                       stream, w.rec, ntile, w.tlo, w.thi, w.slo, w.shi);
     if (int rc = check_launch("kNN tile boxes")) return rc;
     const int64_t ngroup = ceil_div(ntile, kGroup);
     hipLaunchKernelGGL(group_box_kernel, dim3(static_cast<unsigned>(ceil_div(ngroup, kBlock / kWave))), dim3(kBlock), 0,
