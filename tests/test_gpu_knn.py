@@ -79,6 +79,8 @@ def test_knn_all_rows_above_brute_force_limit(lib):
     g = synth.knn_inputs(20000)
     check(lib, g["pos"], 1, 16)
     check(lib, cloud("cluster", 17000, 5), 2, 9)
+    # binary-grid coordinates: many equal distances at the box-skip boundaries of tiles and runs
+    check(lib, cloud("grid", 18000, 6), 1, 32)
 
 
 def test_knn_non_finite_points(lib):
