@@ -288,10 +288,8 @@ __device__ __forceinline__ void put_k(float *__restrict__ base, int64_t unit, co
 
 // Phase 1 over every cell of this wave; `flush(cnt, dn, d0, id, first)` runs
 // phase 2 for the destinations d0 .. d0 + dn - 1 (lane d holds the list
-// length `cnt` and point id `id` of destination d).  TWO tests two destinations
-// per candidate step (two independent chains; measured faster for the backward,
-// whose flushes are longer, and slower for the forward).
-template <bool TWO, class Flush>
+// length `cnt` and point id `id` of destination d).
+template <class Flush>
 __device__ __forceinline__ void cell_consume(const Params &p, const int64_t *__restrict__ start,
                                              const float4 *__restrict__ rec, float r2, float neg_inv_s2,
                                              CellList &list, int32_t *__restrict__ count, Flush &&flush) {
@@ -319,66 +317,28 @@ __device__ __forceinline__ void cell_consume(const Params &p, const int64_t *__r
                 for (int k = 0; k < 9; ++k)
                     if (pos >= pre[k]) t = b[k] + (pos - pre[k]);
                 const float4 pj = inr ? rec[t] : make_float4(0.0f, 0.0f, 0.0f, __int_as_float(-1));
-                if constexpr (TWO) {
-                    // two destinations per step: two independent test -> ballot -> count -> append
-                    // chains interleave (a lone last destination tests against itself, unused)
-                    for (int d = 0; d < dn; d += 2) {
-                        const bool two = d + 1 < dn;
-                        const float4 pa = rec[d0 + d];                    // uniform addresses: scalar loads
-                        const float4 pb = rec[d0 + (two ? d + 1 : d)];
-                        float da, db;
-                        const bool oka = inr & accept(pa, pj, r2, da) & (__float_as_int(pj.w) != __float_as_int(pa.w));
-                        const bool okb = two & inr & accept(pb, pj, r2, db) & (__float_as_int(pj.w) != __float_as_int(pb.w));
-                        const uint64_t ma = __builtin_amdgcn_ballot_w64(oka);
-                        const uint64_t mb = __builtin_amdgcn_ballot_w64(okb);
-                        if ((ma | mb) == 0) continue;
-                        const int na = __popcll(ma), nb = __popcll(mb);
-                        int ca = __builtin_amdgcn_readlane(cnt, d);
-                        int cb = two ? __builtin_amdgcn_readlane(cnt, d + 1) : 0;
-                        if (ca + na > kCapC || cb + nb > kCapC) {
-                            tot += cnt;
-                            flush(cnt, dn, d0, idl, first);
-                            first = false;
-                            cnt = 0;
-                            ca = 0;
-                            cb = 0;
-                        }
-                        if (oka) {
-                            const int pfx = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(ma >> 32),
-                                                                      __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(ma), 0));
-                            list[d][ca + pfx] = make_float2(pj.w, __expf(da * neg_inv_s2));  // (point id, weight)
-                        }
-                        if (okb) {
-                            const int pfx = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mb >> 32),
-                                                                      __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mb), 0));
-                            list[d + 1][cb + pfx] = make_float2(pj.w, __expf(db * neg_inv_s2));
-                        }
-                        cnt = lane == d ? ca + na : (two && lane == d + 1 ? cb + nb : cnt);
+                for (int d = 0; d < dn; ++d) {
+                    const float4 pd = rec[d0 + d];  // uniform address: a scalar load
+                    float d2;
+                    const bool near = accept(pd, pj, r2, d2);
+                    const bool ok = inr & near & (__float_as_int(pj.w) != __float_as_int(pd.w));
+                    const uint64_t mask = __builtin_amdgcn_ballot_w64(ok);
+                    if (mask == 0) continue;
+                    const int nnew = __popcll(mask);
+                    int cd = __builtin_amdgcn_readlane(cnt, d);
+                    if (cd + nnew > kCapC) {
+                        tot += cnt;
+                        flush(cnt, dn, d0, idl, first);
+                        first = false;
+                        cnt = 0;
+                        cd = 0;
                     }
-                } else {
-                    for (int d = 0; d < dn; ++d) {
-                        const float4 pd = rec[d0 + d];  // uniform address: a scalar load
-                        float d2;
-                        const bool near = accept(pd, pj, r2, d2);
-                        const bool ok = inr & near & (__float_as_int(pj.w) != __float_as_int(pd.w));
-                        const uint64_t mask = __builtin_amdgcn_ballot_w64(ok);
-                        if (mask == 0) continue;
-                        const int nnew = __popcll(mask);
-                        int cd = __builtin_amdgcn_readlane(cnt, d);
-                        if (cd + nnew > kCapC) {
-                            tot += cnt;
-                            flush(cnt, dn, d0, idl, first);
-                            first = false;
-                            cnt = 0;
-                            cd = 0;
-                        }
-                        if (ok) {
-                            const int pfx = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
-                                                                      __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0));
-                            list[d][cd + pfx] = make_float2(pj.w, __expf(d2 * neg_inv_s2));  // (point id, weight)
-                        }
-                        cnt = lane == d ? cd + nnew : cnt;
+                    if (ok) {
+                        const int pfx = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                                                  __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0));
+                        list[d][cd + pfx] = make_float2(pj.w, __expf(d2 * neg_inv_s2));  // (point id, weight)
                     }
+                    cnt = lane == d ? cd + nnew : cnt;
                 }
             }
             tot += cnt;
@@ -472,7 +432,7 @@ __global__ __launch_bounds__(kBlock) void radius_fwd_cell_kernel(const Params *_
         }
         lds_fence();
     };
-    cell_consume<false>(p, start, rec, r2, neg_inv_s2, list, count, flush);
+    cell_consume(p, start, rec, r2, neg_inv_s2, list, count, flush);
 }
 
 // Backward on the same schedule: dx_i = sum_j k_ij dy_j and
@@ -618,7 +578,7 @@ __global__ __launch_bounds__(kBlock) void radius_bwd_cell_kernel(const Params *_
         }
         lds_fence();
     };
-    cell_consume<true>(p, start, rec, r2, neg_inv_s2, list, nullptr, flush);
+    cell_consume(p, start, rec, r2, neg_inv_s2, list, nullptr, flush);
 }
 
 __global__ __launch_bounds__(kBlock) void neighbor_count_kernel(const Params *__restrict__ prm,
