@@ -235,8 +235,9 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(const Params *__restrict__ 
 }
 
 // Sum the per-wavefront partials into the parameter gradients in two fixed-order stages: each of
-// kGroups groups of wavefronts per parameter (consecutive wavefronts, in order), then the groups.
-constexpr int kGroups = 32;
+// kGroups groups of wavefronts per parameter (consecutive wavefronts, in order), then the groups;
+// 64 x 64 balances the two stages' serial sums for 4096 partials.
+constexpr int kGroups = 64;
 
 __global__ __launch_bounds__(kWave) void reduce_groups_kernel(const float *__restrict__ part, int64_t nw, int64_t P,
                                                               float *__restrict__ grp) {
