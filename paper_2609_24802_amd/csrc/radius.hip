@@ -200,10 +200,6 @@ __device__ __forceinline__ void lds_fence() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
-__device__ __forceinline__ float readlane_f(float v, int l) {
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
-}
-
 // Cells of XCD (blockIdx.x % 8) form one contiguous range, strided over that
 // XCD's waves, so neighbouring cells are consumed under one L2.  The grid is a
 // multiple of 8 blocks.
