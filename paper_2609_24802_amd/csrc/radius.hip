@@ -345,9 +345,12 @@ __device__ __forceinline__ void cell_consume(const Params &p, const int64_t *__r
 }
 
 // y_i = sum_j k_ij x_j; K floats per unit, LPR lanes per row, UPL units per
-// lane per feature block.
+// lane per feature block. The pair loop is latency-bound, so the one-unit
+// forms are held to 72 registers (7 waves per SIMD instead of 6); the few
+// values this spills cost less than the extra wave gains. The two-unit form
+// would spill dozens and keeps its registers.
 template <int K, int LPR, int UPL>
-__global__ __launch_bounds__(kBlock) void radius_fwd_cell_kernel(const Params *__restrict__ prm,
+__global__ __launch_bounds__(kBlock, UPL == 1 ? 7 : 1) void radius_fwd_cell_kernel(const Params *__restrict__ prm,
                                                                  const int64_t *__restrict__ start,
                                                                  const float4 *__restrict__ rec,
                                                                  const float *__restrict__ xs, int64_t fu, float r2,
