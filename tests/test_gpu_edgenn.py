@@ -54,7 +54,8 @@ def check(lib, pos, x, radius, prm, dy):
 
 @pytest.mark.parametrize("n,F,H,O,r", [(300, 8, 16, 4, 0.15), (500, 0, 32, 3, 0.12), (400, 3, 5, 1, 0.13),
                                        (600, 32, 32, 3, 0.1), (256, 64, 64, 8, 0.2), (350, 16, 64, 2, 0.14),
-                                       (1, 8, 32, 3, 0.1), (2000, 8, 32, 3, 0.06), (900, 12, 20, 5, 0.09)])
+                                       (1, 8, 32, 3, 0.1), (2000, 8, 32, 3, 0.06), (900, 12, 20, 5, 0.09),
+                                       (700, 24, 12, 2, 0.11)])
 def test_edgenn_against_oracle(lib, n, F, H, O, r):
     check(lib, *case(n, F, H, O, r, seed=n + F + H))
 
