@@ -168,8 +168,8 @@ size_t tiga_mp_csr_bwd_workspace(const tiga_csr *rel, int32_t feat, int reducer)
  * either may be NULL (skipped) and each is overwritten.  dw requires
  * TIGA_MSG_EDGE_SCALED_SRC.
  * rev == NULL: dx accumulates with device fp32 atomics: no set-up, summation
- *   order not fixed, and bound by the atomics (at feat = 64 about six times
- *   slower than the gather mode).
+ *   order not fixed, and bound by the atomics (at feat = 64 a little over twice
+ *   the time of the gather mode).
  * rev != NULL: dx is gathered over the reverse incidence (deterministic); build
  *   it once per topology with tiga_csr_transpose.
  * Errors: as tiga_mp_csr_fwd. */

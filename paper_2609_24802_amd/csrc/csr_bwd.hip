@@ -39,6 +39,24 @@ __device__ __forceinline__ void edge_pass(const EdgeT &t, int64_t row, int64_t e
         g = load_unit<K>(t.dy, row * t.fu + u);
         if constexpr (RED == RED_MAX) load_unit_i<K>(t.arg, row * t.fu + u, ga);
     }
+    // dx is scattered lane-contiguously: atomic k of lane l adds to float f0 + k L of the source
+    // row, f0 = (u - l) K + l. Over the L lanes and K atomics this covers exactly the K L floats of
+    // units u - l .. u - l + L - 1, and each atomic instruction of an edge writes one contiguous
+    // run of L floats instead of L floats spaced K apart.
+    const int64_t nf = t.fu * K, f0 = (u - l) * K + l;
+    float gt[K];
+    int gat[K];
+    bool fok[K];
+    if constexpr (DX) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const int64_t f = f0 + static_cast<int64_t>(k) * L;
+            fok[k] = f < nf && e1 > e0;
+            gt[k] = fok[k] ? t.dy[row * nf + f] : 0.0f;
+            gat[k] = -1;
+            if constexpr (RED == RED_MAX) gat[k] = fok[k] ? t.arg[row * nf + f] : -1;
+        }
+    }
     for (int64_t base = e0; base < e1; base += SL * kUnroll) {
         int32_t c[kUnroll];
         float wv[kUnroll];
@@ -64,11 +82,12 @@ __device__ __forceinline__ void edge_pass(const EdgeT &t, int64_t row, int64_t e
         for (int r = 0; r < kUnroll; ++r) {
             const int64_t e = base + static_cast<int64_t>(r) * SL + s;
             if constexpr (DX) {
-                if (ok[r] && uok) {
-                    float *dst = t.dx + (static_cast<int64_t>(c[r]) * t.fu + u) * K;
+                if (ok[r]) {
+                    float *dst = t.dx + static_cast<int64_t>(c[r]) * nf + f0;
 #pragma unroll
                     for (int k = 0; k < K; ++k)
-                        if (RED == RED_SUM || ga[k] == static_cast<int>(e)) unsafeAtomicAdd(dst + k, wv[r] * g.v[k]);
+                        if (fok[k] && (RED == RED_SUM || gat[k] == static_cast<int>(e)))
+                            unsafeAtomicAdd(dst + k * L, wv[r] * gt[k]);
                 }
             }
             if constexpr (DW) {

@@ -130,6 +130,27 @@ def test_max_forward_backward_exact(lib, F):
         assert_terms_close(host(dw), rdw, rdwa, what=f"max dw F={F}")
 
 
+@pytest.mark.parametrize("F", [12, 20, 44, 260])
+def test_atomic_backward_ragged_unit_blocks(lib, F):
+    """Atomic-mode dx at widths whose last block of 16-byte units is partly outside the row: the
+    lane-contiguous scatter must cover exactly the row's F floats. Integer inputs make every sum
+    exact, so the order of the atomics does not matter."""
+    deg = mixed_degrees(700, 300 + F, big=(9000,))
+    row_ptr, col, x, w, dy = make_graph(deg, 900, F, seed=F + 31, integer=True)
+    rel, _, _ = run_fwd(lib, row_ptr, col, x, w, 900, lib.REDUCE_SUM)
+    rdx, _, rdw, _ = oracle.csr_sum_bwd(row_ptr, col, x, w, dy, 900)
+    dx, dw = lib.tiga_mp_csr_bwd(rel, dev(dy), dev(x), dev(w))
+    assert np.array_equal(host(dx), rdx.astype(np.float32))
+    assert np.array_equal(host(dw), rdw.astype(np.float32))
+    _, _, arg = run_fwd(lib, row_ptr, col, x, w, 900, lib.REDUCE_MAX)
+    _, rarg = oracle.csr_max_fwd(row_ptr, col, x, w)
+    assert np.array_equal(arg, rarg)
+    mdx, _, mdw, _ = oracle.csr_max_bwd(row_ptr, col, x, w, rarg, dy, 900)
+    dx, dw = lib.tiga_mp_csr_bwd(rel, dev(dy), dev(x), dev(w), reducer=lib.REDUCE_MAX, argmax=dev(arg))
+    assert np.array_equal(host(dx), mdx.astype(np.float32))
+    assert np.array_equal(host(dw), mdw.astype(np.float32))
+
+
 def test_max_ties_and_signed_zeros(lib):
     # duplicated edges with equal weights, all-zero rows of x, and w = 0 with
     # negative x (a -0 message) next to +0 messages
