@@ -99,56 +99,100 @@ __global__ __launch_bounds__(kBlock) void radix_hist_kernel(const int32_t *__res
     counts[static_cast<int64_t>(threadIdx.x) * nblocks + blockIdx.x] = hist[threadIdx.x];
 }
 
-// Stable scatter.  Elements of a tile are ranked in (round, wave, lane) order,
-// which is their input order; equal digits keep that order.  The second
+// Stable scatter through LDS.  The tile's elements are ranked in (round, wave,
+// lane) order, which is their input order, and placed in LDS grouped by digit;
+// the block then writes each digit's run of the tile with consecutive lanes on
+// consecutive addresses (a tile of 2048 elements holds about 8 per digit, so the
+// stores come in runs instead of one element per digit and round).  The second
 // payload is optional (null in and out).
 __global__ __launch_bounds__(kBlock) void radix_scatter_kernel(
     const int32_t *__restrict__ keys_in, const int32_t *__restrict__ v0_in, const int32_t *__restrict__ v1_in,
     int32_t *__restrict__ keys_out, int32_t *__restrict__ v0_out, int32_t *__restrict__ v1_out, int64_t n,
     int shift, int64_t nblocks, const int64_t *__restrict__ offsets, int iota_v0) {
-    __shared__ int64_t run[kRadix];
+    __shared__ int64_t run[kRadix];   // output position of this tile's first element of each digit
+    __shared__ int first[kRadix];     // LDS slot of this tile's first element of each digit
+    __shared__ int fill[kRadix];      // digit counts, then elements of each digit placed so far
+    __shared__ int wsum[kWavesPerBlock];
     __shared__ int wcnt[kWavesPerBlock][kRadix];
-    run[threadIdx.x] = offsets[static_cast<int64_t>(threadIdx.x) * nblocks + blockIdx.x];
+    __shared__ int32_t sk[kSortTile], sa[kSortTile], sb[kSortTile];
+    const int t = threadIdx.x;
     const int lane = lane_id();
-    const int wave = threadIdx.x / kWave;
+    const int wave = t / kWave;
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kSortTile;
+    const int total = static_cast<int>(n - base < kSortTile ? n - base : kSortTile);
+    run[t] = offsets[static_cast<int64_t>(t) * nblocks + blockIdx.x];
+    fill[t] = 0;
+    __syncthreads();
+    int32_t key[kSortItems], a[kSortItems], b[kSortItems];
+    int digit[kSortItems];
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+        const int j = r * kBlock + t;
+        key[r] = a[r] = b[r] = 0;
+        digit[r] = 0;
+        if (j < total) {
+            const int64_t i = base + j;
+            key[r] = keys_in[i];
+            a[r] = iota_v0 ? static_cast<int32_t>(i) : v0_in[i];
+            b[r] = v1_in ? v1_in[i] : 0;
+            digit[r] = (static_cast<uint32_t>(key[r]) >> shift) & (kRadix - 1);
+            atomicAdd(&fill[digit[r]], 1);
+        }
+    }
+    __syncthreads();
+    // exclusive scan of the tile's digit counts, thread t = digit t
+    const int cnt = fill[t];
+    int incl = cnt;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int v = __shfl_up(incl, o);
+        if (lane >= o) incl += v;
+    }
+    if (lane == kWave - 1) wsum[wave] = incl;
+    __syncthreads();
+    int before = 0;
+    for (int w = 0; w < wave; ++w) before += wsum[w];
+    first[t] = before + incl - cnt;
+    fill[t] = 0;
     for (int r = 0; r < kSortItems; ++r) {
 #pragma unroll
-        for (int w = 0; w < kWavesPerBlock; ++w) wcnt[w][threadIdx.x] = 0;
+        for (int w = 0; w < kWavesPerBlock; ++w) wcnt[w][t] = 0;
         __syncthreads();
-        const int64_t i = base + r * kBlock + threadIdx.x;
-        const bool valid = i < n;
-        int32_t key = 0, a = 0, b = 0;
-        int digit = 0;
-        if (valid) {
-            key = keys_in[i];
-            a = iota_v0 ? static_cast<int32_t>(i) : v0_in[i];
-            b = v1_in ? v1_in[i] : 0;
-            digit = (static_cast<uint32_t>(key) >> shift) & (kRadix - 1);
-        }
+        const bool valid = r * kBlock + t < total;
         uint64_t peers = __ballot(valid);
 #pragma unroll
         for (int bit = 0; bit < kRadixBits; ++bit) {
-            const uint64_t m = __ballot((digit >> bit) & 1);
-            peers &= ((digit >> bit) & 1) ? m : ~m;
+            const uint64_t m = __ballot((digit[r] >> bit) & 1);
+            peers &= ((digit[r] >> bit) & 1) ? m : ~m;
         }
         const int rank = __popcll(peers & lt_mask);
-        if (valid && rank == 0) wcnt[wave][digit] = __popcll(peers);
+        if (valid && rank == 0) wcnt[wave][digit[r]] = __popcll(peers);
         __syncthreads();
         if (valid) {
-            int64_t pos = run[digit] + rank;
-            for (int w = 0; w < wave; ++w) pos += wcnt[w][digit];
-            keys_out[pos] = key;
-            v0_out[pos] = a;
-            if (v1_out) v1_out[pos] = b;
+            const int d = digit[r];
+            int slot = first[d] + fill[d] + rank;
+            for (int w = 0; w < wave; ++w) slot += wcnt[w][d];
+            sk[slot] = key[r];
+            sa[slot] = a[r];
+            sb[slot] = b[r];
         }
         __syncthreads();
-        int64_t add = 0;
+        int add = 0;
 #pragma unroll
-        for (int w = 0; w < kWavesPerBlock; ++w) add += wcnt[w][threadIdx.x];
-        run[threadIdx.x] += add;
-        __syncthreads();
+        for (int w = 0; w < kWavesPerBlock; ++w) add += wcnt[w][t];
+        fill[t] += add;
+    }
+    __syncthreads();
+    for (int slot = t; slot < total; slot += kBlock) {
+        const int32_t k = sk[slot];
+        const int d = (static_cast<uint32_t>(k) >> shift) & (kRadix - 1);
+        const int64_t pos = run[d] + (slot - first[d]);
+        if (pos < n) {
+            keys_out[pos] = k;
+            v0_out[pos] = sa[slot];
+            if (v1_out) v1_out[pos] = sb[slot];
+        }
     }
 }
 

@@ -151,6 +151,32 @@ def test_atomic_backward_ragged_unit_blocks(lib, F):
     assert np.array_equal(host(dw), mdw.astype(np.float32))
 
 
+@pytest.mark.parametrize("num_src,hot", [(3_000_000, 40), (200, 0), (70_000, 5)])
+def test_transpose_is_a_stable_sort_by_source(lib, num_src, hot):
+    """The reverse incidence lists each source's edges in forward-edge order: numpy's stable
+    argsort of col fixes edge_id, dst_idx and src_ptr exactly (1 to 3 radix passes, many tiles,
+    a ragged last tile, and hot sources whose runs span tiles)."""
+    rng = np.random.default_rng(num_src + hot)
+    deg = rng.integers(0, 9, 40_000)
+    deg[rng.integers(0, deg.size, 30)] = 3000
+    rp = np.zeros(deg.size + 1, np.int64)
+    np.cumsum(deg, out=rp[1:])
+    e = int(rp[-1])
+    col = rng.integers(0, num_src, e).astype(np.int32)
+    if hot:
+        pick = rng.random(e) < 0.3
+        col[pick] = rng.integers(0, hot, int(pick.sum()))
+    rev = lib.tiga_csr_transpose(lib.Csr(dev(rp), dev(col), num_src))
+    torch.cuda.synchronize()
+    order = np.argsort(col, kind="stable")
+    rows = np.repeat(np.arange(deg.size, dtype=np.int32), deg)
+    ptr = np.zeros(num_src + 1, np.int64)
+    np.cumsum(np.bincount(col, minlength=num_src), out=ptr[1:])
+    assert np.array_equal(host(rev.edge_id), order.astype(np.int32))
+    assert np.array_equal(host(rev.dst_idx), rows[order])
+    assert np.array_equal(host(rev.src_ptr), ptr)
+
+
 def test_max_ties_and_signed_zeros(lib):
     # duplicated edges with equal weights, all-zero rows of x, and w = 0 with
     # negative x (a -0 message) next to +0 messages
