@@ -55,8 +55,7 @@ def _load():
                 "tiga_oracle_radius_bwd": (C.c_int, [i64, i32, vp, vp, vp, f32, f32, i64, vp, vp, vp, vp, vp]),
                 "tiga_oracle_radius_neighbors": (C.c_int, [i64, vp, f32, i64, vp, vp, vp, vp]),
                 "tiga_oracle_dense_fwd": (None, [i64, vp, vp, f32, i64, vp, vp, vp]),
-                "tiga_oracle_edgenn": (None, [i64, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
-                                              vp, vp, vp, vp]),
+                "tiga_oracle_edgenn": (None, [i64, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
                 "tiga_oracle_knn": (C.c_int, [i64, i32, vp, vp, i32, i64, vp, vp, vp, vp]),
                 "tiga_oracle_f16_to_double": (C.c_double, [C.c_uint16]),
                 "tiga_oracle_bf16_to_double": (C.c_double, [C.c_uint16]),
@@ -250,9 +249,16 @@ def knn(pos, x, k, pts=None):
     return nbr, y, ya
 
 
-def edgenn(pos, x, ptr, idx, W1, b1, W2, b2, dy=None):
+_EDGENN_OUTS = ("y", "dx", "dp", "dW1", "db1", "dW2", "db2")
+
+
+def edgenn(pos, x, ptr, idx, W1, b1, W2, b2, dy=None, terms=False):
     """Edge-local MLP message summed per destination over the relation (ptr, idx); with dy also the
-    gradients of <dy, y>.  Returns dict(y, dx, dp, dW1, db1, dW2, db2) in fp64."""
+    gradients of <dy, y>.  Returns dict(y, dx, dp, dW1, db1, dW2, db2) in fp64.
+
+    With terms=True returns (values, mag, slack), three such dicts: mag is each output's
+    absolute-value evaluation with the oracle's ReLU decisions held (the error bound of any fp32
+    evaluation order), slack what reaches the output through ReLU decisions fp32 cannot settle."""
     pos, x = _c(pos, np.float32).reshape(-1, 3), _c(x, np.float32)
     n = pos.shape[0]
     x = x.reshape(n, -1)
@@ -262,11 +268,21 @@ def edgenn(pos, x, ptr, idx, W1, b1, W2, b2, dy=None):
     assert W1.shape == (H, 3 + F) and b1.shape == (H,) and W2.shape == (O, H) and b2.shape == (O,)
     ptr, idx = _c(ptr, np.int64), _c(idx, np.int32)
     dy = _c(dy, np.float32)
-    out = dict(y=np.empty((n, O)))
-    if dy is not None:
-        out.update(dx=np.empty((n, F)), dp=np.empty((n, 3)), dW1=np.empty((H, 3 + F)), db1=np.empty(H),
-                   dW2=np.empty((O, H)), db2=np.empty(O))
-    g = lambda k: _p(out.get(k))
+    shapes = dict(y=(n, O), dx=(n, F), dp=(n, 3), dW1=(H, 3 + F), db1=(H,), dW2=(O, H), db2=(O,))
+    keys = _EDGENN_OUTS if dy is not None else ("y",)
+
+    def outs():
+        return {k: np.empty(shapes[k]) for k in keys}
+
+    def table(d):
+        return (C.c_void_p * 7)(*[_p(d.get(k)) for k in _EDGENN_OUTS])
+
+    val = outs()
+    mag = outs() if terms else None
+    slack = outs() if terms else None
+    tv = table(val)
+    tm = table(mag) if terms else None
+    ts = table(slack) if terms else None
     _load().tiga_oracle_edgenn(n, F, H, O, _p(pos), _p(x), _p(ptr), _p(idx), _p(W1), _p(b1), _p(W2), _p(b2),
-                               _p(dy), g("y"), g("dx"), g("dp"), g("dW1"), g("db1"), g("dW2"), g("db2"))
-    return out
+                               _p(dy), tv, tm, ts)
+    return (val, mag, slack) if terms else val

@@ -520,10 +520,14 @@ int tiga_oracle_radius_neighbors(int64_t n, const float *pos, float radius, int6
 /* ------------------------------------------------------------------------ */
 
 /* Softened inverse-square message summed over all j != i:
- *   y_i = sum_{j != i} q_j (p_j - p_i) / (|p_j - p_i|^2 + eps^2)^(3/2). */
+ *   y_i = sum_{j != i} q_j (p_j - p_i) / (|p_j - p_i|^2 + eps^2)^(3/2).
+ * The softening constant is given as the fp32 value eps; its square enters as
+ * the fp32 product eps*eps (one rounding), the constant a single-precision
+ * implementation of the message is handed.  Everything else is fp64. */
 void tiga_oracle_dense_fwd(int64_t n, const float *pos, const float *q, float eps,
                            int64_t npts, const int64_t *pts, double *y, double *yabs) {
-    double e2 = (double)eps * (double)eps;
+    const float e2f = eps * eps;
+    const double e2 = (double)e2f;
     int64_t k;
 #pragma omp parallel for schedule(dynamic, 16)
     for (k = 0; k < npts; ++k) {
@@ -549,7 +553,7 @@ void tiga_oracle_dense_fwd(int64_t n, const float *pos, const float *q, float ep
 
 /* ------------------------------------------------------------------------ */
 /* Online-softmax reducer over an implicit triangular or dense relation      */
-/* (Section 4.8, online softmax; appendix "Causal attention as message       */
+/* (Section 5.2, online softmax; appendix "Causal attention as message       */
 /* passing")                                                                 */
 /* ------------------------------------------------------------------------ */
 
@@ -724,75 +728,154 @@ int tiga_oracle_knn(int64_t n, int32_t F, const float *pos, const float *x, int3
  *   m_ij  = W2 r_ij + b2                            (O values; the final bias is
  *                                                    part of every message)
  *   y_i   = sum_{j in row i} m_ij                   (an empty row gives 0)
- * W1 is [H][3 + F], b1 [H], W2 [O][H], b2 [O], all fp32 row-major; y is fp64
- * [n][O].  If dy ([n][O], fp32) is given, the gradients of L = sum_i <dy_i, y_i>
- * with the relation held fixed are formed as well (fp64, each may be NULL):
+ * W1 is [H][3 + F], b1 [H], W2 [O][H], b2 [O], all fp32 row-major.  If dy
+ * ([n][O], fp32) is given, the gradients of L = sum_i <dy_i, y_i> with the
+ * relation held fixed are formed as well:
  *   dm = dy_i;  dW2 += dm r^T;  db2 += dm;  da = (W2^T dm) * [a > 0];
  *   dW1 += da in^T;  db1 += da;  din = W1^T da;
  *   dp_j += din[0..3);  dp_i -= din[0..3);  dx_j += din[3..3+F).
- * The derivative of max(a, 0) at a = 0 is taken as 0.  Serial over destinations
- * in ascending order. */
+ * The derivative of max(a, 0) at a = 0 is taken as 0.  Serial over
+ * destinations in ascending order; all arithmetic fp64.
+ *
+ * Outputs come as three arrays of seven pointers, in the order
+ *   y [n][O], dx [n][F], dp [n][3], dW1 [H][3+F], db1 [H], dW2 [O][H], db2 [O]
+ * (any pointer, or the whole mag / slack array, may be NULL):
+ *   val:   the values above;
+ *   mag:   for every output, its absolute-value evaluation with this oracle's
+ *          ReLU decisions held: every input, weight, bias and cotangent is
+ *          replaced by its absolute value, the output of an active unit by the
+ *          absolute-value evaluation of its pre-activation
+ *          aa = |b1| + sum_c |W1[h][c]| |in_c|, and an inactive unit
+ *          contributes nothing.  It bounds the rounding error of any fp32
+ *          evaluation order, as the sum of |terms| does for a plain sum;
+ *   slack: the absolute-value evaluation of what reaches the output through
+ *          units whose ReLU decision fp32 cannot settle, |a| <= 2^-14 aa (an
+ *          fp32 evaluation of a with up to 3 + F + 1 roundings is off by at
+ *          most about 2^-17 aa), taken as if the unit were active.  A unit's
+ *          decision flipping changes an output by at most its slack. */
+enum { EN_Y, EN_DX, EN_DP, EN_DW1, EN_DB1, EN_DW2, EN_DB2, EN_OUTS };
+
+static void en_zero(double *p, int64_t count) {
+    if (p) memset(p, 0, sizeof(double) * (size_t)count);
+}
+
 void tiga_oracle_edgenn(int64_t n, int32_t F, int32_t H, int32_t O, const float *pos, const float *x,
                         const int64_t *ptr, const int32_t *idx, const float *W1, const float *b1,
-                        const float *W2, const float *b2, const float *dy, double *y, double *dx,
-                        double *dp, double *dW1, double *db1, double *dW2, double *db2) {
+                        const float *W2, const float *b2, const float *dy, double *const *val,
+                        double *const *mag, double *const *slack) {
     const int32_t D = 3 + F;
+    const double unsettled = ldexp(1.0, -14);
+    const int64_t sizes[EN_OUTS] = {n * O, n * F, n * 3, (int64_t)H * D, H, (int64_t)O * H, O};
+    double *v[EN_OUTS], *m[EN_OUTS], *sl[EN_OUTS];
+    for (int k = 0; k < EN_OUTS; ++k) {
+        v[k] = val ? val[k] : NULL;
+        m[k] = mag ? mag[k] : NULL;
+        sl[k] = slack ? slack[k] : NULL;
+        en_zero(v[k], sizes[k]);
+        en_zero(m[k], sizes[k]);
+        en_zero(sl[k], sizes[k]);
+    }
     double *in = (double *)malloc(sizeof(double) * (size_t)D);
+    double *ina = (double *)malloc(sizeof(double) * (size_t)D);
     double *a = (double *)malloc(sizeof(double) * (size_t)H);
+    double *aa = (double *)malloc(sizeof(double) * (size_t)H);
     double *da = (double *)malloc(sizeof(double) * (size_t)H);
-    if (y) memset(y, 0, sizeof(double) * (size_t)(n * O));
-    if (dx) memset(dx, 0, sizeof(double) * (size_t)(n * F));
-    if (dp) memset(dp, 0, sizeof(double) * (size_t)(n * 3));
-    if (dW1) memset(dW1, 0, sizeof(double) * (size_t)(H * D));
-    if (db1) memset(db1, 0, sizeof(double) * (size_t)H);
-    if (dW2) memset(dW2, 0, sizeof(double) * (size_t)(O * H));
-    if (db2) memset(db2, 0, sizeof(double) * (size_t)O);
+    double *ga = (double *)malloc(sizeof(double) * (size_t)H);
     for (int64_t i = 0; i < n; ++i) {
         for (int64_t e = ptr[i]; e < ptr[i + 1]; ++e) {
             const int64_t j = idx[e];
             for (int c = 0; c < 3; ++c) in[c] = (double)pos[j * 3 + c] - (double)pos[i * 3 + c];
             for (int c = 0; c < F; ++c) in[3 + c] = (double)x[j * F + c];
+            for (int c = 0; c < D; ++c) ina[c] = fabs(in[c]);
             for (int h = 0; h < H; ++h) {
-                double s = (double)b1[h];
-                for (int c = 0; c < D; ++c) s += (double)W1[h * D + c] * in[c];
-                a[h] = s;
-            }
-            if (y)
-                for (int o = 0; o < O; ++o) {
-                    double s = (double)b2[o];
-                    for (int h = 0; h < H; ++h) s += (double)W2[o * H + h] * (a[h] > 0.0 ? a[h] : 0.0);
-                    y[i * O + o] += s;
+                double s = (double)b1[h], sa = fabs((double)b1[h]);
+                for (int c = 0; c < D; ++c) {
+                    s += (double)W1[h * D + c] * in[c];
+                    sa += fabs((double)W1[h * D + c]) * ina[c];
                 }
+                a[h] = s;
+                aa[h] = sa;
+            }
+#define ACTIVE(h) (a[h] > 0.0)
+#define UNSETTLED(h) (fabs(a[h]) <= unsettled * aa[h])
+            /* forward */
+            for (int o = 0; o < O; ++o) {
+                double s = (double)b2[o], sa = fabs((double)b2[o]), su = 0.0;
+                for (int h = 0; h < H; ++h) {
+                    const double w2 = (double)W2[o * H + h];
+                    s += w2 * (ACTIVE(h) ? a[h] : 0.0);
+                    sa += fabs(w2) * (ACTIVE(h) ? aa[h] : 0.0);
+                    if (UNSETTLED(h)) su += fabs(w2) * aa[h];
+                }
+                if (v[EN_Y]) v[EN_Y][i * O + o] += s;
+                if (m[EN_Y]) m[EN_Y][i * O + o] += sa;
+                if (sl[EN_Y]) sl[EN_Y][i * O + o] += su;
+            }
             if (!dy) continue;
             const float *dm = dy + i * O;
             for (int o = 0; o < O; ++o) {
-                if (dW2)
-                    for (int h = 0; h < H; ++h) dW2[o * H + h] += (double)dm[o] * (a[h] > 0.0 ? a[h] : 0.0);
-                if (db2) db2[o] += (double)dm[o];
+                const double g = (double)dm[o], gabs = fabs(g);
+                for (int h = 0; h < H; ++h) {
+                    if (v[EN_DW2]) v[EN_DW2][o * H + h] += g * (ACTIVE(h) ? a[h] : 0.0);
+                    if (m[EN_DW2]) m[EN_DW2][o * H + h] += gabs * (ACTIVE(h) ? aa[h] : 0.0);
+                    if (sl[EN_DW2] && UNSETTLED(h)) sl[EN_DW2][o * H + h] += gabs * aa[h];
+                }
+                if (v[EN_DB2]) v[EN_DB2][o] += g;
+                if (m[EN_DB2]) m[EN_DB2][o] += gabs;
             }
             for (int h = 0; h < H; ++h) {
-                double s = 0.0;
-                for (int o = 0; o < O; ++o) s += (double)W2[o * H + h] * (double)dm[o];
-                da[h] = a[h] > 0.0 ? s : 0.0;
-                if (db1) db1[h] += da[h];
-                if (dW1)
-                    for (int c = 0; c < D; ++c) dW1[h * D + c] += da[h] * in[c];
-            }
-            for (int c = 0; c < D; ++c) {
-                double s = 0.0;
-                for (int h = 0; h < H; ++h) s += (double)W1[h * D + c] * da[h];
-                if (c < 3) {
-                    if (dp) {
-                        dp[j * 3 + c] += s;
-                        dp[i * 3 + c] -= s;
-                    }
-                } else if (dx) {
-                    dx[j * F + (c - 3)] += s;
+                double s = 0.0, sa = 0.0;
+                for (int o = 0; o < O; ++o) {
+                    s += (double)W2[o * H + h] * (double)dm[o];
+                    sa += fabs((double)W2[o * H + h]) * fabs((double)dm[o]);
+                }
+                da[h] = ACTIVE(h) ? s : 0.0;
+                ga[h] = sa; /* the absolute-value evaluation of da, mask open */
+                const double gm = ACTIVE(h) ? sa : 0.0, gu = UNSETTLED(h) ? sa : 0.0;
+                if (v[EN_DB1]) v[EN_DB1][h] += da[h];
+                if (m[EN_DB1]) m[EN_DB1][h] += gm;
+                if (sl[EN_DB1]) sl[EN_DB1][h] += gu;
+                for (int c = 0; c < D; ++c) {
+                    if (v[EN_DW1]) v[EN_DW1][h * D + c] += da[h] * in[c];
+                    if (m[EN_DW1]) m[EN_DW1][h * D + c] += gm * ina[c];
+                    if (sl[EN_DW1]) sl[EN_DW1][h * D + c] += gu * ina[c];
                 }
             }
+            for (int c = 0; c < D; ++c) {
+                double s = 0.0, sa = 0.0, su = 0.0;
+                for (int h = 0; h < H; ++h) {
+                    const double w1 = (double)W1[h * D + c];
+                    s += w1 * da[h];
+                    sa += fabs(w1) * (ACTIVE(h) ? ga[h] : 0.0);
+                    if (UNSETTLED(h)) su += fabs(w1) * ga[h];
+                }
+                if (c < 3) {
+                    if (v[EN_DP]) {
+                        v[EN_DP][j * 3 + c] += s;
+                        v[EN_DP][i * 3 + c] -= s;
+                    }
+                    if (m[EN_DP]) {
+                        m[EN_DP][j * 3 + c] += sa;
+                        m[EN_DP][i * 3 + c] += sa;
+                    }
+                    if (sl[EN_DP]) {
+                        sl[EN_DP][j * 3 + c] += su;
+                        sl[EN_DP][i * 3 + c] += su;
+                    }
+                } else {
+                    if (v[EN_DX]) v[EN_DX][j * F + (c - 3)] += s;
+                    if (m[EN_DX]) m[EN_DX][j * F + (c - 3)] += sa;
+                    if (sl[EN_DX]) sl[EN_DX][j * F + (c - 3)] += su;
+                }
+            }
+#undef ACTIVE
+#undef UNSETTLED
         }
     }
     free(in);
+    free(ina);
     free(a);
+    free(aa);
     free(da);
+    free(ga);
 }

@@ -80,3 +80,33 @@ def test_subset_rows():
     pts = np.array([1999, 0, 1000])
     ys, yas = oracle.dense_fwd(g["pos"], g["q"], g["eps"], pts=pts)
     assert np.array_equal(ys, y[pts]) and np.array_equal(yas, ya[pts])
+
+
+def test_sum_of_term_magnitudes_is_exact_at_the_corners():
+    """With positive charges, a particle below every other one in all three coordinates receives only
+    nonnegative terms, one above every other one only nonpositive terms: there sum|terms| equals
+    |y| component by component.  Elsewhere it bounds |y| and exceeds it."""
+    n = 500
+    pos = synth.uniform_f32(n * 3, -1.0, 1.0, (60, n)).reshape(n, 3)
+    pos[0] = -1.5
+    pos[1] = 1.5
+    q = synth.uniform_f32(n, 0.5, 1.5, (61, n))
+    y, ya = oracle.dense_fwd(pos, q, np.float32(1e-2))
+    assert np.all(y[0] > 0) and np.array_equal(ya[0], y[0])
+    assert np.all(y[1] < 0) and np.array_equal(ya[1], -y[1])
+    assert np.all(np.abs(y) <= ya * (1 + 1e-15)) and (ya[2:] > np.abs(y[2:]) * (1 + 1e-9)).all()
+
+
+def test_softening_constant_is_the_fp32_square():
+    """eps = 0.01 is not a binary fraction: the constant is fl32(eps * eps), not the fp64 square.
+    At separation 0 the message is 0; two particles at a distance d give
+    |y| = q d / (d^2 + fl32(eps^2))^(3/2) exactly in fp64 arithmetic."""
+    eps = np.float32(1e-2)
+    e2 = float(np.float32(eps * eps))
+    assert e2 != float(eps) ** 2
+    pos = np.array([[0, 0, 0], [0.0078125, 0, 0]], np.float32)
+    q = np.array([1.0, 2.0], np.float32)
+    y, _ = oracle.dense_fwd(pos, q, eps)
+    d = 0.0078125
+    s = d * d + e2
+    assert y[0, 0] == 2.0 * d / (s * np.sqrt(s))

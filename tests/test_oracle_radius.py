@@ -168,3 +168,86 @@ def test_config3_radius_constant_and_mean_degree():
     inner = np.nonzero(np.all((pos > 2 * rn) & (pos < 1 - 2 * rn), axis=1))[0][:4000]
     _, _, cnt = oracle.radius_fwd(pos, np.zeros((n, 1), np.float32), rn, rn / 2, pts=inner)
     assert abs(cnt.mean() - 32.0) < 0.6
+
+
+def _corner_cloud(n, seed):
+    """A cloud whose point 0 lies below every other point in all three coordinates and whose last
+    point lies above every other point, inside one radius of each other."""
+    pos = synth.uniform_f32(n * 3, 0.2, 0.3, (98, n, seed)).reshape(n, 3)
+    pos[0] = 0.19
+    pos[-1] = 0.31
+    return pos
+
+
+@pytest.mark.parametrize("n", [300, 4500])
+def test_sum_of_term_magnitudes_is_exact_without_cancellation(n):
+    """Each output's sum|terms| equals the output itself when no term can be negative: y with x >= 0,
+    dx with dy >= 0, and the position gradient of a point below (above) all of its neighbours, whose
+    displacements are all >= 0 (<= 0), with x and dy positive.  n = 4500 takes the cell directory."""
+    pos = _corner_cloud(n, 1)
+    F = 3
+    x = synth.uniform_f32(n * F, 0.5, 1.5, (99, n, 1)).reshape(n, F)
+    dy = synth.uniform_f32(n * F, 0.5, 1.5, (99, n, 2)).reshape(n, F)
+    r, s = np.float32(0.2), np.float32(0.05)
+    y, ya, cnt = oracle.radius_fwd(pos, x, r, s)
+    assert np.array_equal(ya, y) and cnt.min() > 0
+    dx, dxa, dp, dpa = oracle.radius_bwd(pos, x, dy, r, s)
+    assert np.array_equal(dxa, dx)
+    assert np.all(dp[0] > 0) and np.array_equal(dpa[0], dp[0])
+    assert np.all(dp[-1] < 0) and np.array_equal(dpa[-1], -dp[-1])
+    # with mixed signs the magnitudes bound the values and exceed them somewhere
+    xm = synth.normal_f32(n * F, (99, n, 3)).reshape(n, F)
+    dym = synth.normal_f32(n * F, (99, n, 4)).reshape(n, F)
+    y, ya, _ = oracle.radius_fwd(pos, xm, r, s)
+    dx, dxa, dp, dpa = oracle.radius_bwd(pos, xm, dym, r, s)
+    for v, m in ((y, ya), (dx, dxa), (dp, dpa)):
+        assert np.all(np.abs(v) <= m * (1 + 1e-15)) and (m > np.abs(v) * (1 + 1e-9)).any()
+
+
+def test_position_gradient_magnitude_two_points():
+    """Two neighbours: dp_0 = (2k/sigma^2) d (<dy_0, x_1> + <dy_1, x_0>) with d = p_1 - p_0 >= 0, so
+    with positive features its magnitude is dp_0 and that of dp_1 is -dp_1 = dp_0."""
+    pos = np.array([[0.1, 0.2, 0.3], [0.125, 0.25, 0.3125]], np.float32)
+    x = np.array([[1.0, 2.0], [0.5, 3.0]], np.float32)
+    dy = np.array([[2.0, 1.0], [1.0, 0.25]], np.float32)
+    r, s = np.float32(0.5), np.float32(0.25)
+    dx, dxa, dp, dpa = oracle.radius_bwd(pos, x, dy, r, s)
+    d = pos[1].astype(np.float64) - pos[0]
+    k = np.exp(-(d @ d) / float(s) ** 2)
+    inner = float(dy[0] @ x[1] + dy[1] @ x[0])
+    np.testing.assert_allclose(dp[0], 2 * k / float(s) ** 2 * d * inner, rtol=1e-14)
+    assert np.array_equal(dpa[0], dp[0]) and np.array_equal(dpa[1], -dp[1])
+    assert np.array_equal(dp[1], -dp[0])
+    # mixed signs: the inner products' four terms enter with their absolute values
+    dy = np.array([[2.0, -1.0], [-1.0, 0.25]], np.float32)
+    x = np.array([[1.0, -2.0], [0.5, 3.0]], np.float32)
+    dx, dxa, dp, dpa = oracle.radius_bwd(pos, x, dy, r, s)
+    absinner = float(np.abs(dy[0]) @ np.abs(x[1]) + np.abs(dy[1]) @ np.abs(x[0]))
+    np.testing.assert_allclose(dpa[0], 2 * k / float(s) ** 2 * d * absinner, rtol=1e-14)
+    np.testing.assert_allclose(dpa[1], dpa[0], rtol=1e-14)
+    np.testing.assert_allclose(dxa, k * np.abs(dy[::-1]), rtol=1e-14)
+
+
+def test_config3_cloud_against_kdtree():
+    """The paper's edge-set protocol on the measured cloud itself (1M points): the oracle's relation
+    equals scipy's fp64 ball query (distance <= r), except for pairs whose fp64 squared distance lies
+    within 4 fp32 ulp of r^2, where fp32 rounding may decide either way."""
+    g = synth.config3()
+    pos, r = g["pos"], g["radius"]
+    n = pos.shape[0]
+    ptr, idx = oracle.radius_neighbors(pos, r)
+    src = np.repeat(np.arange(n, dtype=np.int64), np.diff(ptr))
+    up = src < idx
+    assert 2 * int(up.sum()) == int(ptr[-1])            # symmetric: each pair listed both ways
+    mine = src[up] * n + idx[up]
+    tree = cKDTree(pos.astype(np.float64))
+    pairs = tree.query_pairs(float(r), output_type="ndarray").astype(np.int64)
+    ref = pairs.min(1) * n + pairs.max(1)
+    diff = np.setxor1d(mine, ref)
+    assert diff.size < 50
+    i, j = diff // n, diff % n
+    d = pos[j].astype(np.float64) - pos[i]
+    d2 = (d * d).sum(1)
+    r2 = float(np.float32(r) * np.float32(r))
+    ulp = float(np.spacing(np.float32(r2)))
+    assert np.all(np.abs(d2 - r2) <= 4 * ulp), np.abs(d2 - r2).max() / ulp
