@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define TIGA_MP_ABI_VERSION 1
+#define TIGA_MP_ABI_VERSION 2
 
 /* Status codes. */
 enum tiga_status {
@@ -92,13 +92,12 @@ typedef struct {
  *   src_ptr: int64 [num_src + 1]; source j owns slots [src_ptr[j], src_ptr[j+1]).
  *   edge_id: int32 [num_edges]; the forward edge position of each slot,
  *            ascending within a source (a stable transpose).
- *   dst_idx: int32 [num_edges]; the destination row of that edge.
  * Built by tiga_csr_transpose; valid only for the unchanged topology (a
- * topology snapshot is fixed for derivatives, Section 3.2). */
+ * topology snapshot is fixed for derivatives, Section 3.2).  The struct lives
+ * in HOST memory, the two arrays on the device. */
 typedef struct {
     const int64_t *src_ptr;
     const int32_t *edge_id;
-    const int32_t *dst_idx;
 } tiga_csr_t;
 
 /* ---------------------------------------------------------------- errors */
@@ -171,7 +170,9 @@ size_t tiga_mp_csr_bwd_workspace(const tiga_csr *rel, int32_t feat, int reducer)
  *   order not fixed, and bound by the atomics (at feat = 64 a little over twice
  *   the time of the gather mode).
  * rev != NULL: dx is gathered over the reverse incidence (deterministic); build
- *   it once per topology with tiga_csr_transpose.
+ *   it once per topology with tiga_csr_transpose.  The destination row of
+ *   each reverse slot is derived during the call from row_ptr and edge_id
+ *   (into the workspace).
  * Errors: as tiga_mp_csr_fwd. */
 int tiga_mp_csr_bwd(const tiga_csr *rel, const tiga_csr_t *rev, int32_t feat,
                     const float *x_src, int msg, const float *w_edge, int reducer,
@@ -183,10 +184,10 @@ size_t tiga_csr_transpose_workspace(const tiga_csr *rel);
 
 /* Build the reverse incidence (see tiga_csr_t) with a stable sort by source:
  * within a source, edge ids ascend.  Topology set-up: build once per
- * unchanged topology.  src_ptr int64 [num_src+1], edge_id and dst_idx int32
- * [num_edges], all overwritten.  Requires num_edges < 2^31. */
+ * unchanged topology.  src_ptr int64 [num_src+1] and edge_id int32
+ * [num_edges], both overwritten.  Requires num_edges < 2^31. */
 int tiga_csr_transpose(const tiga_csr *rel, int64_t *src_ptr, int32_t *edge_id,
-                       int32_t *dst_idx, void *ws, size_t ws_bytes, void *stream);
+                       void *ws, size_t ws_bytes, void *stream);
 
 /* CSR validation (the paper's validate="full" and basic modes, Section 6.3):
  *   level 1: host-only metadata checks (sizes, pointers); enqueues nothing.
@@ -213,6 +214,8 @@ size_t tiga_mp_radius_workspace(int64_t n, int32_t feat);
  * The cell directory is rebuilt on every call (stateless).
  *   pos: fp32 [n, 3]; x: fp32 [n, feat]; y: fp32 [n, feat] (input order);
  *   count: int32 [n] or NULL.  reducer must be TIGA_REDUCE_SUM.
+ *   feat == 0 computes the counts only (x and y may be NULL; count required):
+ *   the first phase of tiga_radius_neighbors.
  * Requires n < 2^31, radius > 0, sigma > 0, finite positions. */
 int tiga_mp_radius_fwd(int64_t n, int32_t feat, const float *pos, const float *x,
                        float radius, float sigma, int reducer, float *y, int32_t *count,
@@ -229,15 +232,18 @@ int tiga_mp_radius_bwd(int64_t n, int32_t feat, const float *pos, const float *x
                        void *ws, size_t ws_bytes, void *stream);
 
 /* Accepted neighbour lists of the radius relation, ascending per point (the
- * relation a fused call consumes, exported for exact checking).  Two phases:
- *   nbr_idx == NULL: writes count int32 [n] and nbr_ptr int64 [n+1] (exclusive
- *                    prefix of count); the caller then reads nbr_ptr[n].
- *   nbr_idx != NULL: fills nbr_idx int32 [nbr_ptr[n]] using the nbr_ptr of
- *                    phase one (count may be NULL).
+ * relation a fused call consumes, exported for exact checking; the paper
+ * resolves a generated relation to CSR for inspection, Section 4.9).  Two
+ * phases: the counts come from tiga_mp_radius_fwd (feat 0 computes only
+ * them), the caller forms nbr_ptr int64 [n+1] as their exclusive prefix sum,
+ * and this call fills nbr_idx int32 [nbr_ptr[n]].
+ *   nbr_ptr: device, read only.  Each point's list is written only inside its
+ *            span [nbr_ptr[i], nbr_ptr[i+1]); if a span differs from that
+ *            point's count the call returns TIGA_EINVAL (nothing is written
+ *            outside the spans, the lists are then incomplete).
  * Synchronizes `stream`.  Not on the fused path: for tests and inspection. */
-int tiga_radius_neighbors(int64_t n, const float *pos, float radius, int32_t *count,
-                          int64_t *nbr_ptr, int32_t *nbr_idx, void *ws, size_t ws_bytes,
-                          void *stream);
+int tiga_radius_neighbors(int64_t n, const float *pos, float radius, const int64_t *nbr_ptr,
+                          int32_t *nbr_idx, void *ws, size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------- dense all-pairs relation */
 
@@ -327,7 +333,7 @@ enum tiga_relation {
 
 /* Online-softmax reducer over an implicit triangular or dense relation: the
  * streaming attention forward (appendix "Causal attention as message
- * passing"; reducer state of Section 4.8: running maximum, mass and
+ * passing"; reducer state of Section 5.2: running maximum, mass and
  * accumulator, combined by rescaling into a common maximum).  Per head h and
  * destination i, with the message (score, value) of source j:
  *   s_ij = scale * <q_i, k_j>,

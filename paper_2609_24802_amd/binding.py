@@ -39,7 +39,7 @@ class _Csr(C.Structure):
 
 
 class _CsrT(C.Structure):
-    _fields_ = [("src_ptr", C.c_void_p), ("edge_id", C.c_void_p), ("dst_idx", C.c_void_p)]
+    _fields_ = [("src_ptr", C.c_void_p), ("edge_id", C.c_void_p)]
 
 
 _lib = None
@@ -56,8 +56,7 @@ _SIGS = {
                                   C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
                                   C.c_void_p]),
     "tiga_csr_transpose_workspace": (C.c_size_t, [C.c_void_p]),
-    "tiga_csr_transpose": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
-                                     C.c_void_p]),
+    "tiga_csr_transpose": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
     "tiga_csr_validate": (C.c_int, [C.c_void_p, C.c_int, C.c_void_p]),
     "tiga_mp_radius_workspace": (C.c_size_t, [C.c_int64, C.c_int32]),
     "tiga_mp_radius_fwd": (C.c_int, [C.c_int64, C.c_int32, C.c_void_p, C.c_void_p, C.c_float, C.c_float, C.c_int,
@@ -65,7 +64,7 @@ _SIGS = {
     "tiga_mp_radius_bwd": (C.c_int, [C.c_int64, C.c_int32, C.c_void_p, C.c_void_p, C.c_float, C.c_float,
                                      C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
     "tiga_radius_neighbors": (C.c_int, [C.c_int64, C.c_void_p, C.c_float, C.c_void_p, C.c_void_p, C.c_void_p,
-                                        C.c_void_p, C.c_size_t, C.c_void_p]),
+                                        C.c_size_t, C.c_void_p]),
     "tiga_mp_dense_workspace": (C.c_size_t, [C.c_int64]),
     "tiga_mp_dense_fwd": (C.c_int, [C.c_int64, C.c_void_p, C.c_void_p, C.c_float, C.c_int, C.c_void_p,
                                     C.c_void_p, C.c_size_t, C.c_void_p]),
@@ -164,10 +163,9 @@ class Csr:
 class CsrT:
     """Reverse incidence built by :func:`tiga_csr_transpose`."""
 
-    def __init__(self, src_ptr, edge_id, dst_idx):
-        self.src_ptr, self.edge_id, self.dst_idx = src_ptr, edge_id, dst_idx
-        self._c = _CsrT(src_ptr.data_ptr(), edge_id.data_ptr() if edge_id.numel() else None,
-                        dst_idx.data_ptr() if dst_idx.numel() else None)
+    def __init__(self, src_ptr, edge_id):
+        self.src_ptr, self.edge_id = src_ptr, edge_id
+        self._c = _CsrT(src_ptr.data_ptr(), edge_id.data_ptr() if edge_id.numel() else None)
 
     @property
     def ref(self):
@@ -280,11 +278,10 @@ def tiga_csr_transpose(rel: Csr) -> CsrT:
     dev = rel.row_ptr.device
     src_ptr = torch.empty(rel.num_src + 1, dtype=torch.int64, device=dev)
     edge_id = torch.empty(rel.num_edges, dtype=torch.int32, device=dev)
-    dst_idx = torch.empty(rel.num_edges, dtype=torch.int32, device=dev)
     ws = _workspace(lib.tiga_csr_transpose_workspace(rel.ref), dev)
-    _check(lib.tiga_csr_transpose(rel.ref, _ptr(src_ptr), _ptr(edge_id) if rel.num_edges else None,
-                                  _ptr(dst_idx) if rel.num_edges else None, _ptr(ws), ws.numel(), _stream()))
-    return CsrT(src_ptr, edge_id, dst_idx)
+    _check(lib.tiga_csr_transpose(rel.ref, _ptr(src_ptr), _ptr(edge_id) if rel.num_edges else None, _ptr(ws),
+                                  ws.numel(), _stream()))
+    return CsrT(src_ptr, edge_id)
 
 
 def tiga_csr_validate(rel: Csr, level: int = 2):
@@ -326,19 +323,26 @@ def tiga_mp_radius_bwd(pos, x, dy, radius: float, sigma: float, want_dx: bool = 
     return dx, dpos
 
 
-def tiga_radius_neighbors(pos: torch.Tensor, radius: float):
-    """Accepted neighbour lists; returns (count int32, ptr int64 [n+1], idx int32).  Synchronizes."""
+def tiga_radius_neighbors(pos: torch.Tensor, radius: float, count: torch.Tensor | None = None):
+    """Accepted neighbour lists; returns (count int32, ptr int64 [n+1], idx int32).  Synchronizes.
+
+    The two phases of the C call: the counts come from the forward with no features (or are
+    passed in), their exclusive prefix sum is the caller's nbr_ptr, then the lists are filled."""
     lib = load()
     n = pos.shape[0]
     _dev(pos, torch.float32, "pos", (n, 3))
-    count = torch.empty(n, dtype=torch.int32, device=pos.device)
-    ptr = torch.empty(n + 1, dtype=torch.int64, device=pos.device)
     ws = _workspace(lib.tiga_mp_radius_workspace(n, 0), pos.device)
-    _check(lib.tiga_radius_neighbors(n, _ptr(pos), float(radius), _ptr(count), _ptr(ptr), None, _ptr(ws),
-                                     ws.numel(), _stream()))
+    if count is None:
+        count = torch.empty(n, dtype=torch.int32, device=pos.device)
+        _check(lib.tiga_mp_radius_fwd(n, 0, _ptr(pos), None, float(radius), 1.0, REDUCE_SUM, None, _ptr(count),
+                                      _ptr(ws), ws.numel(), _stream()))
+    else:
+        _dev(count, torch.int32, "count", (n,))
+    ptr = torch.zeros(n + 1, dtype=torch.int64, device=pos.device)
+    torch.cumsum(count, 0, out=ptr[1:])
     total = int(ptr[-1].item())
     idx = torch.empty(max(total, 1), dtype=torch.int32, device=pos.device)
-    _check(lib.tiga_radius_neighbors(n, _ptr(pos), float(radius), None, _ptr(ptr), _ptr(idx), _ptr(ws), ws.numel(),
+    _check(lib.tiga_radius_neighbors(n, _ptr(pos), float(radius), _ptr(ptr), _ptr(idx), _ptr(ws), ws.numel(),
                                      _stream()))
     return count, ptr, idx[:total]
 

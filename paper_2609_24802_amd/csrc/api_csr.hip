@@ -135,8 +135,7 @@ int tiga_mp_csr_bwd(const tiga_csr *rel, const tiga_csr_t *rev, int32_t feat, co
         if (rel->num_edges > INT32_MAX)
             return fail(TIGA_EUNSUPPORTED, "reverse incidence needs num_edges < 2^31");
         if (rel->num_src > 0 && !rev->src_ptr) return fail(TIGA_EINVAL, "rev->src_ptr is NULL");
-        if (rel->num_edges > 0 && (!rev->edge_id || !rev->dst_idx))
-            return fail(TIGA_EINVAL, "rev->edge_id / rev->dst_idx is NULL");
+        if (rel->num_edges > 0 && !rev->edge_id) return fail(TIGA_EINVAL, "rev->edge_id is NULL");
     }
     const size_t need = tiga_mp_csr_bwd_workspace(rel, feat, reducer);
     if (int rc = check_ws(ws, ws_bytes, need)) return rc;
@@ -150,16 +149,16 @@ size_t tiga_csr_transpose_workspace(const tiga_csr *rel) {
     return transpose_ws_bytes(rel->num_dst, rel->num_src, rel->num_edges);
 }
 
-int tiga_csr_transpose(const tiga_csr *rel, int64_t *src_ptr, int32_t *edge_id, int32_t *dst_idx, void *ws,
-                       size_t ws_bytes, void *stream) {
+int tiga_csr_transpose(const tiga_csr *rel, int64_t *src_ptr, int32_t *edge_id, void *ws, size_t ws_bytes,
+                       void *stream) {
     EntryScope scope;
     if (int rc = check_csr_meta(rel)) return rc;
     if (rel->num_edges > INT32_MAX) return fail(TIGA_EUNSUPPORTED, "transpose needs num_edges < 2^31");
     if (!src_ptr) return fail(TIGA_EINVAL, "src_ptr is NULL");
-    if (rel->num_edges > 0 && (!edge_id || !dst_idx)) return fail(TIGA_EINVAL, "edge_id / dst_idx is NULL");
+    if (rel->num_edges > 0 && !edge_id) return fail(TIGA_EINVAL, "edge_id is NULL");
     const size_t need = tiga_csr_transpose_workspace(rel);
     if (int rc = check_ws(ws, ws_bytes, need)) return rc;
-    return launch_transpose(rel, src_ptr, edge_id, dst_idx, ws, static_cast<hipStream_t>(stream));
+    return launch_transpose(rel, src_ptr, edge_id, ws, static_cast<hipStream_t>(stream));
 }
 
 int tiga_csr_validate(const tiga_csr *rel, int level, void *stream) {

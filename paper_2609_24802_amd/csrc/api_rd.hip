@@ -42,12 +42,13 @@ int tiga_mp_radius_fwd(int64_t n, int32_t feat, const float *pos, const float *x
                        int reducer, float *y, int32_t *count, void *ws, size_t ws_bytes, void *stream) {
     EntryScope scope;
     if (int rc = check_points(n, pos)) return rc;
-    if (feat < 1) return fail(TIGA_EINVAL, "feat must be >= 1 (got %d)", feat);
+    if (feat < 0) return fail(TIGA_EINVAL, "feat must be >= 0 (got %d)", feat);
     if (reducer == TIGA_REDUCE_MAX) return fail(TIGA_EUNSUPPORTED, "the radius relation supports the sum reducer only");
     if (reducer != TIGA_REDUCE_SUM) return fail(TIGA_EINVAL, "unknown reducer %d", reducer);
     if (int rc = check_radius(radius, sigma)) return rc;
+    if (feat == 0 && !count) return fail(TIGA_EINVAL, "feat 0 computes counts only: count is required");
     if (n == 0) return TIGA_OK;
-    if (!x || !y) return fail(TIGA_EINVAL, "x and y are required");
+    if (feat > 0 && (!x || !y)) return fail(TIGA_EINVAL, "x and y are required");
     if (int rc = check_ws(ws, ws_bytes, radius::workspace_bytes(n, feat))) return rc;
     return radius::forward(n, feat, pos, x, radius, sigma, y, count, ws, static_cast<hipStream_t>(stream));
 }
@@ -65,19 +66,16 @@ int tiga_mp_radius_bwd(int64_t n, int32_t feat, const float *pos, const float *x
     return radius::backward(n, feat, pos, x, radius, sigma, dy, dx, dpos, ws, static_cast<hipStream_t>(stream));
 }
 
-int tiga_radius_neighbors(int64_t n, const float *pos, float radius, int32_t *count, int64_t *nbr_ptr,
-                          int32_t *nbr_idx, void *ws, size_t ws_bytes, void *stream) {
+int tiga_radius_neighbors(int64_t n, const float *pos, float radius, const int64_t *nbr_ptr, int32_t *nbr_idx,
+                          void *ws, size_t ws_bytes, void *stream) {
     EntryScope scope;
     if (int rc = check_points(n, pos)) return rc;
     if (int rc = check_radius(radius, 1.0f)) return rc;
+    if (n == 0) return TIGA_OK;
     if (!nbr_ptr) return fail(TIGA_EINVAL, "nbr_ptr is NULL");
-    if (n == 0) {
-        if (nbr_idx) return TIGA_OK;
-        if (int rc = fill_u32(nbr_ptr, 0u, 2, static_cast<hipStream_t>(stream))) return rc;
-        return check_hip(hipStreamSynchronize(static_cast<hipStream_t>(stream)), "neighbours: synchronize");
-    }
+    if (!nbr_idx) return fail(TIGA_EINVAL, "nbr_idx is NULL");
     if (int rc = check_ws(ws, ws_bytes, radius::workspace_bytes(n, 0))) return rc;
-    return radius::neighbors(n, pos, radius, count, nbr_ptr, nbr_idx, ws, static_cast<hipStream_t>(stream));
+    return radius::neighbors(n, pos, radius, nbr_ptr, nbr_idx, ws, static_cast<hipStream_t>(stream));
 }
 
 size_t tiga_mp_dense_workspace(int64_t n) {
@@ -92,6 +90,11 @@ int tiga_mp_dense_fwd(int64_t n, const float *pos, const float *q, float eps, in
     if (reducer == TIGA_REDUCE_MAX) return fail(TIGA_EUNSUPPORTED, "the dense relation supports the sum reducer only");
     if (reducer != TIGA_REDUCE_SUM) return fail(TIGA_EINVAL, "unknown reducer %d", reducer);
     if (!(eps > 0.0f) || !(eps < 3.0e38f)) return fail(TIGA_EINVAL, "eps must be finite and > 0");
+    // the message is formed with the fp32 constant eps * eps: it must be a finite normal number, or the
+    // zero-displacement self term (0 * rsq(0)^3) would not vanish
+    const float eps2 = eps * eps;
+    if (!(eps2 >= 1.17549435e-38f) || !(eps2 < 3.0e38f))
+        return fail(TIGA_EINVAL, "eps * eps (%g) must be a finite normal fp32 number", static_cast<double>(eps2));
     if (n == 0) return TIGA_OK;
     if (!q || !y) return fail(TIGA_EINVAL, "q and y are required");
     if (int rc = check_ws(ws, ws_bytes, dense::workspace_bytes(n))) return rc;
@@ -99,6 +102,14 @@ int tiga_mp_dense_fwd(int64_t n, const float *pos, const float *q, float eps, in
 }
 
 namespace {
+
+// The edge-MLP path's shared cell directory holds up to 8 n + 64 cells, indexed by int32 keys.
+int check_shared_cells(int64_t n) {
+    if (8 * n + 64 > INT32_MAX)
+        return fail(TIGA_EUNSUPPORTED, "n %lld: the cell directory of the edge MLP needs 8 n + 64 < 2^31",
+                    (long long)n);
+    return TIGA_OK;
+}
 
 int check_net(int32_t feat, int32_t hidden, int32_t out) {
     if (feat < 0 || hidden < 1 || out < 1) return fail(TIGA_EINVAL, "need feat >= 0, hidden >= 1, out >= 1");
@@ -120,6 +131,7 @@ int tiga_mp_edgenn_fwd(int64_t n, int32_t feat, int32_t hidden, int32_t out, con
                        void *ws, size_t ws_bytes, void *stream) {
     EntryScope scope;
     if (int rc = check_points(n, pos)) return rc;
+    if (int rc = check_shared_cells(n)) return rc;
     if (int rc = check_net(feat, hidden, out)) return rc;
     if (int rc = check_radius(radius, 1.0f)) return rc;
     if (n == 0) return TIGA_OK;
@@ -135,6 +147,7 @@ int tiga_mp_edgenn_bwd(int64_t n, int32_t feat, int32_t hidden, int32_t out, con
                        void *ws, size_t ws_bytes, void *stream) {
     EntryScope scope;
     if (int rc = check_points(n, pos)) return rc;
+    if (int rc = check_shared_cells(n)) return rc;
     if (int rc = check_net(feat, hidden, out)) return rc;
     if (int rc = check_radius(radius, 1.0f)) return rc;
     if (n == 0) {

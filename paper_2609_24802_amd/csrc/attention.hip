@@ -1,6 +1,6 @@
 // Online-softmax reducer over an implicit triangular or dense relation: the streaming attention
 // forward of the appendix "Causal attention as message passing", with the reducer state of
-// Section 4.8 (running maximum m, mass l, accumulator o; two states combine by rescaling into the
+// Section 5.2 (running maximum m, mass l, accumulator o; two states combine by rescaling into the
 // common maximum).  For head h and destination i:
 //   s_ij = scale * <q_i, k_j>,  y_i = sum_{j in N(i)} exp(s_ij) v_j / sum_{j in N(i)} exp(s_ij)
 // with N(i) = {0..i} (triangular, diagonal included) or {0..n-1} (dense).  No score or weight
@@ -313,7 +313,7 @@ __device__ __forceinline__ void scores_of(f4 (*s)[2], const u4 (&qreg)[2][Geo<D>
     }
 }
 
-// Online-softmax state update of one tile (Section 4.8), log2 domain, producing the weights pb.
+// Online-softmax state update of one tile (Section 5.2), log2 domain, producing the weights pb.
 // Fast path: the weights are formed against the current reference point m and the mass of the
 // tile (an MFMA against an all-ones operand) is checked: a tile mass of at most 2^12 for every
 // query bounds every weight by 2^12, far inside the 16-bit range.  A larger, infinite or NaN mass

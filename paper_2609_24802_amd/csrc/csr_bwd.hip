@@ -164,16 +164,43 @@ int edge_flags(bool dw, bool dx, int L, const EdgeT &t, int64_t nedges, void *ws
     return edge_lanes<K, RED, false, true>(L, t, nedges, ws, stream);
 }
 
+// Workspace of the backward: the destination row of every edge and of every reverse slot
+// (num_edges int32 each; used with the reverse incidence), then the region the plan of either
+// traversal takes.
+struct BwdWs {
+    int32_t *row_of_edge;
+    int32_t *row_of_slot;
+    void *rest;
+};
+
+BwdWs carve_bwd(void *ws, int64_t num_edges) {
+    Carve c(ws);
+    BwdWs w;
+    w.row_of_edge = c.take<int32_t>(num_edges);
+    w.row_of_slot = c.take<int32_t>(num_edges);
+    w.rest = ws ? static_cast<char *>(ws) + c.bytes() : nullptr;
+    return w;
+}
+
+size_t bwd_rows_bytes(int64_t num_edges) {
+    Carve c(nullptr);
+    c.take<int32_t>(num_edges);
+    c.take<int32_t>(num_edges);
+    return c.bytes();
+}
+
 }  // namespace
 
 size_t bwd_ws_bytes(int64_t num_dst, int64_t num_src, int64_t num_edges, int64_t feat) {
     size_t a = traversal_ws_bytes(num_dst, num_edges, feat, false);
     size_t b = traversal_ws_bytes(num_src, num_edges, feat, false);
-    return a > b ? a : b;
+    return bwd_rows_bytes(num_edges) + (a > b ? a : b);
 }
 
-int launch_bwd(const BwdArgs &a, void *ws, hipStream_t stream) {
+int launch_bwd(const BwdArgs &a, void *ws_all, hipStream_t stream) {
     const tiga_csr *rel = a.rel;
+    const BwdWs bw = carve_bwd(ws_all, rel->num_edges);
+    void *ws = bw.rest;
     const bool vec = a.feat % 4 == 0 && aligned16(a.dy) && (!a.dx || aligned16(a.dx)) &&
                      (!a.dw || !a.x || aligned16(a.x)) && (!a.arg || aligned16(a.arg));
     const Layout lay = layout_for(a.feat, vec);
@@ -199,7 +226,10 @@ int launch_bwd(const BwdArgs &a, void *ws, hipStream_t stream) {
         if (rc) return rc;
     }
     if (a.dx && a.rev && rel->num_src > 0) {
-        Trav t{a.rev->src_ptr, a.rev->dst_idx, a.w, a.rev->edge_id, a.dy, rel->num_src, lay.fu, a.arg, 0u,
+        // the reverse incidence carries forward edge ids only; the destination of each slot is
+        // derived here from row_ptr (sequential writes, then one gather by edge id)
+        if (int rc = launch_slot_rows(rel, a.rev->edge_id, bw.row_of_edge, bw.row_of_slot, stream)) return rc;
+        Trav t{a.rev->src_ptr, bw.row_of_slot, a.w, a.rev->edge_id, a.dy, rel->num_src, lay.fu, a.arg, 0u,
                rel->num_edges};
         const int wm = a.red == RED_MAX ? W_ROUTE : W_INDIRECT;
         EdgeGrad eg;

@@ -207,6 +207,15 @@ __global__ __launch_bounds__(kBlock) void expand_rows_kernel(const int64_t *__re
     }
 }
 
+// out[s] = table[index[s]] for s in [0, n).
+__global__ __launch_bounds__(kBlock) void gather_i32_kernel(const int32_t *__restrict__ table,
+                                                            const int32_t *__restrict__ index, int64_t n,
+                                                            int32_t *__restrict__ out) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t s = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; s < n; s += stride)
+        out[s] = table[index[s]];
+}
+
 // ptr[j] = first sorted position with key >= j, for j in [0, nkeys]: one
 // binary search per j, so long runs of absent keys cost no serial work.
 __global__ __launch_bounds__(kBlock) void ptr_from_sorted_kernel(const int32_t *__restrict__ sorted, int64_t n,
@@ -342,25 +351,32 @@ size_t transpose_ws_bytes(int64_t num_dst, int64_t num_src, int64_t num_edges) {
     (void)num_dst;
     (void)num_src;
     Carve c(nullptr);
-    carve_sort(c, num_edges, true);
+    carve_sort(c, num_edges, false);
     return c.bytes();
 }
 
-int launch_transpose(const tiga_csr *rel, int64_t *src_ptr, int32_t *edge_id, int32_t *dst_idx, void *ws,
-                     hipStream_t stream) {
+int launch_transpose(const tiga_csr *rel, int64_t *src_ptr, int32_t *edge_id, void *ws, hipStream_t stream) {
     const int64_t n = rel->num_edges;
     Carve c(ws);
-    SortWs s = carve_sort(c, n, true);
+    SortWs s = carve_sort(c, n, false);
     if (n == 0) return fill_u32(src_ptr, 0u, 2 * (rel->num_src + 1), stream);
-    // destination of every edge position, sorted along as the payload; the
-    // first pass reads it from the second ping-pong buffer
-    const int eb = persistent_blocks(rel->num_dst, 8);
-    hipLaunchKernelGGL(expand_rows_kernel, dim3(eb), dim3(kBlock), 0, stream, rel->row_ptr, rel->num_dst, s.b[1]);
-    if (int rc = check_launch("expand rows")) return rc;
     const int32_t *sorted = nullptr;
-    if (int rc = radix_sort(rel->col_idx, s.b[1], n, rel->num_src, nullptr, edge_id, dst_idx, s, &sorted, stream))
+    if (int rc = radix_sort(rel->col_idx, nullptr, n, rel->num_src, nullptr, edge_id, nullptr, s, &sorted, stream))
         return rc;
     return ptr_from_sorted(sorted, n, rel->num_src, src_ptr, stream);
+}
+
+int launch_slot_rows(const tiga_csr *rel, const int32_t *edge_id, int32_t *row_of_edge, int32_t *row_of_slot,
+                     hipStream_t stream) {
+    const int64_t n = rel->num_edges;
+    if (n == 0) return TIGA_OK;
+    const int eb = persistent_blocks(rel->num_dst, 8);
+    hipLaunchKernelGGL(expand_rows_kernel, dim3(eb), dim3(kBlock), 0, stream, rel->row_ptr, rel->num_dst,
+                       row_of_edge);
+    if (int rc = check_launch("expand rows")) return rc;
+    const int gb = persistent_blocks(ceil_div(n, kWave), 8);
+    hipLaunchKernelGGL(gather_i32_kernel, dim3(gb), dim3(kBlock), 0, stream, row_of_edge, edge_id, n, row_of_slot);
+    return check_launch("destination of each reverse slot");
 }
 
 size_t sort_keys_ws_bytes(int64_t n) {

@@ -583,7 +583,6 @@ __global__ __launch_bounds__(kBlock) void radius_bwd_cell_kernel(const Params *_
 __global__ __launch_bounds__(kBlock) void neighbor_count_kernel(const Params *__restrict__ prm,
                                                                 const int64_t *__restrict__ start,
                                                                 const float4 *__restrict__ rec, int64_t n, float r2,
-                                                                int64_t *__restrict__ cnt64,
                                                                 int32_t *__restrict__ count) {
     const Params p = *prm;
     const int64_t s = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -596,28 +595,36 @@ __global__ __launch_bounds__(kBlock) void neighbor_count_kernel(const Params *__
         float d2;
         if (accept(pi, pj, r2, d2) && __float_as_int(pj.w) != i) ++c;
     });
-    cnt64[i] = c;
-    if (count) count[i] = c;
+    count[i] = c;
 }
 
 __global__ __launch_bounds__(kBlock) void neighbor_fill_kernel(const Params *__restrict__ prm,
                                                                const int64_t *__restrict__ start,
                                                                const float4 *__restrict__ rec, int64_t n, float r2,
                                                                const int64_t *__restrict__ ptr,
-                                                               int32_t *__restrict__ idx) {
+                                                               int32_t *__restrict__ idx,
+                                                               uint32_t *__restrict__ mismatch) {
     const Params p = *prm;
     const int64_t s = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (s >= n) return;
     const float4 pi = rec[s];
     const int32_t i = __float_as_int(pi.w);
+    // writes stay inside the caller's span [ptr[i], ptr[i+1]); a span that is not the point's
+    // neighbour count is reported, never overrun
     const int64_t b = ptr[i];
+    const int64_t e = ptr[i + 1];
     int64_t w = b;
     for_candidates(p, start, pi, [&](int64_t t) {
         const float4 pj = rec[t];
         float d2;
         const int32_t j = __float_as_int(pj.w);
-        if (accept(pi, pj, r2, d2) && j != i) idx[w++] = j;
+        if (accept(pi, pj, r2, d2) && j != i) {
+            if (w < e) idx[w] = j;
+            ++w;
+        }
     });
+    if (w != e) atomicOr(mismatch, 1u);
+    if (w > e) w = e;
     // insertion sort of this point's list (ascending ids)
     for (int64_t a = b + 1; a < w; ++a) {
         const int32_t v = idx[a];
@@ -639,6 +646,7 @@ struct Ws {
     float4 *rec;
     void *sort;
     void *scan;
+    uint32_t *flag;
     int64_t max_cells;
     int bbox_blocks;
 };
@@ -659,6 +667,7 @@ Ws carve(Carve &c, int64_t n, int64_t cells_per_point = 1) {
     w.rec = c.take<float4>(n);
     w.sort = c.take<char>(csr::sort_keys_ws_bytes(n));
     w.scan = c.take<char>(scan_ws_bytes(n + 1));
+    w.flag = c.take<uint32_t>(1);
     return w;
 }
 
@@ -764,6 +773,15 @@ size_t workspace_bytes(int64_t n, int64_t feat) {
 
 int forward(int64_t n, int32_t feat, const float *pos, const float *x, float radius, float sigma, float *y,
             int32_t *count, void *ws, hipStream_t stream) {
+    if (feat == 0) {
+        // no features: the relation's counts only
+        Carve c(ws);
+        Ws w = carve(c, n);
+        if (int rc = build(n, pos, radius, w, stream)) return rc;
+        hipLaunchKernelGGL(neighbor_count_kernel, dim3(static_cast<unsigned>(ceil_div(n, kBlock))), dim3(kBlock), 0,
+                           stream, w.prm, w.start, w.rec, n, radius * radius, count);
+        return check_launch("radius counts");
+    }
     // 16-byte units when every row starts on a 16-byte boundary
     const bool vec = feat % 4 == 0 && aligned16(x) && aligned16(y);
     const int64_t fu = vec ? feat / 4 : feat;
@@ -822,27 +840,25 @@ int build_cells(int64_t n, const float *pos, float radius, void *ws, Cells &out,
     return TIGA_OK;
 }
 
-int neighbors(int64_t n, const float *pos, float radius, int32_t *count, int64_t *nbr_ptr, int32_t *nbr_idx,
-              void *ws, hipStream_t stream) {
+int neighbors(int64_t n, const float *pos, float radius, const int64_t *nbr_ptr, int32_t *nbr_idx, void *ws,
+              hipStream_t stream) {
     Carve c(ws);
     Ws w = carve(c, n);
     if (int rc = build(n, pos, radius, w, stream)) return rc;
-    const int64_t *start = w.start;
-    const float r2 = radius * radius;
+    if (int rc = fill_u32(w.flag, 0u, 1, stream)) return rc;
     const dim3 grid(static_cast<unsigned>(ceil_div(n, kBlock)));
-    if (!nbr_idx) {
-        // counts into nbr_ptr[0..n), then the exclusive scan in place
-        hipLaunchKernelGGL(neighbor_count_kernel, grid, dim3(kBlock), 0, stream, w.prm, start, w.rec, n, r2, nbr_ptr,
-                           count);
-        if (int rc = check_launch("radius neighbour count")) return rc;
-        if (int rc = fill_u32(nbr_ptr + n, 0u, 2, stream)) return rc;
-        if (int rc = launch_excl_scan(nbr_ptr, nbr_ptr, n + 1, w.scan, stream)) return rc;
-    } else {
-        hipLaunchKernelGGL(neighbor_fill_kernel, grid, dim3(kBlock), 0, stream, w.prm, start, w.rec, n, r2, nbr_ptr,
-                           nbr_idx);
-        if (int rc = check_launch("radius neighbour fill")) return rc;
-    }
-    return check_hip(hipStreamSynchronize(stream), "radius neighbours: synchronize");
+    hipLaunchKernelGGL(neighbor_fill_kernel, grid, dim3(kBlock), 0, stream, w.prm, w.start, w.rec, n, radius * radius,
+                       nbr_ptr, nbr_idx, w.flag);
+    if (int rc = check_launch("radius neighbour fill")) return rc;
+    uint32_t mismatch = 0;
+    if (int rc = check_hip(hipMemcpyAsync(&mismatch, w.flag, sizeof mismatch, hipMemcpyDeviceToHost, stream),
+                           "radius neighbours: copy"))
+        return rc;
+    if (int rc = check_hip(hipStreamSynchronize(stream), "radius neighbours: synchronize")) return rc;
+    if (mismatch)
+        return fail(TIGA_EINVAL, "nbr_ptr is not the exclusive prefix of the relation's neighbour counts "
+                                 "(spans were filled without overrun, the lists are incomplete)");
+    return TIGA_OK;
 }
 
 }  // namespace radius

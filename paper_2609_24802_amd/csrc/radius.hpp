@@ -11,8 +11,8 @@ int forward(int64_t n, int32_t feat, const float *pos, const float *x, float rad
             int32_t *count, void *ws, hipStream_t stream);
 int backward(int64_t n, int32_t feat, const float *pos, const float *x, float radius, float sigma, const float *dy,
              float *dx, float *dpos, void *ws, hipStream_t stream);
-int neighbors(int64_t n, const float *pos, float radius, int32_t *count, int64_t *nbr_ptr, int32_t *nbr_idx,
-              void *ws, hipStream_t stream);
+int neighbors(int64_t n, const float *pos, float radius, const int64_t *nbr_ptr, int32_t *nbr_idx, void *ws,
+              hipStream_t stream);
 
 }  // namespace radius
 }  // namespace tiga

@@ -37,7 +37,33 @@ def test_exports_every_declared_symbol(clib):
 
 
 def test_abi_version(clib):
-    assert clib.tiga_mp_abi_version() == 1
+    assert clib.tiga_mp_abi_version() == 2
+
+
+def test_struct_layouts_match_the_header(tmp_path):
+    """The binding's ctypes structs have the header's field offsets and sizes (a C program compiled
+    against include/tiga_mp.h prints them): the relation is (num_dst, num_src, num_edges, row_ptr,
+    col_idx) and the reverse incidence is exactly (src_ptr, edge_id)."""
+    import subprocess
+    from paper_2609_24802_amd.binding import _Csr, _CsrT
+    src = tmp_path / "layout.c"
+    src.write_text(
+        '#include <stdio.h>\n#include <stddef.h>\n#include "tiga_mp.h"\n'
+        'int main(void) {\n'
+        '  printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(tiga_csr), offsetof(tiga_csr, num_dst),\n'
+        '         offsetof(tiga_csr, num_src), offsetof(tiga_csr, num_edges), offsetof(tiga_csr, row_ptr),\n'
+        '         offsetof(tiga_csr, col_idx));\n'
+        '  printf("%zu %zu %zu\\n", sizeof(tiga_csr_t), offsetof(tiga_csr_t, src_ptr), offsetof(tiga_csr_t, edge_id));\n'
+        '  return 0;\n}\n')
+    exe = tmp_path / "layout"
+    subprocess.check_call(["gcc", "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)])
+    out = subprocess.check_output([str(exe)]).decode().split("\n")
+    csr = [int(v) for v in out[0].split()]
+    rev = [int(v) for v in out[1].split()]
+    assert csr == [C.sizeof(_Csr)] + [getattr(_Csr, f).offset for f in
+                                      ("num_dst", "num_src", "num_edges", "row_ptr", "col_idx")]
+    assert rev == [C.sizeof(_CsrT), _CsrT.src_ptr.offset, _CsrT.edge_id.offset]
+    assert rev == [16, 0, 8] and [f for f, _ in _CsrT._fields_] == ["src_ptr", "edge_id"]
 
 
 def _csr(num_dst, num_src, num_edges, rp=0x1000, col=0x2000):
@@ -89,8 +115,10 @@ def test_csr_backward_and_transpose_errors(clib):
                               fake, None, fake, 1 << 40, None)
     assert rc == b.TIGA_EINVAL  # max without argmax
     big = _csr(4, 4, 3 << 30)
-    rc = clib.tiga_csr_transpose(C.byref(big), fake, fake, fake, fake, 1 << 40, None)
+    rc = clib.tiga_csr_transpose(C.byref(big), fake, fake, fake, 1 << 40, None)
     assert rc == b.TIGA_EUNSUPPORTED
+    rc = clib.tiga_csr_transpose(C.byref(rel), fake, None, fake, 1 << 40, None)
+    assert rc == b.TIGA_EINVAL and b"edge_id" in clib.tiga_last_error()
     rc = clib.tiga_csr_validate(C.byref(rel), 3, None)
     assert rc == b.TIGA_EINVAL
     assert clib.tiga_csr_validate(C.byref(rel), 1, None) == b.TIGA_OK
@@ -112,6 +140,20 @@ def test_radius_dense_errors(clib):
     assert rc == b.TIGA_EINVAL
     rc = clib.tiga_mp_dense_fwd(100, fake, fake, 0.01, b.REDUCE_MAX, fake, fake, 1 << 40, None)
     assert rc == b.TIGA_EUNSUPPORTED
+    rc = clib.tiga_mp_dense_fwd(100, fake, fake, 1e-20, b.REDUCE_SUM, fake, fake, 1 << 40, None)
+    assert rc == b.TIGA_EINVAL and b"normal" in clib.tiga_last_error()   # eps^2 underflows in fp32
+    rc = clib.tiga_mp_dense_fwd(100, fake, fake, 1e20, b.REDUCE_SUM, fake, fake, 1 << 40, None)
+    assert rc == b.TIGA_EINVAL   # eps^2 overflows in fp32
+    # feat 0 computes counts only, so count is required
+    rc = clib.tiga_mp_radius_fwd(100, 0, fake, None, 0.1, 0.05, b.REDUCE_SUM, None, None, fake, 1 << 40, None)
+    assert rc == b.TIGA_EINVAL and b"count" in clib.tiga_last_error()
+    rc = clib.tiga_mp_radius_fwd(100, -1, fake, None, 0.1, 0.05, b.REDUCE_SUM, None, fake, fake, 1 << 40, None)
+    assert rc == b.TIGA_EINVAL
+    # neighbour lists: nbr_ptr and nbr_idx are required, the workspace is checked
+    assert clib.tiga_radius_neighbors(100, fake, 0.1, None, fake, fake, 1 << 40, None) == b.TIGA_EINVAL
+    assert clib.tiga_radius_neighbors(100, fake, 0.1, fake, None, fake, 1 << 40, None) == b.TIGA_EINVAL
+    assert clib.tiga_radius_neighbors(100, fake, 0.1, fake, fake, fake, 8, None) == b.TIGA_EWORKSPACE
+    assert clib.tiga_radius_neighbors(0, None, 0.1, None, None, None, 0, None) == b.TIGA_OK
     # empty inputs are valid no-ops
     assert clib.tiga_mp_dense_fwd(0, None, None, 0.01, b.REDUCE_SUM, None, None, 0, None) == b.TIGA_OK
     assert clib.tiga_mp_radius_fwd(0, 8, None, None, 0.1, 0.05, b.REDUCE_SUM, None, None, None, 0, None) == b.TIGA_OK
@@ -181,6 +223,7 @@ def test_edgenn_errors(clib):
     assert call(H=0) == b.TIGA_EINVAL
     assert call(r=0.0) == b.TIGA_EINVAL
     assert call(wsb=8) == b.TIGA_EWORKSPACE
+    assert call(n=300_000_000) == b.TIGA_EUNSUPPORTED   # the shared cell directory's int32 keys
     assert call(n=0, ws=None, wsb=0) == b.TIGA_OK
     assert clib.tiga_mp_edgenn_bwd(100, 8, 32, 3, f, f, 0.1, f, f, f, f, None, f, f, f, f, f, f, f, big,
                                    None) == b.TIGA_EINVAL   # dy is required

@@ -162,11 +162,22 @@ def test_radius_rejects_max(lib):
 
 
 def test_config3_full_size_sampled(lib):
+    """The measured workload (1M points, F = 32): every count of the fused forward and every
+    neighbour list bit-exact against the oracle's relation; values and gradients on 4,000 points."""
     g = synth.config3()
     pos, x, dy, r, s = g["pos"], g["x"], g["dy"], g["radius"], g["sigma"]
+    n = pos.shape[0]
     pd, xd, dyd = dev(pos), dev(x), dev(dy)
+    print(f"config 3: forward n={n} F={x.shape[1]}", flush=True)
     y, cnt = lib.tiga_mp_radius_fwd(pd, xd, r, s)
-    pts = np.unique(np.random.default_rng(4).integers(0, pos.shape[0], 4000))
+    rptr, ridx = oracle.radius_neighbors(pos, r)
+    assert np.array_equal(host(cnt), np.diff(rptr).astype(np.int32))
+    print("config 3: neighbour lists", flush=True)
+    c2, ptr, idx = lib.tiga_radius_neighbors(pd, r)
+    assert np.array_equal(host(ptr), rptr)
+    assert np.array_equal(host(idx), ridx)
+    del c2, ptr, idx
+    pts = np.unique(np.random.default_rng(4).integers(0, n, 4000))
     ry, rya, rcnt = oracle.radius_fwd(pos, x, r, s, pts=pts)
     assert np.array_equal(host(cnt)[pts], rcnt)
     assert_terms_close(host(y)[pts], ry, rya, what="config 3 y")
@@ -175,8 +186,28 @@ def test_config3_full_size_sampled(lib):
     assert_terms_close(host(dx)[pts], rdx, rdxa, what="config 3 dx")
     assert_terms_close(host(dp)[pts], rdp, rdpa, what="config 3 dpos")
     # symmetric relation: the directed pair count is even; mean degree near 32
-    total = int(host(cnt).astype(np.int64).sum())
-    assert total % 2 == 0 and abs(total / pos.shape[0] - 31.3) < 0.3
+    total = int(rptr[-1])
+    assert total % 2 == 0 and abs(total / n - 31.3) < 0.3
+
+
+def test_config3_infinite_sigma_is_exact(lib):
+    """sigma -> infinity makes every kernel weight exactly 1 (fp32 1/sigma^2 is 0), so the fused sums
+    are plain neighbour sums of small integers, exact in any order: y and dx equal the oracle's
+    fp64 sums bit for bit over all 1M points of the measured cloud."""
+    g = synth.config3()
+    pos, r = g["pos"], g["radius"]
+    n, F = pos.shape[0], 32
+    rng = np.random.default_rng(17)
+    x = rng.integers(-8, 9, (n, F)).astype(np.float32)
+    dy = rng.integers(-8, 9, (n, F)).astype(np.float32)
+    sig = np.float32(1e30)
+    y, cnt = lib.tiga_mp_radius_fwd(dev(pos), dev(x), r, sig)
+    ry, _, rcnt = oracle.radius_fwd(pos, x, r, sig)
+    assert np.array_equal(host(cnt), rcnt)
+    assert np.array_equal(host(y).astype(np.float64), ry)
+    dx, _ = lib.tiga_mp_radius_bwd(dev(pos), dev(x), dev(dy), r, sig, want_dpos=False)
+    rdx, _, _, _ = oracle.radius_bwd(pos, x, dy, r, sig)
+    assert np.array_equal(host(dx).astype(np.float64), rdx)
 
 
 @pytest.mark.parametrize("n", [1, 2, 3, 255, 256, 257, 1000, 5003])
@@ -223,3 +254,22 @@ def test_radius_autograd_wrapper(lib):
     rdx, rdxa, rdp, rdpa = oracle.radius_bwd(pos, x, dy, r, s)
     assert_terms_close(host(xt.grad), rdx, rdxa, what="autograd radius dx")
     assert_terms_close(host(pt.grad), rdp, rdpa, what="autograd radius dpos")
+
+
+def test_radius_neighbors_rejects_a_wrong_pointer_array(lib):
+    """nbr_ptr is the caller's: spans that do not match the counts are reported as TIGA_EINVAL.  Here
+    one span is one longer and the next one shorter, so every write still lands inside the array."""
+    pos = cloud("uniform", 3000, 5)
+    r = np.float32(0.06)
+    cnt, ptr, idx = lib.tiga_radius_neighbors(dev(pos), r)
+    k = int(np.argmax(host(cnt) > 0)) + 1
+    bad = ptr.clone()
+    bad[k] += 1
+    ws = torch.empty(lib.load().tiga_mp_radius_workspace(3000, 0), dtype=torch.uint8, device="cuda")
+    out = torch.full_like(idx, -7)
+    rc = lib.load().tiga_radius_neighbors(3000, lib._ptr(dev(pos)), float(r), lib._ptr(bad), lib._ptr(out),
+                                          lib._ptr(ws), ws.numel(), lib._stream())
+    assert rc == lib.TIGA_EINVAL
+    assert b"exclusive prefix" in lib.load().tiga_last_error()
+    rptr, ridx = oracle.radius_neighbors(pos, r)
+    assert np.array_equal(host(ptr), rptr) and np.array_equal(host(idx), ridx)

@@ -1,8 +1,8 @@
-"""Pins for the oracle's online-softmax attention (Section 4.8 and the appendix on causal attention).
+"""Pins for the oracle's online-softmax attention (Section 5.2 and the appendix on causal attention).
 
 Each check comes from something other than the oracle's own formula: the IEEE definitions (through
 numpy's own conversions), closed forms, the combine law of the online-softmax state printed in
-Section 4.8, invariances of the softmax, and the relation's structure (the triangular row i is the
+Section 5.2, invariances of the softmax, and the relation's structure (the triangular row i is the
 dense relation over the first i + 1 tokens)."""
 import math
 
@@ -87,7 +87,7 @@ def test_two_token_closed_form_and_head_separation():
 
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
 def test_online_softmax_combine_law(dtype):
-    """Section 4.8: two nonempty states (m, l, o) over disjoint key sets combine by rescaling into
+    """Section 5.2: two nonempty states (m, l, o) over disjoint key sets combine by rescaling into
     the common maximum.  With the finalized state of a set being (lse, 1, y), combining the states
     of halves A and B must give the state of A u B."""
     nA, nB, H, D = 23, 41, 2, 64
