@@ -132,6 +132,24 @@ int tiga_mp_csr_fwd(const tiga_csr *rel, int32_t feat, const float *x_src, int m
                     const float *w_edge, int reducer, float *y, int32_t *argmax,
                     void *ws, size_t ws_bytes, void *stream);
 
+/* Allocation-free tiga_mp_csr_fwd, for callers that cannot allocate device
+ * memory (work under stream capture, tight serving loops, harnesses that
+ * forbid allocation).  Same arguments, results and errors as tiga_mp_csr_fwd
+ * without the workspace: the library keeps a fixed device array of
+ * tiga_mp_csr_fwd_noalloc_limit() bytes (64 MiB) per device, taken from its
+ * code object when this entry point is first called on that device and held
+ * until the process ends.  A relation whose tiga_mp_csr_fwd_workspace exceeds
+ * the limit is rejected with TIGA_EUNSUPPORTED before anything is enqueued.
+ * The call makes no allocation (no hipMalloc, hipFree or allocating library
+ * routine).  Every call on a device uses that device's one array: calls that
+ * overlap on one device (other streams, other threads) race and must be
+ * serialized by the caller; calls in order on one stream are safe.  The
+ * device is the current device, and `stream` must belong to it. */
+size_t tiga_mp_csr_fwd_noalloc_limit(void);
+int tiga_mp_csr_fwd_noalloc(const tiga_csr *rel, int32_t feat, const float *x_src, int msg,
+                            const float *w_edge, int reducer, float *y, int32_t *argmax,
+                            void *stream);
+
 /* Workspace bytes for tiga_mp_csr_fwd_paged with pages of at most page_edges
  * edges (0 on error).  Independent of the relation's size. */
 size_t tiga_mp_csr_fwd_paged_workspace(int32_t feat, int reducer, int64_t page_edges);

@@ -51,6 +51,9 @@ _SIGS = {
     "tiga_mp_csr_fwd_workspace": (C.c_size_t, [C.c_void_p, C.c_int32, C.c_int]),
     "tiga_mp_csr_fwd": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_int, C.c_void_p, C.c_int, C.c_void_p,
                                   C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tiga_mp_csr_fwd_noalloc_limit": (C.c_size_t, []),
+    "tiga_mp_csr_fwd_noalloc": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_int, C.c_void_p, C.c_int,
+                                          C.c_void_p, C.c_void_p, C.c_void_p]),
     "tiga_mp_csr_bwd_workspace": (C.c_size_t, [C.c_void_p, C.c_int32, C.c_int]),
     "tiga_mp_csr_bwd": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_int, C.c_void_p, C.c_int,
                                   C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
@@ -203,6 +206,26 @@ def tiga_mp_csr_fwd(rel: Csr, x: torch.Tensor, w: torch.Tensor | None = None, re
         ws = _workspace(need, x.device)
     _check(lib.tiga_mp_csr_fwd(rel.ref, feat, _ptr(x), msg, _ptr(w), reducer, _ptr(y), _ptr(argmax),
                                _ptr(ws), ws.numel(), _stream()))
+    return y, argmax
+
+
+def tiga_mp_csr_fwd_noalloc(rel: Csr, x: torch.Tensor, w: torch.Tensor | None = None, reducer: int = REDUCE_SUM,
+                            y: torch.Tensor | None = None, argmax: torch.Tensor | None = None):
+    """tiga_mp_csr_fwd without a workspace (the library's fixed per-device array); pass y (and argmax)
+    to make the whole call allocation-free.  Returns (y, argmax or None)."""
+    lib = load()
+    feat = x.shape[1]
+    _dev(x, torch.float32, "x", (rel.num_src, feat))
+    msg = MSG_SRC
+    if w is not None:
+        _dev(w, torch.float32, "w", (rel.num_edges,))
+        msg = MSG_EDGE_SCALED_SRC
+    if y is None:
+        y = torch.empty(rel.num_dst, feat, dtype=torch.float32, device=x.device)
+    if reducer == REDUCE_MAX and argmax is None:
+        argmax = torch.empty(rel.num_dst, feat, dtype=torch.int32, device=x.device)
+    _check(lib.tiga_mp_csr_fwd_noalloc(rel.ref, feat, _ptr(x), msg, _ptr(w), reducer, _ptr(y), _ptr(argmax),
+                                       _stream()))
     return y, argmax
 
 
