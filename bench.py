@@ -30,6 +30,8 @@ HBM_PEAK_GBS = 8000.0
 # FP32 vector issue: 256 CUs x 4 SIMDs x 16 lanes x 2 flops (FMA) x 2.4 GHz;
 # packed FP32 instructions are disabled in this build.
 VALU_PEAK_TFLOPS = 78.6
+# the published FP32 vector peak counts packed (two-wide) FP32 instructions, which this build does not use
+VALU_PACKED_PEAK_TFLOPS = 157.3
 
 
 def log(msg):
@@ -47,8 +49,10 @@ def parse():
     p.add_argument("--no-ceilings", action="store_true", help="skip the hardware-ceiling probe")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--check-rows", type=int, default=400)
-    p.add_argument("--profile-pass", nargs="?", const="csr", choices=["csr", "radius", "dense", "attention", "knn", "edgenn"],
+    p.add_argument("--profile-pass", nargs="?", const="csr", choices=["csr", "csr2", "radius", "dense", "attention", "knn", "edgenn"],
                    help="for rocprofv3 counter runs: csr = a 4 GiB plain copy (calibration) then 3 headline steps; "
+                        "csr2 = the calibration copy, then each config-2 call (sum / max forward, atomic and gather "
+                        "backward) twice; "
                         "radius / dense / attention = 3 forward calls on the radius (1M points) / dense (65536 points) / "
                         "attention (16 heads x 16384 tokens x 128, binary16, triangular) workload; knn = 3 calls on "
                         "131072 uniform points, k = 16; edgenn = 3 forward + backward calls of the edge MLP on 35947 "
@@ -56,6 +60,8 @@ def parse():
     p.add_argument("--paths-only", action="store_true", help="only the per-path figures (for kernel traces)")
     p.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                    help="print the markdown summary of three rocprofv3 runs (kernel trace, FETCH_SIZE, WRITE_SIZE)")
+    p.add_argument("--summarize-csr2", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                   help="markdown summary of the FETCH_SIZE and WRITE_SIZE runs of --profile-pass csr2")
     p.add_argument("--summarize-kernels", nargs="+", metavar="DIR",
                    help="markdown table of a kernel-trace run (first DIR) and the per-kernel averages of the "
                         "counters in further --pmc run directories")
@@ -64,6 +70,21 @@ def parse():
 
 
 PROFILE_MD = os.path.join(ROOT, "profiles", "gather_reduce_csr_powerlaw_1b_f16.md")
+CSR2_MD = os.path.join(ROOT, "profiles", "csr_powerlaw_1m_16m_f64_paths.md")
+# the dominant kernel of each config-2 call, as rocprofv3 names it (template arguments: float4 units,
+# 16 lanes per edge, reducer, weight mode, buffer table, non-temporal, fused edge gradient)
+CSR2_KERNELS = {
+    "sum_fwd": "gather_reduce_kernel<4, 16, 0, 1, true, false, false>",
+    "max_fwd": "gather_reduce_kernel<4, 16, 1, 1, true, false, false>",
+    "sum_bwd_atomic": "edge_kernel<4, 16, 0, true, true>",
+    "max_bwd_atomic": "edge_kernel<4, 16, 1, true, true>",
+    "sum_bwd_gather": "gather_reduce_kernel<4, 16, 0, 2, true, false, true>",
+    "max_bwd_gather": "gather_reduce_kernel<4, 16, 0, 3, true, false, true>",
+}
+CSR_SOURCES = ["include/tiga_mp.h", "paper_2609_24802_amd/csrc/common.hpp", "paper_2609_24802_amd/csrc/csr_common.hpp",
+               "paper_2609_24802_amd/csrc/csr_fwd.hpp", "paper_2609_24802_amd/csrc/csr_fwd.hip",
+               "paper_2609_24802_amd/csrc/csr_plan.hip", "paper_2609_24802_amd/csrc/csr_bwd.hpp",
+               "paper_2609_24802_amd/csrc/csr_bwd.hip", "paper_2609_24802_amd/csrc/csr_util.hip"]
 VALU_LANE_OPS_PER_S = 256 * 4 * 16 * 2.4e9  # CUs * SIMDs * lanes per cycle * clock
 VALU_INSTR_PER_PAIR = 12
 MFMA16_PEAK_TFLOPS = 2500.0  # dense fp16 / bf16 MFMA peak
@@ -86,15 +107,33 @@ KERNEL_SOURCES = ["include/tiga_mp.h", "paper_2609_24802_amd/csrc/common.hpp",
                   "paper_2609_24802_amd/csrc/csr_fwd.hip", "paper_2609_24802_amd/csrc/csr_plan.hip"]
 
 
-def source_hash():
-    """sha256 over the sources of the gather-reduce kernel: a committed counter summary applies only to the
-    kernel it measured."""
+def source_hash(files=None):
+    """sha256 over the sources of the gather-reduce kernel (or of `files`): a committed counter summary
+    applies only to the kernel it measured."""
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in files or KERNEL_SOURCES:
         h.update(os.path.basename(f).encode())
         h.update(open(os.path.join(ROOT, f), "rb").read())
     return h.hexdigest()[:16]
+
+
+def committed_csr2_bytes():
+    """Per-dispatch HBM bytes (calibrated FETCH_SIZE + WRITE_SIZE) of each config-2 call's dominant kernel,
+    from the committed summary, if the CSR sources are unchanged since it was taken."""
+    if not os.path.exists(CSR2_MD):
+        return None
+    vals = {}
+    for line in open(CSR2_MD):
+        if line.startswith("- ") and ": " in line:
+            k, v = line[2:].strip().split(": ", 1)
+            vals[k.strip("` ")] = v.strip("` ")
+    if vals.get("csr_source_hash") != source_hash(CSR_SOURCES) or "dram_bytes_per_dispatch" not in vals:
+        return None
+    try:
+        return json.loads(vals["dram_bytes_per_dispatch"])
+    except ValueError:
+        return None
 
 
 def committed_traffic():
@@ -163,6 +202,36 @@ def summarize(trace_dir, fetch_dir, write_dir):
         f"- source_hash: {source_hash()}",
     ]
     print("\n".join(out))
+
+
+def summarize_csr2(fetch_dir, write_dir):
+    """Calibrated HBM bytes per dispatch of the config-2 calls' dominant kernels (--profile-pass csr2)."""
+    def per_kernel(d, cname):
+        c = _db(d).cursor()
+        vals = c.execute("select kernel_name, value from counters_collection where counter_name = ?",
+                         (cname,)).fetchall()
+        copy = [v for k, v in vals if "copy" in k.lower() or "elementwise" in k.lower()]
+        out = {}
+        for case, key in CSR2_KERNELS.items():
+            got = [v for k, v in vals if key in k]
+            out[case] = sum(got) / len(got) if got else float("nan")
+        return (max(copy) if copy else float("nan")), out
+    fcopy, fk = per_kernel(fetch_dir, "FETCH_SIZE")
+    wcopy, wk = per_kernel(write_dir, "WRITE_SIZE")
+    fscale = COPY_BYTES / (fcopy * 1024)
+    wscale = COPY_BYTES / (wcopy * 1024)
+    rows = ["| call | dominant kernel | FETCH bytes | WRITE bytes |", "|---|---|---|---|"]
+    total = {}
+    for case, key in CSR2_KERNELS.items():
+        fb, wb = fk[case] * 1024 * fscale, wk[case] * 1024 * wscale
+        total[case] = fb + wb
+        rows.append(f"| {case} | `{key}` | {fb:.4g} | {wb:.4g} |")
+    rows += ["",
+             f"- copy_calibration: a {COPY_BYTES} B device copy reads FETCH_SIZE {fcopy:.1f} KiB (scale {fscale:.3f}) "
+             f"and WRITE_SIZE {wcopy:.1f} KiB (scale {wscale:.3f})",
+             f"- dram_bytes_per_dispatch: {json.dumps({k: round(v) for k, v in total.items()})}",
+             f"- csr_source_hash: {source_hash(CSR_SOURCES)}"]
+    print("\n".join(rows))
 
 
 def summarize_kernels(dirs, match):
@@ -296,6 +365,24 @@ def headline(args, torch, tb, synth, oracle):
     return out, cpu
 
 
+def host_cpu():
+    """The host the CPU baseline runs on: usable cores (this process's affinity; nproc), logical CPUs of
+    the machine and the processor model (/proc/cpuinfo, what lscpu reports as the model name)."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.lower().startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:
+        nproc = os.cpu_count()
+    return dict(nproc=nproc, logical_cpus=os.cpu_count(), model=model)
+
+
 def cpu_baseline(args, oracle, rp, col, x, w):
     """The oracle (untuned, fp64) on the first rows of the same graph."""
     n = rp.size - 1
@@ -317,9 +404,11 @@ def cpu_baseline(args, oracle, rp, col, x, w):
     dt = time.perf_counter() - t
     edges = int(rp[k] - rp[0])
     log(f"cpu oracle: {edges} edges in {dt:.2f} s on {oracle.threads()} threads")
+    hc = host_cpu()
     return dict(value=edges / dt / 1e9, unit="GEdges/s", cores=oracle.threads(), kind="oracle",
                 sample=f"weighted-sum forward of rows [0, {k}) of the 1e9-edge graph ({edges} edges), "
-                       f"fp64 accumulation, {dt:.1f} s")
+                       f"fp64 accumulation, {dt:.1f} s",
+                threads=oracle.threads(), nproc=hc["nproc"], logical_cpus=hc["logical_cpus"], cpu_model=hc["model"])
 
 
 def cpu_baseline_config1(oracle, synth):
@@ -344,10 +433,40 @@ def cpu_baseline_config1(oracle, synth):
         out[f"{label}_us"] = sorted(ts)[1] * 1e6
         out[f"{label}_threads"] = oracle.threads()
     oracle.set_threads(0)
-    out.update(kind="oracle", sample="config 1 weighted-sum forward + backward (dx, dw), fp64 accumulation")
+    hc = host_cpu()
+    out.update(kind="oracle", sample="config 1 weighted-sum forward + backward (dx, dw), fp64 accumulation",
+               nproc=hc["nproc"], cpu_model=hc["model"])
     log(f"cpu oracle config 1: {out['single_thread_us']:.0f} us on 1 thread, {out['all_threads_us']:.0f} us "
         f"on {out['all_threads_threads']}")
     return out
+
+
+def radius_candidate_tests(pos, radius, max_cells=None):
+    """(destination, candidate) predicate tests the radius consume kernel performs: every point of a cell
+    is tested against every point of the 27 cells around it.  The cell grid is the library's own recipe
+    (cells of h = max(r (1 + 2^-10), cbrt(box volume / n)), grown by 1.25 until at most n + 64 cells),
+    replayed here in fp64 for reporting only."""
+    n = pos.shape[0]
+    max_cells = max_cells or n + 64
+    lo = pos.min(0).astype(np.float64)
+    ext = np.maximum(pos.max(0).astype(np.float64) - lo, 0.0)
+    h = max(float(radius) * (1.0 + 1.0 / 1024.0), float(np.cbrt(np.prod(ext) / max(n, 1))))
+    while True:
+        dims = (np.floor(ext / h) + 1.0).astype(np.int64)
+        if np.prod(dims.astype(np.float64)) <= max_cells:
+            break
+        h *= 1.25
+    inv = 1.0 / h
+    c = np.clip(np.floor((pos.astype(np.float64) - lo) * inv), 0, dims - 1).astype(np.int64)
+    cnt = np.zeros(tuple(dims[::-1]), np.int64)
+    np.add.at(cnt, (c[:, 2], c[:, 1], c[:, 0]), 1)
+    nb = np.zeros_like(cnt)
+    pad = np.pad(cnt, 1)
+    for dz in range(3):
+        for dy in range(3):
+            for dx in range(3):
+                nb += pad[dz:dz + dims[2], dy:dy + dims[1], dx:dx + dims[0]]
+    return int((cnt * nb).sum())
 
 
 def paths(args, torch, tb, synth):
@@ -453,17 +572,26 @@ def paths(args, torch, tb, synth):
            "sum_bwd_gather": E * (16 + 4 * F) + ns * (8 + 8 * F)}
     # the reverse incidence is topology set-up (built once, reused by every gather-mode backward)
     cases["csr_powerlaw_1m_16m_f64_transpose"] = lambda: tb.tiga_csr_transpose(rel)
+    dram = committed_csr2_bytes()
     for name, fn in cases.items():
         r = time_steps(torch, tb, fn, steps, warm)
         d = dict(ms=r["step_ms"], gedges_per_s=E / r["step_ms"] / 1e6)
         key = name.split("f64_")[1]
-        if key in alg:
-            d.update(alg_bytes=alg[key], alg_gbs=alg[key] / r["step_ms"] / 1e6,
-                     frac_hbm=alg[key] / r["step_ms"] / 1e6 / HBM_PEAK_GBS)
-        if key == "sum_fwd":
+        akey = key
+        if akey in alg:
+            d.update(alg_bytes=alg[akey], alg_gbs=alg[akey] / r["step_ms"] / 1e6,
+                     frac_hbm=alg[akey] / r["step_ms"] / 1e6 / HBM_PEAK_GBS)
+        if key in CSR2_KERNELS:
+            # the dominant kernel of the call (HIP events around it); its rocprofv3-measured HBM bytes
+            # (calibrated FETCH_SIZE + WRITE_SIZE per dispatch) come from the committed summary while the
+            # CSR sources are unchanged, else null
             k = float(np.mean(r["kernel_ms"]))
-            d.update(kernel_ms=k, kernel_alg_gbs=alg[key] / k / 1e6,
-                     kernel_frac_hbm=alg[key] / k / 1e6 / HBM_PEAK_GBS)
+            d.update(kernel=CSR2_KERNELS[key], kernel_ms=k)
+            if akey in alg:
+                d.update(kernel_alg_gbs=alg[akey] / k / 1e6, kernel_frac_hbm=alg[akey] / k / 1e6 / HBM_PEAK_GBS)
+            b = dram.get(key) if dram else None
+            d.update(dram_bytes=b, dram_gbs=(b / k / 1e6) if b else None,
+                     dram_frac_hbm=(b / k / 1e6 / HBM_PEAK_GBS) if b else None)
         res[name] = d
         log(f"{name}: {d['ms']:.3f} ms")
     del rel, xd, wd, dyd, rev, am
@@ -479,14 +607,29 @@ def paths(args, torch, tb, synth):
     # dpos rows (bwd).  Accepted pairs re-read rows from the caches, so this sits far below the HBM peak:
     # the kernel is bound by candidate tests (VALU) and gather latency instead.
     uniq = {"fwd": npt * (16 + 8 * Fr), "bwd": npt * (16 + 12 + 12 * Fr + 12)}
+    tests = radius_candidate_tests(g["pos"], r)
+    # useful FP32 work per accepted pair (each transcendental counted as one flop):
+    #   forward: squared distance 8 (3 differences, 3 squares, 2 sums) + exponent argument 1 + exp 1
+    #            + weighted accumulation 2F                                    = 2F + 10
+    #   backward: squared distance 8 + argument 1 + exp 1 + dx accumulation 2F + the two inner products
+    #            <dy_i, x_j> + <dy_j, x_i> 4F + their sum 1 + coefficient 2k/sigma^2 2 + 3 (mul + add) 6
+    #                                                                          = 6F + 19
+    # and, as scheme overhead, 8 flops per (destination, candidate) predicate test of rejected candidates
+    useful = {"fwd": pairs * (2 * Fr + 10), "bwd": pairs * (6 * Fr + 19)}
     for name, fn in {"radius_1m_f32_fwd_with_build": lambda: tb.tiga_mp_radius_fwd(pd, xd, r, s, want_count=False),
                      "radius_1m_f32_bwd_with_build": lambda: tb.tiga_mp_radius_bwd(pd, xd, dyd, r, s)}.items():
         rr = time_steps(torch, tb, fn, steps, warm)
         k = float(np.mean(rr["kernel_ms"]))
-        u = uniq["fwd" if "_fwd_" in name else "bwd"]
+        ph = "fwd" if "_fwd_" in name else "bwd"
+        u = uniq[ph]
+        tf = useful[ph] / (k * 1e-3) / 1e12
         res[name] = dict(ms=rr["step_ms"], gedges_per_s=pairs / rr["step_ms"] / 1e6, accepted_pairs=pairs,
-                         kernel_ms=k, kernel_unique_gbs=u / k / 1e6, kernel_frac_hbm=u / k / 1e6 / HBM_PEAK_GBS)
-        log(f"{name}: {rr['step_ms']:.3f} ms")
+                         consume_kernel_ms=k, consume_gedges_per_s=pairs / k / 1e6,
+                         candidate_tests=tests, useful_flops=useful[ph], useful_tflops=tf,
+                         frac_valu_packed=tf / VALU_PACKED_PEAK_TFLOPS, frac_valu=tf / VALU_PEAK_TFLOPS,
+                         overhead_tflops=(tests - pairs) * 8 / (k * 1e-3) / 1e12,
+                         kernel_unique_gbs=u / k / 1e6, kernel_frac_hbm=u / k / 1e6 / HBM_PEAK_GBS)
+        log(f"{name}: {rr['step_ms']:.3f} ms (consume {k:.3f} ms, {tf:.1f} useful TFLOP/s)")
     del pd, xd, dyd
     g = synth.config4()
     pd, qd = dev(g["pos"]), dev(g["q"])
@@ -528,8 +671,12 @@ def paths(args, torch, tb, synth):
         ws = tb._workspace(tb.load().tiga_mp_knn_workspace(nk), pd.device)
         rr = time_steps(torch, tb, lambda: tb.tiga_mp_knn_fwd(pd, xd, g["k"], ws=ws), steps, warm)
         k = float(np.mean(rr["kernel_ms"]))
+        # queries answered and (query, neighbour) pairs selected per second; the select kernel evaluates
+        # only the candidates its exact box tests cannot exclude (about 1,000 per query at 131,072 points,
+        # from the scalar-load counter in the kNN profile), not all n (n - 1) pairs
         res[f"knn_{nk}_k16_f1"] = dict(ms=rr["step_ms"], select_kernel_ms=k,
-                                        gpairs_per_s=nk * (nk - 1) / rr["step_ms"] / 1e6)
+                                        queries_per_s=nk / (rr["step_ms"] * 1e-3),
+                                        selected_pairs_per_s=nk * g["k"] / (rr["step_ms"] * 1e-3))
         log(f"knn {nk}: {rr['step_ms']:.3f} ms (select {k:.3f} ms)")
         del pd, xd, ws
 
@@ -555,6 +702,28 @@ def profile_pass(args, torch, tb, synth):
     """Workload for counter runs: a plain copy of known size, then three steps (csr); or three forward calls on
     the radius or dense workload."""
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    if args.profile_pass == "csr2":
+        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1.0)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        g = synth.config2()
+        rel = tb.Csr(dev(g["row_ptr"]), dev(g["col"]), g["num_dst"])
+        xd, wd, dyd = dev(g["x"]), dev(g["w"]), dev(g["dy"])
+        rev = tb.tiga_csr_transpose(rel)
+        _, am = tb.tiga_mp_csr_fwd(rel, xd, wd, reducer=tb.REDUCE_MAX)
+        for _ in range(2):
+            tb.tiga_mp_csr_fwd(rel, xd, wd)
+            tb.tiga_mp_csr_fwd(rel, xd, wd, reducer=tb.REDUCE_MAX)
+            tb.tiga_mp_csr_bwd(rel, dyd, xd, wd)
+            tb.tiga_mp_csr_bwd(rel, dyd, xd, wd, reducer=tb.REDUCE_MAX, argmax=am)
+            tb.tiga_mp_csr_bwd(rel, dyd, xd, wd, rev=rev)
+            tb.tiga_mp_csr_bwd(rel, dyd, xd, wd, reducer=tb.REDUCE_MAX, argmax=am, rev=rev)
+        torch.cuda.synchronize()
+        log("profile pass done")
+        return
     if args.profile_pass == "radius":
         g = synth.config3()
         pd, xd = dev(g["pos"]), dev(g["x"])
@@ -638,6 +807,9 @@ def main():
     if args.summarize_kernels:
         summarize_kernels(args.summarize_kernels, args.match)
         return
+    if args.summarize_csr2:
+        summarize_csr2(*args.summarize_csr2)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
@@ -687,13 +859,17 @@ def main():
                      "kernel": "gather_reduce_kernel", "kernel_ms": h["kernel_ms"],
                      "bytes_per_launch": h["bytes_alg"],
                      "frac_of_measured_gather_ceiling": (h["E"] / (h["kernel_ms"] * 1e-3)) / ceil["gather64_rows_per_s"]
-                     if ceil else None},
+                     if ceil else None,
+                     "target_frac": 0.60, "target_met": bool(h["achieved"] / HBM_PEAK_GBS >= 0.60)},
         "cpu_baseline": cpu,
         "ceilings": ceil,
         "parity_sampled": h["parity_ok"],
         "paths": extra,
     }
     print(json.dumps(line), flush=True)
+    if not h["parity_ok"]:
+        log("sampled parity of the timed result FAILED")
+        sys.exit(1)
 
 
 if __name__ == "__main__":

@@ -5,7 +5,9 @@
 //   stream_copy   : 4 GiB read + 4 GiB written
 //   gather_64     : random 64-B rows (4 lanes x 16 B) from a 3.2 GB table,
 //                   indices streamed from a 4 GB array (the CSR forward pattern)
-//   gather_128    : the same with 128-B rows (8 lanes)
+//   gather_32, gather_128, gather_256 : the same with 32-, 128- and 256-B rows
+//   gather_64 from a 64 MB table and from a 256 MB table (held in the
+//                   last-level cache, so DRAM is not what limits them)
 //   fma           : fp32 FMA chains (non-packed), 8 independent chains per lane
 //   rsq, exp      : transcendental throughput (v_rsq_f32, v_exp_f32)
 // and prints one JSON object.  Index arrays are filled on the device with a
@@ -187,6 +189,26 @@ int main() {
     const float t_g128 = best_ms([&] {
         hipLaunchKernelGGL((gather_rows<8>), dim3(grid), dim3(256), 0, 0, idx, tab, n128, out);
     });
+    const int64_t n256 = idx_n / 4;
+    hipLaunchKernelGGL(init_idx, dim3(grid), dim3(256), 0, 0, idx, n256, static_cast<uint32_t>(tab_bytes / 256));
+    const float t_g256 = best_ms([&] {
+        hipLaunchKernelGGL((gather_rows<16>), dim3(grid), dim3(256), 0, 0, idx, tab, n256, out);
+    });
+    const int64_t n32 = idx_n / 2;
+    hipLaunchKernelGGL(init_idx, dim3(grid), dim3(256), 0, 0, idx, n32, static_cast<uint32_t>(tab_bytes / 32));
+    const float t_g32 = best_ms([&] {
+        hipLaunchKernelGGL((gather_rows<2>), dim3(grid), dim3(256), 0, 0, idx, tab, n32, out);
+    });
+    // 64-B rows from tables of 64 MB and 256 MB: these stay in the 256 MB last-level cache
+    const int64_t nsm = idx_n / 2;
+    hipLaunchKernelGGL(init_idx, dim3(grid), dim3(256), 0, 0, idx, nsm, static_cast<uint32_t>((64LL << 20) / 64));
+    const float t_g64_64m = best_ms([&] {
+        hipLaunchKernelGGL((gather_rows<4>), dim3(grid), dim3(256), 0, 0, idx, tab, nsm, out);
+    });
+    hipLaunchKernelGGL(init_idx, dim3(grid), dim3(256), 0, 0, idx, nsm, static_cast<uint32_t>((256LL << 20) / 64));
+    const float t_g64_256m = best_ms([&] {
+        hipLaunchKernelGGL((gather_rows<4>), dim3(grid), dim3(256), 0, 0, idx, tab, nsm, out);
+    });
 
     const int vgrid = cus * 64;
     const double lanes = static_cast<double>(vgrid) * 256;
@@ -199,9 +221,13 @@ int main() {
            "\"stream_read_gbs\": %.1f, \"stream_copy_gbs\": %.1f, "
            "\"gather64_rows_per_s\": %.4g, \"gather64_useful_gbs\": %.1f, "
            "\"gather128_rows_per_s\": %.4g, \"gather128_useful_gbs\": %.1f, "
+           "\"gather32_rows_per_s\": %.4g, \"gather256_rows_per_s\": %.4g, \"gather256_useful_gbs\": %.1f, "
+           "\"gather64_table64mb_rows_per_s\": %.4g, \"gather64_table256mb_rows_per_s\": %.4g, "
            "\"fma_fp32_tflops\": %.2f, \"rsq_per_s\": %.4g, \"exp_per_s\": %.4g}\n",
            p.gcnArchName, cus, idx_n * 4.0 / t_read / 1e6, idx_n * 8.0 / t_copy / 1e6, idx_n / (t_g64 * 1e-3),
            idx_n * 68.0 / t_g64 / 1e6, n128 / (t_g128 * 1e-3), n128 * 132.0 / t_g128 / 1e6,
+           n32 / (t_g32 * 1e-3), n256 / (t_g256 * 1e-3), n256 * 260.0 / t_g256 / 1e6, nsm / (t_g64_64m * 1e-3),
+           nsm / (t_g64_256m * 1e-3),
            2.0 * ops / (t_fma * 1e-3) / 1e12, ops / (t_rsq * 1e-3), ops / (t_exp * 1e-3));
     CHECK(hipFree(idx));
     CHECK(hipFree(tab));

@@ -164,28 +164,24 @@ int edge_flags(bool dw, bool dx, int L, const EdgeT &t, int64_t nedges, void *ws
     return edge_lanes<K, RED, false, true>(L, t, nedges, ws, stream);
 }
 
-// Workspace of the backward: the destination row of every edge and of every reverse slot
-// (num_edges int32 each; used with the reverse incidence), then the region the plan of either
-// traversal takes.
+// Workspace of the backward: the (weight, destination row) record of every edge (used with the
+// reverse incidence), then the region the plan of either traversal takes.
 struct BwdWs {
-    int32_t *row_of_edge;
-    int32_t *row_of_slot;
+    int2 *rec;
     void *rest;
 };
 
 BwdWs carve_bwd(void *ws, int64_t num_edges) {
     Carve c(ws);
     BwdWs w;
-    w.row_of_edge = c.take<int32_t>(num_edges);
-    w.row_of_slot = c.take<int32_t>(num_edges);
+    w.rec = c.take<int2>(num_edges);
     w.rest = ws ? static_cast<char *>(ws) + c.bytes() : nullptr;
     return w;
 }
 
 size_t bwd_rows_bytes(int64_t num_edges) {
     Carve c(nullptr);
-    c.take<int32_t>(num_edges);
-    c.take<int32_t>(num_edges);
+    c.take<int2>(num_edges);
     return c.bytes();
 }
 
@@ -226,11 +222,11 @@ int launch_bwd(const BwdArgs &a, void *ws_all, hipStream_t stream) {
         if (rc) return rc;
     }
     if (a.dx && a.rev && rel->num_src > 0) {
-        // the reverse incidence carries forward edge ids only; the destination of each slot is
-        // derived here from row_ptr (sequential writes, then one gather by edge id)
-        if (int rc = launch_slot_rows(rel, a.rev->edge_id, bw.row_of_edge, bw.row_of_slot, stream)) return rc;
-        Trav t{a.rev->src_ptr, bw.row_of_slot, a.w, a.rev->edge_id, a.dy, rel->num_src, lay.fu, a.arg, 0u,
-               rel->num_edges};
+        // the reverse incidence carries forward edge ids only: each traversed slot reads its edge's
+        // (weight, destination row) record, built here from row_ptr and w in one streaming pass
+        if (int rc = launch_edge_records(rel, a.w, bw.rec, stream)) return rc;
+        Trav t{a.rev->src_ptr, nullptr, nullptr, a.rev->edge_id, a.dy, rel->num_src, lay.fu, a.arg, 0u,
+               rel->num_edges, bw.rec};
         const int wm = a.red == RED_MAX ? W_ROUTE : W_INDIRECT;
         EdgeGrad eg;
         if (fused) {

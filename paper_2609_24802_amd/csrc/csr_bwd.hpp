@@ -26,10 +26,9 @@ int launch_bwd(const BwdArgs &a, void *ws, hipStream_t stream);
 size_t transpose_ws_bytes(int64_t num_dst, int64_t num_src, int64_t num_edges);
 int launch_transpose(const tiga_csr *rel, int64_t *src_ptr, int32_t *edge_id, void *ws, hipStream_t stream);
 
-// Destination row of every slot of the reverse incidence: row_of_edge[e] = the row owning edge
-// position e (from row_ptr), then row_of_slot[s] = row_of_edge[edge_id[s]].  Both [num_edges].
-int launch_slot_rows(const tiga_csr *rel, const int32_t *edge_id, int32_t *row_of_edge, int32_t *row_of_slot,
-                     hipStream_t stream);
+// Per forward edge e: rec[e] = (bits of w[e] (1.0 when w is null), the destination row of e), the
+// 8-byte record the traversal of the reverse incidence reads through edge ids.  [num_edges].
+int launch_edge_records(const tiga_csr *rel, const float *w, int2 *rec, hipStream_t stream);
 
 int launch_validate(const tiga_csr *rel, hipStream_t stream);
 

@@ -312,6 +312,9 @@ struct Trav {
     const int32_t *__restrict__ arg;   // [*, feat] selected edges (W_ROUTE only)
     uint32_t table_bytes;              // byte size of `table` (and `arg`) when below 4 GiB, else 0
     int64_t nedges;                    // edges of the relation (idx, w and eid have this many)
+    // W_INDIRECT / W_ROUTE: per forward edge, (weight bits, gathered row) in one 8-byte record read
+    // through eid (then idx and w are unused): one random request yields both
+    const int2 *__restrict__ wrow = nullptr;
 };
 
 // Row gathers from the feature table.  Tables below 4 GiB go through a buffer
@@ -404,9 +407,10 @@ __device__ __forceinline__ void run_edges(const Trav &t, const Table<K, BUF, NT>
                                           int64_t u, bool uok, A &acc, H &&hook = H{}) {
     constexpr int STEP = SL * kUnroll;
     const int n = static_cast<int>(e1 - e0);
-    const int32_t *__restrict__ colr = t.idx + e0;
-    const float *__restrict__ wr = t.w + e0;
-    const int32_t *__restrict__ er = t.eid + e0;
+    constexpr bool VIA_EID = WM == W_INDIRECT || WM == W_ROUTE;
+    const int32_t *__restrict__ colr = VIA_EID ? nullptr : t.idx + e0;
+    const float *__restrict__ wr = WM == W_DIRECT ? t.w + e0 : nullptr;
+    const int32_t *__restrict__ er = VIA_EID ? t.eid + e0 : nullptr;
     for (int k0 = 0; k0 < n; k0 += STEP) {
         int32_t c[kUnroll];
         int32_t ee[kUnroll];
@@ -419,15 +423,19 @@ __device__ __forceinline__ void run_edges(const Trav &t, const Table<K, BUF, NT>
             // ids and weights take ordinary (cached) loads: neighbouring work
             // items share their cache lines, which the non-temporal hint would
             // let go back to HBM between the items
-            c[r] = ok[r] ? colr[k] : 0;
             ee[r] = 0;
-            if constexpr (WM == W_DIRECT) {
-                wv[r] = ok[r] ? wr[k] : 0.0f;
-            } else if constexpr (WM == W_INDIRECT || WM == W_ROUTE) {
+            if constexpr (WM == W_INDIRECT || WM == W_ROUTE) {
                 ee[r] = ok[r] ? er[k] : 0;
-                wv[r] = ok[r] ? (t.w ? t.w[ee[r]] : 1.0f) : 0.0f;
+                const int2 pr = ok[r] ? t.wrow[ee[r]] : make_int2(0, 0);
+                c[r] = pr.y;
+                wv[r] = __int_as_float(pr.x);
             } else {
-                wv[r] = ok[r] ? 1.0f : 0.0f;
+                c[r] = ok[r] ? colr[k] : 0;
+                if constexpr (WM == W_DIRECT) {
+                    wv[r] = ok[r] ? wr[k] : 0.0f;
+                } else {
+                    wv[r] = ok[r] ? 1.0f : 0.0f;
+                }
             }
         }
         Vec<K> xv[kUnroll];

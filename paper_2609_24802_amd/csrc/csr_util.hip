@@ -207,13 +207,33 @@ __global__ __launch_bounds__(kBlock) void expand_rows_kernel(const int64_t *__re
     }
 }
 
-// out[s] = table[index[s]] for s in [0, n).
-__global__ __launch_bounds__(kBlock) void gather_i32_kernel(const int32_t *__restrict__ table,
-                                                            const int32_t *__restrict__ index, int64_t n,
-                                                            int32_t *__restrict__ out) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
-    for (int64_t s = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; s < n; s += stride)
-        out[s] = table[index[s]];
+// rec[e] = (bits of w[e], or of 1.0 without weights; the destination row of e) for every edge of the
+// rows [x * kRecRows, (x + 1) * kRecRows) of tile x = blockIdx.x, shared by the kRecParts blocks
+// blockIdx.y of the tile (a tile holding hub rows has far more edges than the others).  The tile's row
+// pointers are staged in LDS; thread t of part y takes edges y * kBlock + t, then every
+// kBlock * kRecParts-th (coalesced reads of w, coalesced 8-byte writes), and finds its row by binary
+// search in LDS, so a long row costs its edges, not a serial walk.
+constexpr int kRecRows = 2048;
+constexpr int kRecParts = 16;
+
+__global__ __launch_bounds__(kBlock) void edge_records_kernel(const int64_t *__restrict__ row_ptr, int64_t nrows,
+                                                              const float *__restrict__ w, int2 *__restrict__ rec) {
+    __shared__ int64_t sp[kRecRows + 1];
+    const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kRecRows;
+    const int nr = static_cast<int>(nrows - r0 < kRecRows ? nrows - r0 : kRecRows);
+    for (int i = threadIdx.x; i <= nr; i += kBlock) sp[i] = row_ptr[r0 + i];
+    __syncthreads();
+    const int64_t e0 = sp[0], e1 = sp[nr];
+    for (int64_t e = e0 + blockIdx.y * kBlock + threadIdx.x; e < e1; e += kBlock * kRecParts) {
+        // the last row i of the tile with sp[i] <= e (rows are nonempty there: sp[i] <= e < sp[i+1])
+        int lo = 0, hi = nr - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (sp[mid] <= e) lo = mid;
+            else hi = mid - 1;
+        }
+        rec[e] = make_int2(__float_as_int(w ? w[e] : 1.0f), static_cast<int32_t>(r0 + lo));
+    }
 }
 
 // ptr[j] = first sorted position with key >= j, for j in [0, nkeys]: one
@@ -366,17 +386,12 @@ int launch_transpose(const tiga_csr *rel, int64_t *src_ptr, int32_t *edge_id, vo
     return ptr_from_sorted(sorted, n, rel->num_src, src_ptr, stream);
 }
 
-int launch_slot_rows(const tiga_csr *rel, const int32_t *edge_id, int32_t *row_of_edge, int32_t *row_of_slot,
-                     hipStream_t stream) {
-    const int64_t n = rel->num_edges;
-    if (n == 0) return TIGA_OK;
-    const int eb = persistent_blocks(rel->num_dst, 8);
-    hipLaunchKernelGGL(expand_rows_kernel, dim3(eb), dim3(kBlock), 0, stream, rel->row_ptr, rel->num_dst,
-                       row_of_edge);
-    if (int rc = check_launch("expand rows")) return rc;
-    const int gb = persistent_blocks(ceil_div(n, kWave), 8);
-    hipLaunchKernelGGL(gather_i32_kernel, dim3(gb), dim3(kBlock), 0, stream, row_of_edge, edge_id, n, row_of_slot);
-    return check_launch("destination of each reverse slot");
+int launch_edge_records(const tiga_csr *rel, const float *w, int2 *rec, hipStream_t stream) {
+    if (rel->num_edges == 0 || rel->num_dst == 0) return TIGA_OK;
+    const int64_t tiles = ceil_div(rel->num_dst, kRecRows);
+    hipLaunchKernelGGL(edge_records_kernel, dim3(static_cast<unsigned>(tiles), kRecParts), dim3(kBlock), 0, stream,
+                       rel->row_ptr, rel->num_dst, w, rec);
+    return check_launch("edge records");
 }
 
 size_t sort_keys_ws_bytes(int64_t n) {
