@@ -11,9 +11,12 @@
 //                           one long chunk or several short ones.  A row of
 //                           several chunks writes partial states that a merge
 //                           kernel combines in chunk order.
-// Chunk descriptors come from a deterministic plan (count per tile, scan,
-// write) without global atomics; each carries its edge range, so a work item
-// needs no dependent row-pointer load.
+// Chunk descriptors come from a one-pass plan: each block of rows scans its
+// own rows' needs and reserves its descriptor range with one atomic add per
+// class; each descriptor carries its edge range, so a work item needs no
+// dependent row-pointer load.  Where a block's range lands depends on timing,
+// but every chunk's reduction and every split row's merge (in chunk order)
+// do not, so results are deterministic.
 //
 // Lane layout: a feature row is FU "units" (float4 when the vector path
 // applies, else float).  L lanes (a power of two >= FU, at most 64) cover one
@@ -96,24 +99,44 @@ struct alignas(16) Split {
     int32_t pad;
 };
 
-// Written by the plan: chunks of each class (stored class after class),
-// partial slots, split rows.
+// Written by the plan: chunks of each class, partial slots and split rows
+// reserved so far (atomic counters, cleared by the plan's first kernel), and
+// the first descriptor of classes 1 and 2 (class c's descriptors live in their
+// own region of the chunk array, sized by PlanBounds::cap).
+// Each counter sits on a cache line of its own (k < kClasses: chunks of class k; then partial
+// slots, then split rows), so that the tiles' reservations on different counters proceed in
+// parallel in different L2 channels.
+struct alignas(256) PlanCounter {
+    unsigned long long v;
+};
+enum { kCtrSlots = kClasses, kCtrSplits = kClasses + 1 };
 struct PlanCounts {
-    unsigned long long cls[kClasses];
-    unsigned long long slots, splits;
-    unsigned long long pad[3];
+    PlanCounter ctr[kPlanVals];
+    unsigned long long off[2];
 };
 
 struct PlanBounds {
-    int64_t tiles, max_chunks, max_slots, max_splits;
+    int64_t tiles, cap[kClasses], max_chunks, max_slots, max_splits;
 };
 
+// Capacities: a chunk of class c holds more than lo_c edges (class 0: a full
+// chunk, or a last chunk longer than the class-1 bound; class c > 0: a last
+// chunk longer than the next class's bound, or than the short-row bound), and
+// every class-1 or class-2 chunk ends a distinct row.
 inline PlanBounds plan_bounds(int64_t nrows, int64_t nedges, const Geom &g) {
     PlanBounds b;
     b.tiles = ceil_div(nrows > 0 ? nrows : 1, kPlanTile);
-    int64_t long_rows = nedges / (g.DS + 1);
-    if (long_rows > nrows) long_rows = nrows;
-    b.max_chunks = long_rows + nedges / g.CH + 1;
+    for (int c = 0; c < kClasses; ++c) {
+        int64_t cap = 0;
+        if (c < g.nclass) {
+            const int64_t lo = c + 1 < g.nclass ? g.cap[c + 1] : g.DS;
+            cap = nedges / (lo + 1);
+            if (c > 0 && cap > nrows) cap = nrows;
+            cap += 1;
+        }
+        b.cap[c] = cap;
+    }
+    b.max_chunks = b.cap[0] + b.cap[1] + b.cap[2];
     b.max_splits = nedges / (g.CH + 1) + 1;
     b.max_slots = 2 * (nedges / g.CH) + 2;
     return b;
@@ -123,8 +146,7 @@ inline PlanBounds plan_bounds(int64_t nrows, int64_t nedges, const Geom &g) {
 // max) per slot.
 struct PlanWs {
     PlanCounts *counts;
-    int64_t *tile_vals;  // kPlanVals per tile (counts, then offsets)
-    Desc *chunks;
+    Desc *chunks;  // class 0 at [0, cap0), class 1 at [cap0, cap0 + cap1), class 2 after
     Split *splits;
     float *part_v;
     int32_t *part_e;
@@ -133,7 +155,6 @@ struct PlanWs {
 inline PlanWs carve_plan(Carve &c, const PlanBounds &b, int64_t feat, bool with_arg) {
     PlanWs w;
     w.counts = c.take<PlanCounts>(1);
-    w.tile_vals = c.take<int64_t>(kPlanVals * b.tiles);
     w.chunks = c.take<Desc>(b.max_chunks);
     w.splits = c.take<Split>(b.max_splits);
     w.part_v = c.take<float>(b.max_slots * feat);
@@ -141,7 +162,8 @@ inline PlanWs carve_plan(Carve &c, const PlanBounds &b, int64_t feat, bool with_
     return w;
 }
 
-// Enqueue the plan (three kernels) for rows [0, nrows) of `ptr`.
+// Enqueue the plan (two kernels: clear the counters, then one pass over the rows) for rows
+// [0, nrows) of `ptr`.
 int launch_plan(const int64_t *ptr, int64_t nrows, const Geom &g, const PlanBounds &b,
                 const PlanWs &w, hipStream_t stream);
 
@@ -480,11 +502,11 @@ struct Items {
 
 __device__ __forceinline__ Items make_items(const PlanCounts *__restrict__ pc, int64_t n_groups) {
     Items it;
-    it.n0 = static_cast<int64_t>(pc->cls[0]);
-    it.n1 = static_cast<int64_t>(pc->cls[1]);
-    it.n2 = static_cast<int64_t>(pc->cls[2]);
-    it.b1 = it.n0;
-    it.b2 = it.n0 + it.n1;
+    it.n0 = static_cast<int64_t>(pc->ctr[0].v);
+    it.n1 = static_cast<int64_t>(pc->ctr[1].v);
+    it.n2 = static_cast<int64_t>(pc->ctr[2].v);
+    it.b1 = static_cast<int64_t>(pc->off[0]);
+    it.b2 = static_cast<int64_t>(pc->off[1]);
     it.s1 = it.n0;
     it.s2 = it.s1 + (it.n1 + 1) / 2;
     it.s3 = it.s2 + (it.n2 + 3) / 4;

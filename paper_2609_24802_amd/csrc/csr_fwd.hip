@@ -139,7 +139,7 @@ __global__ __launch_bounds__(kBlock) void merge_kernel(const Split *__restrict__
     const int lane = lane_id();
     const int64_t wave = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
     const int64_t nwaves = static_cast<int64_t>(gridDim.x) * kWavesPerBlock;
-    const int64_t n_split = static_cast<int64_t>(counts->splits);
+    const int64_t n_split = static_cast<int64_t>(counts->ctr[kCtrSplits].v);
     const int s = lane / L;
     const int l = lane % L;
     for (int64_t it = wave; it < n_split; it += nwaves) {

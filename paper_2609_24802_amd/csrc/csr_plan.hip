@@ -1,12 +1,13 @@
-// Degree-aware row plan (deterministic; no global atomics).
+// Degree-aware row plan, one pass over the rows.
 //
-// count: per tile of kPlanTile rows, the chunks of each class, partial slots
-//        and split rows its non-short rows need;
-// scan:  exclusive prefix over tiles (one block), totals to PlanCounts;
-// write: each tile recomputes its rows and writes descriptors at its offsets,
-//        in row order within each class; class c's descriptors follow those
-//        of classes 0..c-1.
-// Descriptor positions depend only on the topology.
+// init: clear the counters and record where classes 1 and 2 start in the
+//       chunk array (each class has a region of its own capacity);
+// plan: each block takes a tile of kPlanTile rows, scans the chunks of each
+//       class, partial slots and split rows its rows need (block-local scan),
+//       reserves those ranges with one atomic add per counter, and writes the
+//       descriptors in row order within its ranges.
+// Only rows longer than the short-row bound get descriptors; short rows are
+// taken in natural order by the traversal itself.
 #include "csr_common.hpp"
 
 namespace tiga {
@@ -79,75 +80,11 @@ __device__ __forceinline__ Need block_excl_scan(const Need &v, Need &excl) {
     return tot;
 }
 
-template <int L>
-__global__ __launch_bounds__(kBlock) void plan_count_kernel(const int64_t *__restrict__ ptr, int64_t nrows,
-                                                            int64_t *__restrict__ tile_vals) {
-    constexpr Geom g = make_geom(L);  // compile-time chunk geometry: divisions by constants
-    const int64_t base = static_cast<int64_t>(blockIdx.x) * kPlanTile;
-    Need acc;
-#pragma unroll
-    for (int k = 0; k < kPlanVals; ++k) acc.v[k] = 0;
-#pragma unroll
-    for (int r = 0; r < kPlanRowsPerThread; ++r) {
-        int64_t e0, deg;
-        const Need n = row_need(g, ptr, base + r * kBlock + threadIdx.x, nrows, e0, deg);
-#pragma unroll
-        for (int k = 0; k < kPlanVals; ++k) acc.v[k] += n.v[k];
-    }
-    // block totals: wave sums, then thread 0 adds the waves
-    __shared__ int64_t sh[kPlanVals][kWavesPerBlock];
-#pragma unroll
-    for (int k = 0; k < kPlanVals; ++k) {
-        int64_t v = acc.v[k];
-#pragma unroll
-        for (int m = 1; m < kWave; m <<= 1) v += __shfl_xor(v, m, kWave);
-        if (lane_id() == 0) sh[k][threadIdx.x / kWave] = v;
-    }
-    __syncthreads();
+__global__ void plan_init_kernel(PlanCounts *__restrict__ counts, int64_t off1, int64_t off2) {
+    if (threadIdx.x < kPlanVals) counts->ctr[threadIdx.x].v = 0;
     if (threadIdx.x == 0) {
-#pragma unroll
-        for (int k = 0; k < kPlanVals; ++k) {
-            int64_t t = 0;
-#pragma unroll
-            for (int w = 0; w < kWavesPerBlock; ++w) t += sh[k][w];
-            tile_vals[kPlanVals * blockIdx.x + k] = t;
-        }
-    }
-}
-
-// One block of kScanBlock threads: exclusive scan over the tiles, in place,
-// and the totals.  Each thread first sums a contiguous run of tiles, then one
-// block scan combines the runs.
-constexpr int kScanBlock = 1024;
-
-__global__ __launch_bounds__(kScanBlock) void plan_scan_kernel(int64_t *__restrict__ tile_vals, int64_t tiles,
-                                                               PlanCounts *__restrict__ counts) {
-    const int64_t per = (tiles + kScanBlock - 1) / kScanBlock;
-    const int64_t t0 = static_cast<int64_t>(threadIdx.x) * per;
-    const int64_t t1 = t0 + per < tiles ? t0 + per : tiles;
-    Need sum;
-#pragma unroll
-    for (int k = 0; k < kPlanVals; ++k) sum.v[k] = 0;
-    // unrolled so that several tiles' loads are in flight at once
-#pragma unroll 8
-    for (int64_t t = t0; t < t1; ++t)
-#pragma unroll
-        for (int k = 0; k < kPlanVals; ++k) sum.v[k] += tile_vals[kPlanVals * t + k];
-    Need excl;
-    const Need tot = block_excl_scan<kScanBlock>(sum, excl);
-#pragma unroll 8
-    for (int64_t t = t0; t < t1; ++t)
-#pragma unroll
-        for (int k = 0; k < kPlanVals; ++k) {
-            const int64_t v = tile_vals[kPlanVals * t + k];
-            tile_vals[kPlanVals * t + k] = excl.v[k];
-            excl.v[k] += v;
-        }
-    if (threadIdx.x == 0) {
-        for (int c = 0; c < kClasses; ++c) counts->cls[c] = static_cast<unsigned long long>(tot.v[c]);
-        counts->slots = static_cast<unsigned long long>(tot.v[kClasses]);
-        counts->splits = static_cast<unsigned long long>(tot.v[kClasses + 1]);
-        counts->pad[0] = counts->pad[1] = counts->pad[2] = 0;
+        counts->off[0] = static_cast<unsigned long long>(off1);
+        counts->off[1] = static_cast<unsigned long long>(off2);
     }
 }
 
@@ -160,25 +97,19 @@ __global__ __launch_bounds__(kScanBlock) void plan_scan_kernel(int64_t *__restri
 __host__ __device__ constexpr int pad_ix(int i) { return i + (i >> 3); }
 
 template <int L>
-__global__ __launch_bounds__(kBlock) void plan_write_kernel(const int64_t *__restrict__ ptr, int64_t nrows,
-                                                            const int64_t *__restrict__ tile_vals,
-                                                            const PlanCounts *__restrict__ counts,
-                                                            Desc *__restrict__ chunks, Split *__restrict__ splits) {
+__global__ __launch_bounds__(kBlock) void plan_kernel(const int64_t *__restrict__ ptr, int64_t nrows,
+                                                      PlanCounts *__restrict__ counts, Desc *__restrict__ chunks,
+                                                      Split *__restrict__ splits) {
     constexpr Geom g = make_geom(L);
     __shared__ int64_t sptr[pad_ix(kPlanTile) + 1];
+    __shared__ int64_t sbase[kPlanVals];
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kPlanTile;
     for (int i = threadIdx.x; i <= kPlanTile; i += kBlock) {
         const int64_t row = base + i;
         sptr[pad_ix(i)] = ptr[row < nrows ? row : nrows];
     }
     __syncthreads();
-    int64_t cbase[kClasses];
-    int64_t b = 0;
-#pragma unroll
-    for (int c = 0; c < kClasses; ++c) {
-        cbase[c] = b;
-        b += static_cast<int64_t>(counts->cls[c]);
-    }
+    const int64_t cbase[kClasses] = {0, static_cast<int64_t>(counts->off[0]), static_cast<int64_t>(counts->off[1])};
     int64_t e0[kPlanRowsPerThread], deg[kPlanRowsPerThread];
     Need mine;
 #pragma unroll
@@ -194,9 +125,19 @@ __global__ __launch_bounds__(kBlock) void plan_write_kernel(const int64_t *__res
         for (int k = 0; k < kPlanVals; ++k) mine.v[k] += n.v[k];
     }
     Need run;
-    block_excl_scan(mine, run);
+    const Need tot = block_excl_scan(mine, run);
+    // one reservation per counter for the whole tile: thread k adds the tile's total of counter k
+    // (vector atomics, all in flight together)
+    if (threadIdx.x < kPlanVals) {
+        int64_t t = 0;
 #pragma unroll
-    for (int k = 0; k < kPlanVals; ++k) run.v[k] += tile_vals[kPlanVals * blockIdx.x + k];
+        for (int k = 0; k < kPlanVals; ++k) t = threadIdx.x == k ? tot.v[k] : t;
+        sbase[threadIdx.x] =
+            t > 0 ? static_cast<int64_t>(atomicAdd(&counts->ctr[threadIdx.x].v, static_cast<unsigned long long>(t))) : 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kPlanVals; ++k) run.v[k] += sbase[k];
 #pragma unroll
     for (int r = 0; r < kPlanRowsPerThread; ++r) {
         if (deg[r] <= g.DS) continue;
@@ -234,14 +175,11 @@ __global__ __launch_bounds__(kBlock) void plan_write_kernel(const int64_t *__res
 namespace {
 template <int L>
 int launch_plan_t(const int64_t *ptr, int64_t nrows, const PlanBounds &b, const PlanWs &w, hipStream_t stream) {
-    const unsigned tiles = static_cast<unsigned>(b.tiles);
-    hipLaunchKernelGGL(plan_count_kernel<L>, dim3(tiles), dim3(kBlock), 0, stream, ptr, nrows, w.tile_vals);
-    if (int rc = check_launch("plan count")) return rc;
-    hipLaunchKernelGGL(plan_scan_kernel, dim3(1), dim3(kScanBlock), 0, stream, w.tile_vals, b.tiles, w.counts);
-    if (int rc = check_launch("plan scan")) return rc;
-    hipLaunchKernelGGL(plan_write_kernel<L>, dim3(tiles), dim3(kBlock), 0, stream, ptr, nrows, w.tile_vals, w.counts,
-                       w.chunks, w.splits);
-    return check_launch("plan write");
+    hipLaunchKernelGGL(plan_init_kernel, dim3(1), dim3(kWave), 0, stream, w.counts, b.cap[0], b.cap[0] + b.cap[1]);
+    if (int rc = check_launch("plan init")) return rc;
+    hipLaunchKernelGGL(plan_kernel<L>, dim3(static_cast<unsigned>(b.tiles)), dim3(kBlock), 0, stream, ptr, nrows,
+                       w.counts, w.chunks, w.splits);
+    return check_launch("plan");
 }
 }  // namespace
 
