@@ -119,8 +119,10 @@ def source_hash(files=None):
 
 
 def committed_csr2_bytes():
-    """Per-dispatch HBM bytes (calibrated FETCH_SIZE + WRITE_SIZE) of each config-2 call's dominant kernel,
-    from the committed summary, if the CSR sources are unchanged since it was taken."""
+    """Per-dispatch memory-side bytes (calibrated FETCH_SIZE + WRITE_SIZE: what the L2s read from and write
+    to the memory side, i.e. the 256 MB memory-side cache in front of HBM, so an upper bound on HBM traffic)
+    of each config-2 call's dominant kernel, from the committed summary, if the CSR sources are unchanged
+    since it was taken."""
     if not os.path.exists(CSR2_MD):
         return None
     vals = {}
@@ -128,10 +130,10 @@ def committed_csr2_bytes():
         if line.startswith("- ") and ": " in line:
             k, v = line[2:].strip().split(": ", 1)
             vals[k.strip("` ")] = v.strip("` ")
-    if vals.get("csr_source_hash") != source_hash(CSR_SOURCES) or "dram_bytes_per_dispatch" not in vals:
+    if vals.get("csr_source_hash") != source_hash(CSR_SOURCES) or "memside_bytes_per_dispatch" not in vals:
         return None
     try:
-        return json.loads(vals["dram_bytes_per_dispatch"])
+        return json.loads(vals["memside_bytes_per_dispatch"])
     except ValueError:
         return None
 
@@ -229,7 +231,7 @@ def summarize_csr2(fetch_dir, write_dir):
     rows += ["",
              f"- copy_calibration: a {COPY_BYTES} B device copy reads FETCH_SIZE {fcopy:.1f} KiB (scale {fscale:.3f}) "
              f"and WRITE_SIZE {wcopy:.1f} KiB (scale {wscale:.3f})",
-             f"- dram_bytes_per_dispatch: {json.dumps({k: round(v) for k, v in total.items()})}",
+             f"- memside_bytes_per_dispatch: {json.dumps({k: round(v) for k, v in total.items()})}",
              f"- csr_source_hash: {source_hash(CSR_SOURCES)}"]
     print("\n".join(rows))
 
@@ -582,16 +584,17 @@ def paths(args, torch, tb, synth):
             d.update(alg_bytes=alg[akey], alg_gbs=alg[akey] / r["step_ms"] / 1e6,
                      frac_hbm=alg[akey] / r["step_ms"] / 1e6 / HBM_PEAK_GBS)
         if key in CSR2_KERNELS:
-            # the dominant kernel of the call (HIP events around it); its rocprofv3-measured HBM bytes
-            # (calibrated FETCH_SIZE + WRITE_SIZE per dispatch) come from the committed summary while the
-            # CSR sources are unchanged, else null
+            # the dominant kernel of the call (HIP events around it); its rocprofv3-measured memory-side
+            # bytes (calibrated FETCH_SIZE + WRITE_SIZE per dispatch: L2 misses and write-backs, served by
+            # the 256 MB memory-side cache or HBM) come from the committed summary while the CSR sources are
+            # unchanged, else null
             k = float(np.mean(r["kernel_ms"]))
             d.update(kernel=CSR2_KERNELS[key], kernel_ms=k)
             if akey in alg:
                 d.update(kernel_alg_gbs=alg[akey] / k / 1e6, kernel_frac_hbm=alg[akey] / k / 1e6 / HBM_PEAK_GBS)
             b = dram.get(key) if dram else None
-            d.update(dram_bytes=b, dram_gbs=(b / k / 1e6) if b else None,
-                     dram_frac_hbm=(b / k / 1e6 / HBM_PEAK_GBS) if b else None)
+            d.update(memside_bytes=b, memside_gbs=(b / k / 1e6) if b else None,
+                     memside_frac_hbm=(b / k / 1e6 / HBM_PEAK_GBS) if b else None)
         res[name] = d
         log(f"{name}: {d['ms']:.3f} ms")
     del rel, xd, wd, dyd, rev, am
@@ -672,8 +675,8 @@ def paths(args, torch, tb, synth):
         rr = time_steps(torch, tb, lambda: tb.tiga_mp_knn_fwd(pd, xd, g["k"], ws=ws), steps, warm)
         k = float(np.mean(rr["kernel_ms"]))
         # queries answered and (query, neighbour) pairs selected per second; the select kernel evaluates
-        # only the candidates its exact box tests cannot exclude (about 1,000 per query at 131,072 points,
-        # from the scalar-load counter in the kNN profile), not all n (n - 1) pairs
+        # only the candidates its exact box tests cannot exclude (at most about 8,800 per query at
+        # 131,072 points, bounded by the scalar-load counter in the kNN profile), not all n (n - 1) pairs
         res[f"knn_{nk}_k16_f1"] = dict(ms=rr["step_ms"], select_kernel_ms=k,
                                         queries_per_s=nk / (rr["step_ms"] * 1e-3),
                                         selected_pairs_per_s=nk * g["k"] / (rr["step_ms"] * 1e-3))
