@@ -702,8 +702,8 @@ def paths(args, torch, tb, synth):
 
 
 def profile_pass(args, torch, tb, synth):
-    """Workload for counter runs: a plain copy of known size, then three steps (csr); or three forward calls on
-    the radius or dense workload."""
+    """Workload for counter runs: a plain copy of known size, then three steps (csr); or three calls on one of the
+    other workloads (radius: forward and backward)."""
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
     if args.profile_pass == "csr2":
         src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
@@ -729,9 +729,10 @@ def profile_pass(args, torch, tb, synth):
         return
     if args.profile_pass == "radius":
         g = synth.config3()
-        pd, xd = dev(g["pos"]), dev(g["x"])
+        pd, xd, dyd = dev(g["pos"]), dev(g["x"]), dev(g["dy"])
         for _ in range(3):
             tb.tiga_mp_radius_fwd(pd, xd, g["radius"], g["sigma"])
+            tb.tiga_mp_radius_bwd(pd, xd, dyd, g["radius"], g["sigma"])
         torch.cuda.synchronize()
         log("profile pass done")
         return

@@ -62,13 +62,12 @@ __global__ __launch_bounds__(256) void stream_copy(const f32x4 *__restrict__ a, 
         __builtin_nontemporal_store(__builtin_nontemporal_load(a + i), b + i);
 }
 
-// LPR lanes of 16 B per row; 4 rows in flight per lane.  CASE only tells the measurements apart in
+// LPR lanes of 16 B per row; U rows in flight per lane.  CASE only tells the measurements apart in
 // a profiler's per-kernel tables (same code for every case).
-template <int LPR, int CASE>
+template <int LPR, int CASE, int U = 4>
 __global__ __launch_bounds__(256) void gather_rows(const int32_t *__restrict__ idx, const f32x4 *__restrict__ tab,
                                                    int64_t n, float *out) {
     constexpr int S = 64 / LPR;
-    constexpr int U = 4;
     const int lane = threadIdx.x & 63;
     const int slot = lane / LPR, q = lane % LPR;
     const int64_t wave = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -185,6 +184,16 @@ int main() {
     const float t_g64 = best_ms([&] {
         hipLaunchKernelGGL((gather_rows<4, 64>), dim3(grid), dim3(256), 0, 0, idx, tab, idx_n, out);
     });
+    // occupancy: the same 64-byte gathers with 1 row in flight per lane, and with 1/8, 1/4 and 1/2
+    // of the grid (256 CUs x 8 blocks of 4 wavefronts), i.e. 1, 2 and 4 wavefronts per SIMD
+    const float t_g64_u1 = best_ms([&] {
+        hipLaunchKernelGGL((gather_rows<4, 641, 1>), dim3(grid), dim3(256), 0, 0, idx, tab, idx_n, out);
+    });
+    float t_g64_grid[3];
+    for (int k = 0; k < 3; ++k)
+        t_g64_grid[k] = best_ms([&] {
+            hipLaunchKernelGGL((gather_rows<4, 6400>), dim3(grid >> (3 - k)), dim3(256), 0, 0, idx, tab, idx_n, out);
+        });
     const int64_t n128 = idx_n / 2;
     hipLaunchKernelGGL(init_idx, dim3(grid), dim3(256), 0, 0, idx, n128, static_cast<uint32_t>(tab_bytes / 128));
     const float t_g128 = best_ms([&] {
@@ -224,11 +233,13 @@ int main() {
            "\"gather128_rows_per_s\": %.4g, \"gather128_useful_gbs\": %.1f, "
            "\"gather32_rows_per_s\": %.4g, \"gather256_rows_per_s\": %.4g, \"gather256_useful_gbs\": %.1f, "
            "\"gather64_table64mb_rows_per_s\": %.4g, \"gather64_table256mb_rows_per_s\": %.4g, "
+           "\"gather64_one_in_flight_rows_per_s\": %.4g, \"gather64_waves_per_simd_1_2_4_rows_per_s\": [%.4g, %.4g, %.4g], "
            "\"fma_fp32_tflops\": %.2f, \"rsq_per_s\": %.4g, \"exp_per_s\": %.4g}\n",
            p.gcnArchName, cus, idx_n * 4.0 / t_read / 1e6, idx_n * 8.0 / t_copy / 1e6, idx_n / (t_g64 * 1e-3),
            idx_n * 68.0 / t_g64 / 1e6, n128 / (t_g128 * 1e-3), n128 * 132.0 / t_g128 / 1e6,
            n32 / (t_g32 * 1e-3), n256 / (t_g256 * 1e-3), n256 * 260.0 / t_g256 / 1e6, nsm / (t_g64_64m * 1e-3),
-           nsm / (t_g64_256m * 1e-3),
+           nsm / (t_g64_256m * 1e-3), idx_n / (t_g64_u1 * 1e-3), idx_n / (t_g64_grid[0] * 1e-3),
+           idx_n / (t_g64_grid[1] * 1e-3), idx_n / (t_g64_grid[2] * 1e-3),
            2.0 * ops / (t_fma * 1e-3) / 1e12, ops / (t_rsq * 1e-3), ops / (t_exp * 1e-3));
     CHECK(hipFree(idx));
     CHECK(hipFree(tab));
