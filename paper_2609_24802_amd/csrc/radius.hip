@@ -200,52 +200,49 @@ __device__ __forceinline__ void lds_fence() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
-// Cells of XCD (blockIdx.x % 8) form one contiguous range, strided over that
-// XCD's waves, so neighbouring cells are consumed under one L2.  The grid is a
-// multiple of 8 blocks.
-struct CellSched {
-    int64_t c, hi, step;
-};
+// Visit order: the cell grid is cut into bricks of 8 x 8 x 8 cells (thinner at
+// the far faces), walked brick by brick (x-, then y-, then z-major; cells within
+// a brick the same way); order[t] is the t-th cell.  Each XCD (blockIdx.x % 8)
+// owns one contiguous eighth of that order, and its waves take the next cell
+// from a counter of their own (one 256-byte line per XCD) as they finish the
+// last: cell costs vary (Poisson occupancy), and a fixed cells-to-waves split
+// leaves the last waves running long after the rest.  The cells in flight on
+// an XCD at any time thus form a compact block whose neighbour rows stay in
+// that XCD's L2; a run of whole x-rows of cells would instead touch three full
+// z-planes of rows per pass.  The grid is a multiple of 8 blocks.
+constexpr float kLog2e = 1.44269504088896341f;
+constexpr int kBrickLog = 3;
+constexpr int kBrick = 1 << kBrickLog;
+constexpr int kSchedStride = 64;  // uint32 per XCD counter: one 256-byte line each
 
-__device__ __forceinline__ CellSched cell_sched(int64_t ncell) {
-    const unsigned x = blockIdx.x % kXcds, lb = blockIdx.x / kXcds, nbx = gridDim.x / kXcds;
-    // the wave index, made visibly uniform so that cell bounds and destination
-    // records are fetched with scalar loads
-    const int64_t lw = static_cast<int64_t>(lb) * (kBlock / kWave) + uniform(static_cast<int>(threadIdx.x / kWave));
-    CellSched s;
-    s.c = ncell * x / kXcds + lw;
-    s.hi = ncell * (x + 1) / kXcds;
-    s.step = static_cast<int64_t>(nbx) * (kBlock / kWave);
-    return s;
+// Next visit index of this wave's XCD share (one lane's atomic, broadcast).
+__device__ __forceinline__ int64_t next_visit(uint32_t *__restrict__ sched, int64_t lo) {
+    uint32_t v = 0;
+    if (lane_id() == 0) v = atomicAdd(sched + (blockIdx.x % kXcds) * kSchedStride, 1u);
+    return lo + __builtin_amdgcn_readfirstlane(v);
 }
 
-// Wave-uniform candidate runs of cell (cx, cy, cz): run k covers positions
-// [pre[k], pre[k] + len_k) of the flattened candidate sequence, starting at
-// cell-ordered index b[k].  Returns the number of candidates.
-__device__ __forceinline__ int32_t cell_runs(const Params &p, const int64_t *__restrict__ start, int cx, int cy,
-                                             int cz, int32_t (&b)[9], int32_t (&pre)[9]) {
-    const int lane = lane_id();
-    const int x0 = cx > 0 ? cx - 1 : 0;
-    const int x1 = cx + 1 < p.dim[0] ? cx + 1 : p.dim[0] - 1;
-    int32_t rb = 0, rl = 0;
-    if (lane < 9) {
-        const int z = cz - 1 + lane / 3;
-        const int y = cy - 1 + lane % 3;
-        if (z >= 0 && z < p.dim[2] && y >= 0 && y < p.dim[1]) {
-            const int rowc = (z * p.dim[1] + y) * p.dim[0];
-            const int64_t s0 = start[rowc + x0];
-            rb = static_cast<int32_t>(s0);
-            rl = static_cast<int32_t>(start[rowc + x1 + 1] - s0);
-        }
+// order[rank(c)] = c for every cell c: the rank counts the cells of the whole
+// slabs, brick rows and bricks before c's, then c's place inside its brick.
+// Also clears the XCD counters of the consuming kernel that follows.
+__global__ __launch_bounds__(kBlock) void visit_order_kernel(const Params *__restrict__ prm,
+                                                            int32_t *__restrict__ order,
+                                                            uint32_t *__restrict__ sched) {
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < kXcds * kSchedStride; i += kBlock) sched[i] = 0u;
+    const Params p = *prm;
+    const int64_t X = p.dim[0], Y = p.dim[1], Z = p.dim[2];
+    for (int64_t c = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x; c < p.ncell;
+         c += static_cast<int64_t>(gridDim.x) * kBlock) {
+        const int64_t cx = c % X, cy = (c / X) % Y, cz = c / (X * Y);
+        const int64_t x0 = cx & ~static_cast<int64_t>(kBrick - 1), y0 = cy & ~static_cast<int64_t>(kBrick - 1),
+                      z0 = cz & ~static_cast<int64_t>(kBrick - 1);
+        const int64_t h = Z - z0 < kBrick ? Z - z0 : kBrick;
+        const int64_t wy = Y - y0 < kBrick ? Y - y0 : kBrick;
+        const int64_t wx = X - x0 < kBrick ? X - x0 : kBrick;
+        const int64_t rank = z0 * X * Y + y0 * h * X + x0 * h * wy + (cz - z0) * wy * wx + (cy - y0) * wx + (cx - x0);
+        order[rank] = static_cast<int32_t>(c);
     }
-    int32_t total = 0;
-#pragma unroll
-    for (int k = 0; k < 9; ++k) {
-        b[k] = __builtin_amdgcn_readlane(rb, k);
-        pre[k] = total;
-        total += __builtin_amdgcn_readlane(rl, k);
-    }
-    return total;
 }
 
 // Split factor for a flush over dn destinations with G groups: the largest
@@ -282,59 +279,144 @@ __device__ __forceinline__ void put_k(float *__restrict__ base, int64_t unit, co
     }
 }
 
+// v[lane] = val (val and lane wave-uniform): one v_writelane_b32 (the lane
+// select is taken from m0, which does not count against the one-scalar-operand
+// limit).
+__device__ __forceinline__ void set_lane(int &v, int lane, int val) {
+    asm("v_writelane_b32 %0, %1, %2" : "+v"(v) : "s"(val), "{m0}"(lane));
+}
+
+// Candidate positions of a cell: the 3 x 3 (z, y) rows of its neighbourhood,
+// each one run of up to 3 cells that is contiguous in cell order, laid end to
+// end.  Lane k < 9 loads run k's bounds (one round trip for all nine); the runs
+// are then turned, window by window, into an LDS table that maps each candidate
+// position to its cell-ordered record index, so a chunk of 64 candidates is
+// decoded by one LDS read per lane.
+constexpr int kWin = 256;  // candidate positions per table window
+typedef int32_t CandTable[kWin];
+
+struct CellRuns {
+    int32_t pos;    // lane k < 9: first position of run k
+    int32_t len;    // lane k < 9: its length
+    int32_t off;    // lane k < 9: record index - position within run k
+    int32_t total;  // number of candidates (uniform)
+};
+
+__device__ __forceinline__ CellRuns cell_runs(const Params &p, const int64_t *__restrict__ start, int cx, int cy,
+                                              int cz) {
+    const int lane = lane_id();
+    const int x0 = cx > 0 ? cx - 1 : 0;
+    const int x1 = cx + 1 < p.dim[0] ? cx + 1 : p.dim[0] - 1;
+    int64_t s0 = 0;
+    int32_t len = 0;
+    if (lane < 9) {
+        const int z = cz - 1 + lane / 3;
+        const int y = cy - 1 + lane % 3;
+        if (z >= 0 && z < p.dim[2] && y >= 0 && y < p.dim[1]) {
+            const int64_t rowc = (static_cast<int64_t>(z) * p.dim[1] + y) * p.dim[0];
+            s0 = start[rowc + x0];
+            len = static_cast<int32_t>(start[rowc + x1 + 1] - s0);
+        }
+    }
+    // exclusive prefix of the lengths over lanes 0..8
+    int32_t pos = 0, total = 0;
+#pragma unroll
+    for (int k = 0; k < 9; ++k) {
+        const int32_t l = __builtin_amdgcn_readlane(len, k);
+        pos = lane == k ? total : pos;
+        total += l;
+    }
+    return CellRuns{pos, len, static_cast<int32_t>(s0) - pos, total};
+}
+
+// Table entries of positions [w0, min(w0 + kWin, total)).
+__device__ __forceinline__ void fill_candidates(const CellRuns &r, int32_t w0, CandTable &tab) {
+    const int lane = lane_id();
+    const int32_t lo_l = r.pos > w0 ? r.pos : w0;
+    const int32_t hi_l = r.pos + r.len < w0 + kWin ? r.pos + r.len : w0 + kWin;
+#pragma unroll
+    for (int k = 0; k < 9; ++k) {
+        const int32_t lo = __builtin_amdgcn_readlane(lo_l, k), hi = __builtin_amdgcn_readlane(hi_l, k);
+        if (lo >= hi) continue;
+        const int32_t off = __builtin_amdgcn_readlane(r.off, k);
+        for (int32_t q = lo + lane; q < hi; q += kWave) tab[q - w0] = q + off;
+    }
+}
+
 // Phase 1 over every cell of this wave; `flush(cnt, dn, d0, id, first)` runs
 // phase 2 for the destinations d0 .. d0 + dn - 1 (lane d holds the list
-// length `cnt` and point id `id` of destination d).
+// length `cnt` and point id `id` of destination d).  Weights are
+// exp2(d2 * nis_log2e), nis_log2e = -log2(e) / sigma^2.
 template <class Flush>
-__device__ __forceinline__ void cell_consume(const Params &p, const int64_t *__restrict__ start,
-                                             const float4 *__restrict__ rec, float r2, float neg_inv_s2,
-                                             CellList &list, int32_t *__restrict__ count, Flush &&flush) {
+__device__ __forceinline__ void cell_consume(const Params &p, const int32_t *__restrict__ order,
+                                             uint32_t *__restrict__ sched, const int64_t *__restrict__ start,
+                                             const float4 *__restrict__ rec, float r2, float nis_log2e,
+                                             CellList &list, CandTable &tab, int32_t *__restrict__ count,
+                                             Flush &&flush) {
     const int lane = lane_id();
-    const int64_t ncell = p.ncell;
-    for (CellSched sc = cell_sched(ncell); sc.c < sc.hi; sc.c += sc.step) {
-        const int64_t c = sc.c;
+    const int64_t lo = static_cast<int64_t>(p.ncell) * (blockIdx.x % kXcds) / kXcds;
+    const int64_t hi = static_cast<int64_t>(p.ncell) * (blockIdx.x % kXcds + 1) / kXcds;
+    for (int64_t t = next_visit(sched, lo), tn; t < hi; t = tn) {
+        tn = next_visit(sched, lo);  // taken now, used after this cell: its latency is hidden
+        const int64_t c = order[t];
         const int64_t ds = start[c], de = start[c + 1];
         if (ds == de) continue;
         const int cx = static_cast<int>(c % p.dim[0]);
         const int cy = static_cast<int>((c / p.dim[0]) % p.dim[1]);
         const int cz = static_cast<int>(c / (static_cast<int64_t>(p.dim[0]) * p.dim[1]));
-        int32_t b[9], pre[9];
-        const int32_t total = cell_runs(p, start, cx, cy, cz, b, pre);
+        const CellRuns runs = cell_runs(p, start, cx, cy, cz);
+        const int32_t total = runs.total;
+        fill_candidates(runs, 0, tab);
+        // the destinations' own positions, which the test must skip: record
+        // d0 + d sits in run 4 (the cell's own row), at position d0 + d - off_4
+        const int32_t ds_pos = static_cast<int32_t>(ds) - __builtin_amdgcn_readlane(runs.off, 4);
         for (int64_t d0 = ds; d0 < de; d0 += kDch) {
             const int dn = static_cast<int>(de - d0 < kDch ? de - d0 : kDch);
             const int32_t idl = lane < dn ? __float_as_int(rec[d0 + lane].w) : -1;
+            const int32_t self0 = ds_pos + static_cast<int32_t>(d0 - ds);
             int cnt = 0, tot = 0;
             bool first = true;
-            for (int32_t c0 = 0; c0 < total; c0 += kWave) {
-                const int32_t pos = c0 + lane;
-                const bool inr = pos < total;
-                int32_t t = 0;
-#pragma unroll
-                for (int k = 0; k < 9; ++k)
-                    if (pos >= pre[k]) t = b[k] + (pos - pre[k]);
-                const float4 pj = inr ? rec[t] : make_float4(0.0f, 0.0f, 0.0f, __int_as_float(-1));
-                for (int d = 0; d < dn; ++d) {
-                    const float4 pd = rec[d0 + d];  // uniform address: a scalar load
-                    float d2;
-                    const bool near = accept(pd, pj, r2, d2);
-                    const bool ok = inr & near & (__float_as_int(pj.w) != __float_as_int(pd.w));
-                    const uint64_t mask = __builtin_amdgcn_ballot_w64(ok);
-                    if (mask == 0) continue;
-                    const int nnew = __popcll(mask);
-                    int cd = __builtin_amdgcn_readlane(cnt, d);
-                    if (cd + nnew > kCapC) {
-                        tot += cnt;
-                        flush(cnt, dn, d0, idl, first);
-                        first = false;
-                        cnt = 0;
-                        cd = 0;
+            for (int32_t w0 = 0; w0 < total; w0 += kWin) {
+                // window 0 of a cell with at most kWin candidates is filled once per cell
+                if (w0 > 0 || (d0 > ds && total > kWin)) {
+                    lds_fence();
+                    fill_candidates(runs, w0, tab);
+                }
+                lds_fence();
+                const int32_t w1 = total < w0 + kWin ? total : w0 + kWin;
+                for (int32_t c0 = w0; c0 < w1; c0 += kWave) {
+                    const int32_t pos = c0 + lane;
+                    // lanes past the end test a point at +inf, which no destination accepts
+                    const float4 pj = pos < w1 ? rec[tab[pos - w0]]
+                                               : make_float4(__int_as_float(0x7f800000), __int_as_float(0x7f800000),
+                                                             __int_as_float(0x7f800000), __int_as_float(-1));
+                    for (int d = 0; d < dn; ++d) {
+                        const float4 pd = rec[d0 + d];  // uniform address: a scalar load
+                        float d2;
+                        // pos - c0 == self only on the destination's own lane; each
+                        // compare is balloted on its own so that both masks come straight
+                        // from the compares
+                        const bool near = accept(pd, pj, r2, d2);
+                        const bool other = lane != self0 + d - c0;
+                        const uint64_t mask = __builtin_amdgcn_ballot_w64(near) & __builtin_amdgcn_ballot_w64(other);
+                        if (mask == 0) continue;
+                        const int nnew = __popcll(mask);
+                        int cd = __builtin_amdgcn_readlane(cnt, d);
+                        if (cd + nnew > kCapC) {
+                            tot += cnt;
+                            flush(cnt, dn, d0, idl, first);
+                            first = false;
+                            cnt = 0;
+                            cd = 0;
+                        }
+                        if (near & other) {
+                            const int pfx = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                                                      __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0));
+                            // (point id, weight)
+                            list[d][cd + pfx] = make_float2(pj.w, __builtin_amdgcn_exp2f(d2 * nis_log2e));
+                        }
+                        set_lane(cnt, d, cd + nnew);
                     }
-                    if (ok) {
-                        const int pfx = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
-                                                                  __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0));
-                        list[d][cd + pfx] = make_float2(pj.w, __expf(d2 * neg_inv_s2));  // (point id, weight)
-                    }
-                    cnt = lane == d ? cd + nnew : cnt;
                 }
             }
             tot += cnt;
@@ -351,15 +433,19 @@ __device__ __forceinline__ void cell_consume(const Params &p, const int64_t *__r
 // would spill dozens and keeps its registers.
 template <int K, int LPR, int UPL>
 __global__ __launch_bounds__(kBlock, UPL == 1 ? 7 : 1) void radius_fwd_cell_kernel(const Params *__restrict__ prm,
+                                                                 const int32_t *__restrict__ order,
+                                                                 uint32_t *__restrict__ sched,
                                                                  const int64_t *__restrict__ start,
                                                                  const float4 *__restrict__ rec,
                                                                  const float *__restrict__ xs, int64_t fu, float r2,
-                                                                 float neg_inv_s2, float *__restrict__ y,
+                                                                 float nis_log2e, float *__restrict__ y,
                                                                  int32_t *__restrict__ count) {
     constexpr int G = kWave / LPR;
     __shared__ CellList lists[kBlock / kWave];
+    __shared__ CandTable tabs[kBlock / kWave];
     const Params p = *prm;
-    CellList &list = lists[threadIdx.x / kWave];
+    const int wv = uniform(static_cast<int>(threadIdx.x / kWave));
+    CellList &list = lists[wv];
     const int lane = lane_id(), g = lane / LPR, q = lane % LPR;
     const uint32_t ufu = static_cast<uint32_t>(fu);  // n * fu < 2^32 (checked by the host)
     auto flush = [&](int cnt, int dn, int64_t, int32_t idl, bool first) {
@@ -431,27 +517,35 @@ __global__ __launch_bounds__(kBlock, UPL == 1 ? 7 : 1) void radius_fwd_cell_kern
         }
         lds_fence();
     };
-    cell_consume(p, start, rec, r2, neg_inv_s2, list, count, flush);
+    cell_consume(p, order, sched, start, rec, r2, nis_log2e, list, tabs[wv], count, flush);
 }
+
+struct Pos3 {
+    float x, y, z;
+};
 
 // Backward on the same schedule: dx_i = sum_j k_ij dy_j and
 // dp_i = sum_j (2 k_ij / sigma^2) (p_j - p_i) (<dy_i, x_j> + <dy_j, x_i>).
 // Each lane forms the part of the inner products its units cover; the parts
 // of a destination are added by the shuffle tree once per flush.
 template <int K, int LPR, int UPL, bool DX, bool DP>
-__global__ __launch_bounds__(kBlock) void radius_bwd_cell_kernel(const Params *__restrict__ prm,
+__global__ __launch_bounds__(kBlock, DP ? 5 : 6) void radius_bwd_cell_kernel(const Params *__restrict__ prm,
+                                                                 const int32_t *__restrict__ order,
+                                                                 uint32_t *__restrict__ sched,
                                                                  const int64_t *__restrict__ start,
                                                                  const float4 *__restrict__ rec,
                                                                  const float *__restrict__ pos,
                                                                  const float *__restrict__ xs,
                                                                  const float *__restrict__ ys, int64_t fu, float r2,
-                                                                 float neg_inv_s2, float two_inv_s2,
+                                                                 float nis_log2e, float two_inv_s2,
                                                                  float *__restrict__ dx, float *__restrict__ dp) {
     constexpr int G = kWave / LPR;
     constexpr int B = DP ? kBatchDp : kBatch;
     __shared__ CellList lists[kBlock / kWave];
+    __shared__ CandTable tabs[kBlock / kWave];
     const Params p = *prm;
-    CellList &list = lists[threadIdx.x / kWave];
+    const int wv = uniform(static_cast<int>(threadIdx.x / kWave));
+    CellList &list = lists[wv];
     const int lane = lane_id(), g = lane / LPR, q = lane % LPR;
     const uint32_t ufu = static_cast<uint32_t>(fu);  // n * fu < 2^32 (checked by the host)
     auto flush = [&](int cnt, int dn, int64_t d0, int32_t idl, bool first) {
@@ -516,9 +610,10 @@ __global__ __launch_bounds__(kBlock) void radius_bwd_cell_kernel(const Params *_
                             if (DP) load_k<K>(xs, t * ufu + uc[u], live, xj[b][u]);
                         }
                         if (DP) {
-                            // t is a valid point id for every entry (0 past the list end)
-                            const f32x4 v = {pos[t * 3 + 0], pos[t * 3 + 1], pos[t * 3 + 2], 0.0f};
-                            pj[b] = live ? v : f32x4{pd.x, pd.y, pd.z, pd.w};
+                            // t is a valid point id for every entry (0 past the list end);
+                            // one 12-byte load
+                            const Pos3 v = *reinterpret_cast<const Pos3 *>(pos + t * 3);
+                            pj[b] = live ? f32x4{v.x, v.y, v.z, 0.0f} : f32x4{pd.x, pd.y, pd.z, pd.w};
                         }
                     }
 #pragma unroll
@@ -577,7 +672,7 @@ __global__ __launch_bounds__(kBlock) void radius_bwd_cell_kernel(const Params *_
         }
         lds_fence();
     };
-    cell_consume(p, start, rec, r2, neg_inv_s2, list, nullptr, flush);
+    cell_consume(p, order, sched, start, rec, r2, nis_log2e, list, tabs[wv], nullptr, flush);
 }
 
 __global__ __launch_bounds__(kBlock) void neighbor_count_kernel(const Params *__restrict__ prm,
@@ -643,6 +738,8 @@ struct Ws {
     int32_t *cell, *cell_sorted;
     int32_t *perm_b;  // point id at each cell-ordered position
     int64_t *start;   // max_cells + 1 cell boundaries in cell order
+    int32_t *order;   // max_cells: the cell visit order of the consuming kernels
+    uint32_t *sched;  // the consuming kernels' per-XCD cell counters
     float4 *rec;
     void *sort;
     void *scan;
@@ -664,6 +761,8 @@ Ws carve(Carve &c, int64_t n, int64_t cells_per_point = 1) {
     w.cell_sorted = c.take<int32_t>(n);
     w.perm_b = c.take<int32_t>(n);
     w.start = c.take<int64_t>(w.max_cells + 1);
+    w.order = c.take<int32_t>(w.max_cells);
+    w.sched = c.take<uint32_t>(kXcds * kSchedStride);
     w.rec = c.take<float4>(n);
     w.sort = c.take<char>(csr::sort_keys_ws_bytes(n));
     w.scan = c.take<char>(scan_ws_bytes(n + 1));
@@ -697,6 +796,13 @@ int build(int64_t n, const float *pos, float radius, Ws &w, hipStream_t stream, 
     return check_launch("radius records");
 }
 
+// The cell visit order and cleared counters of the consuming kernels (after build).
+int visit_order(const Ws &w, hipStream_t stream) {
+    hipLaunchKernelGGL(visit_order_kernel, dim3(blocks_for(w.max_cells)), dim3(kBlock), 0, stream, w.prm, w.order,
+                       w.sched);
+    return check_launch("radius visit order");
+}
+
 // Persistent grid for the cell kernels: a multiple of 8 blocks (one share
 // per XCD), as many as stay resident.
 int cell_grid(const void *kernel) {
@@ -711,8 +817,8 @@ int fwd_cell(int64_t fu, const Ws &w, const float *x, float r2, float nis, float
     const void *kern = reinterpret_cast<const void *>(&radius_fwd_cell_kernel<K, LPR, UPL>);
     static const int grid = cell_grid(kern);
     prof_before(stream);
-    hipLaunchKernelGGL((radius_fwd_cell_kernel<K, LPR, UPL>), dim3(grid), dim3(kBlock), 0, stream, w.prm, w.start,
-                       w.rec, x, fu, r2, nis, y, count);
+    hipLaunchKernelGGL((radius_fwd_cell_kernel<K, LPR, UPL>), dim3(grid), dim3(kBlock), 0, stream, w.prm, w.order,
+                       w.sched, w.start, w.rec, x, fu, r2, nis, y, count);
     prof_after(stream);
     return check_launch("radius forward");
 }
@@ -740,7 +846,7 @@ int bwd_cell(int64_t fu, const Ws &w, const BwdIo &io, float r2, float nis, floa
     static const int grid = cell_grid(kern);
     prof_before(stream);
     hipLaunchKernelGGL((radius_bwd_cell_kernel<K, LPR, UPL, DX, DP>), dim3(grid), dim3(kBlock), 0, stream, w.prm,
-                       w.start, w.rec, io.pos, io.x, io.dy, fu, r2, nis, tis, io.dx, io.dp);
+                       w.order, w.sched, w.start, w.rec, io.pos, io.x, io.dy, fu, r2, nis, tis, io.dx, io.dp);
     prof_after(stream);
     return check_launch("radius backward");
 }
@@ -789,8 +895,9 @@ int forward(int64_t n, int32_t feat, const float *pos, const float *x, float rad
     Carve c(ws);
     Ws w = carve(c, n);
     if (int rc = build(n, pos, radius, w, stream)) return rc;
+    if (int rc = visit_order(w, stream)) return rc;
     const float r2 = radius * radius;
-    const float nis = -1.0f / (sigma * sigma);
+    const float nis = -1.0f / (sigma * sigma) * kLog2e;  // weights are exp2(d2 * nis)
     if (vec) return fwd_units<4>(fu, w, x, r2, nis, y, count, stream);
     return fwd_units<1>(fu, w, x, r2, nis, y, count, stream);
 }
@@ -803,8 +910,9 @@ int backward(int64_t n, int32_t feat, const float *pos, const float *x, float ra
     Carve c(ws);
     Ws w = carve(c, n);
     if (int rc = build(n, pos, radius, w, stream)) return rc;
+    if (int rc = visit_order(w, stream)) return rc;
     const float r2 = radius * radius;
-    const float nis = -1.0f / (sigma * sigma);
+    const float nis = -1.0f / (sigma * sigma) * kLog2e;  // weights are exp2(d2 * nis)
     const float tis = 2.0f / (sigma * sigma);
     const BwdIo io{pos, x, dy, dx, dpos};
 #define TIGA_B(KK)                                                                  \
