@@ -203,10 +203,13 @@ __device__ __forceinline__ void lds_fence() {
 // Visit order: the cell grid is cut into bricks of 8 x 8 x 8 cells (thinner at
 // the far faces), walked brick by brick (x-, then y-, then z-major; cells within
 // a brick the same way); order[t] is the t-th cell.  Each XCD (blockIdx.x % 8)
-// owns one contiguous eighth of that order, and its waves take the next cell
-// from a counter of their own (one 256-byte line per XCD) as they finish the
-// last: cell costs vary (Poisson occupancy), and a fixed cells-to-waves split
-// leaves the last waves running long after the rest.  The cells in flight on
+// owns one contiguous eighth of that order.  Each of its W waves takes cells
+// w and W + w of the share, then the next cell from a counter of the XCD's own
+// (one 256-byte line per XCD) as it finishes one: cell costs vary (Poisson
+// occupancy), and a fixed cells-to-waves split leaves the last waves running
+// long after the rest.  A wave always knows its next cell one cell ahead (the
+// counter is read, and the next cell's id loaded, while the current one runs),
+// so neither latency is exposed.  The cells in flight on
 // an XCD at any time thus form a compact block whose neighbour rows stay in
 // that XCD's L2; a run of whole x-rows of cells would instead touch three full
 // z-planes of rows per pass.  The grid is a multiple of 8 blocks.
@@ -215,11 +218,11 @@ constexpr int kBrickLog = 3;
 constexpr int kBrick = 1 << kBrickLog;
 constexpr int kSchedStride = 64;  // uint32 per XCD counter: one 256-byte line each
 
-// Next visit index of this wave's XCD share (one lane's atomic, broadcast).
-__device__ __forceinline__ int64_t next_visit(uint32_t *__restrict__ sched, int64_t lo) {
+// Next value of this wave's XCD counter (one lane's atomic, broadcast).
+__device__ __forceinline__ int64_t take_visit(uint32_t *__restrict__ sched) {
     uint32_t v = 0;
     if (lane_id() == 0) v = atomicAdd(sched + (blockIdx.x % kXcds) * kSchedStride, 1u);
-    return lo + __builtin_amdgcn_readfirstlane(v);
+    return __builtin_amdgcn_readfirstlane(v);
 }
 
 // order[rank(c)] = c for every cell c: the rank counts the cells of the whole
@@ -356,9 +359,16 @@ __device__ __forceinline__ void cell_consume(const Params &p, const int32_t *__r
     const int lane = lane_id();
     const int64_t lo = static_cast<int64_t>(p.ncell) * (blockIdx.x % kXcds) / kXcds;
     const int64_t hi = static_cast<int64_t>(p.ncell) * (blockIdx.x % kXcds + 1) / kXcds;
-    for (int64_t t = next_visit(sched, lo), tn; t < hi; t = tn) {
-        tn = next_visit(sched, lo);  // taken now, used after this cell: its latency is hidden
-        const int64_t c = order[t];
+    // waves per XCD and this wave's index among them (uniform)
+    const int64_t nw = static_cast<int64_t>(gridDim.x / kXcds) * (kBlock / kWave);
+    const int64_t lw = static_cast<int64_t>(blockIdx.x / kXcds) * (kBlock / kWave) +
+                       uniform(static_cast<int>(threadIdx.x / kWave));
+    int64_t t = lo + lw, t1 = lo + nw + lw, t2 = hi;
+    int64_t c = t < hi ? order[t] : 0, c1 = 0;
+    for (; t < hi; t = t1, c = c1, t1 = t2) {
+        // the cell after this one: its id now, and the counter for the one after that
+        c1 = t1 < hi ? order[t1] : 0;
+        t2 = t1 < hi ? lo + 2 * nw + take_visit(sched) : hi;
         const int64_t ds = start[c], de = start[c + 1];
         if (ds == de) continue;
         const int cx = static_cast<int>(c % p.dim[0]);
