@@ -219,6 +219,11 @@ int main() {
     const float t_g64_256m = best_ms([&] {
         hipLaunchKernelGGL((gather_rows<4, 64256>), dim3(grid), dim3(256), 0, 0, idx, tab, nsm, out);
     });
+    // and from a 2 MB table, which every XCD's 4 MB L2 holds: no request leaves the XCD
+    hipLaunchKernelGGL(init_idx, dim3(grid), dim3(256), 0, 0, idx, nsm, static_cast<uint32_t>((2LL << 20) / 64));
+    const float t_g64_2m = best_ms([&] {
+        hipLaunchKernelGGL((gather_rows<4, 642>), dim3(grid), dim3(256), 0, 0, idx, tab, nsm, out);
+    });
 
     const int vgrid = cus * 64;
     const double lanes = static_cast<double>(vgrid) * 256;
@@ -232,12 +237,14 @@ int main() {
            "\"gather64_rows_per_s\": %.4g, \"gather64_useful_gbs\": %.1f, "
            "\"gather128_rows_per_s\": %.4g, \"gather128_useful_gbs\": %.1f, "
            "\"gather32_rows_per_s\": %.4g, \"gather256_rows_per_s\": %.4g, \"gather256_useful_gbs\": %.1f, "
+           "\"gather64_table2mb_rows_per_s\": %.4g, "
            "\"gather64_table64mb_rows_per_s\": %.4g, \"gather64_table256mb_rows_per_s\": %.4g, "
            "\"gather64_one_in_flight_rows_per_s\": %.4g, \"gather64_waves_per_simd_1_2_4_rows_per_s\": [%.4g, %.4g, %.4g], "
            "\"fma_fp32_tflops\": %.2f, \"rsq_per_s\": %.4g, \"exp_per_s\": %.4g}\n",
            p.gcnArchName, cus, idx_n * 4.0 / t_read / 1e6, idx_n * 8.0 / t_copy / 1e6, idx_n / (t_g64 * 1e-3),
            idx_n * 68.0 / t_g64 / 1e6, n128 / (t_g128 * 1e-3), n128 * 132.0 / t_g128 / 1e6,
-           n32 / (t_g32 * 1e-3), n256 / (t_g256 * 1e-3), n256 * 260.0 / t_g256 / 1e6, nsm / (t_g64_64m * 1e-3),
+           n32 / (t_g32 * 1e-3), n256 / (t_g256 * 1e-3), n256 * 260.0 / t_g256 / 1e6, nsm / (t_g64_2m * 1e-3),
+           nsm / (t_g64_64m * 1e-3),
            nsm / (t_g64_256m * 1e-3), idx_n / (t_g64_u1 * 1e-3), idx_n / (t_g64_grid[0] * 1e-3),
            idx_n / (t_g64_grid[1] * 1e-3), idx_n / (t_g64_grid[2] * 1e-3),
            2.0 * ops / (t_fma * 1e-3) / 1e12, ops / (t_rsq * 1e-3), ops / (t_exp * 1e-3));
