@@ -861,6 +861,8 @@ def main():
         "roofline": {"bound": "hbm", "achieved": h["achieved"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": h["achieved"] / HBM_PEAK_GBS, "traffic": committed_traffic(),
                      "kernel": "gather_reduce_kernel", "kernel_ms": h["kernel_ms"],
+                     "kernel_ms_median": float(np.median(h["kernel_ms_all"])),
+                     "kernel_ms_range": [float(np.min(h["kernel_ms_all"])), float(np.max(h["kernel_ms_all"]))],
                      "bytes_per_launch": h["bytes_alg"],
                      "frac_of_measured_gather_ceiling": (h["E"] / (h["kernel_ms"] * 1e-3)) / ceil["gather64_rows_per_s"]
                      if ceil else None,
