@@ -19,7 +19,7 @@ ARCH = os.environ.get("TIGA_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-munsafe-fp-atomics",
-    # packed fp32 instructions stay disabled (build policy)
+    # packed fp32 instructions stay disabled by build policy: no v_pk_*_f32 is generated
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
     "-I", os.path.join(ROOT, "include"),
