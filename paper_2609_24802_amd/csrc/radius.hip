@@ -203,25 +203,31 @@ __device__ __forceinline__ void lds_fence() {
 // Visit order: the cell grid is cut into bricks of 8 x 8 x 8 cells (thinner at
 // the far faces), walked brick by brick (x-, then y-, then z-major; cells within
 // a brick the same way); order[t] is the t-th cell.  Each XCD (blockIdx.x % 8)
-// owns one contiguous eighth of that order.  Each of its W waves takes cells
-// w and W + w of the share, then the next cell from a counter of the XCD's own
-// (one 256-byte line per XCD) as it finishes one: cell costs vary (Poisson
-// occupancy), and a fixed cells-to-waves split leaves the last waves running
-// long after the rest.  A wave always knows its next cell one cell ahead (the
-// counter is read, and the next cell's id loaded, while the current one runs),
-// so neither latency is exposed.  The cells in flight on
+// owns one contiguous eighth of that order, dealt out by 4 counters of its own
+// (one 256-byte line each): counter k serves the XCD's waves w = k (mod 4) with
+// the cells k (mod 4) of the share.  Each such wave takes its class's cells w'
+// and W' + w' (w' = w / 4, W' waves in the class), then the next one from the
+// counter as it finishes one: cell costs vary (Poisson occupancy), and a fixed
+// cells-to-waves split leaves the last waves running long after the rest.
+// Increments of one counter are serialized where it lives, so a single counter
+// per XCD capped the rate at which cells could be handed out; four spread the
+// increments while the cells in flight stay one compact run of the order.  A
+// wave always knows its next cell one cell ahead (the counter is read, and the
+// next cell's id loaded, while the current one runs), so neither latency is
+// exposed.  The cells in flight on
 // an XCD at any time thus form a compact block whose neighbour rows stay in
 // that XCD's L2; a run of whole x-rows of cells would instead touch three full
 // z-planes of rows per pass.  The grid is a multiple of 8 blocks.
 constexpr float kLog2e = 1.44269504088896341f;
 constexpr int kBrickLog = 3;
 constexpr int kBrick = 1 << kBrickLog;
-constexpr int kSchedStride = 64;  // uint32 per XCD counter: one 256-byte line each
+constexpr int kSchedStride = 64;  // uint32 per counter: one 256-byte line each
+constexpr int kCtrPerXcd = 4;     // counters per XCD: counter k hands out the cells k (mod 4)
 
 // Next value of this wave's XCD counter (one lane's atomic, broadcast).
-__device__ __forceinline__ int64_t take_visit(uint32_t *__restrict__ sched) {
+__device__ __forceinline__ int64_t take_visit(uint32_t *__restrict__ sched, int k) {
     uint32_t v = 0;
-    if (lane_id() == 0) v = atomicAdd(sched + (blockIdx.x % kXcds) * kSchedStride, 1u);
+    if (lane_id() == 0) v = atomicAdd(sched + ((blockIdx.x % kXcds) * kCtrPerXcd + k) * kSchedStride, 1u);
     return __builtin_amdgcn_readfirstlane(v);
 }
 
@@ -232,7 +238,7 @@ __global__ __launch_bounds__(kBlock) void visit_order_kernel(const Params *__res
                                                             int32_t *__restrict__ order,
                                                             uint32_t *__restrict__ sched) {
     if (blockIdx.x == 0)
-        for (int i = threadIdx.x; i < kXcds * kSchedStride; i += kBlock) sched[i] = 0u;
+        for (int i = threadIdx.x; i < kXcds * kCtrPerXcd * kSchedStride; i += kBlock) sched[i] = 0u;
     const Params p = *prm;
     const int64_t X = p.dim[0], Y = p.dim[1], Z = p.dim[2];
     for (int64_t c = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x; c < p.ncell;
@@ -363,12 +369,16 @@ __device__ __forceinline__ void cell_consume(const Params &p, const int32_t *__r
     const int64_t nw = static_cast<int64_t>(gridDim.x / kXcds) * (kBlock / kWave);
     const int64_t lw = static_cast<int64_t>(blockIdx.x / kXcds) * (kBlock / kWave) +
                        uniform(static_cast<int>(threadIdx.x / kWave));
-    int64_t t = lo + lw, t1 = lo + nw + lw, t2 = hi;
+    // counter k = lw mod 4 serves the nwk waves of that residue; its i-th cell is lo + k + 4 i
+    // (every XCD has at least 4 waves, so every residue is served)
+    const int k = static_cast<int>(lw % kCtrPerXcd);
+    const int64_t nwk = (nw - k + kCtrPerXcd - 1) / kCtrPerXcd, lwk = lw / kCtrPerXcd;
+    int64_t t = lo + k + kCtrPerXcd * lwk, t1 = lo + k + kCtrPerXcd * (nwk + lwk), t2 = hi;
     int64_t c = t < hi ? order[t] : 0, c1 = 0;
     for (; t < hi; t = t1, c = c1, t1 = t2) {
         // the cell after this one: its id now, and the counter for the one after that
         c1 = t1 < hi ? order[t1] : 0;
-        t2 = t1 < hi ? lo + 2 * nw + take_visit(sched) : hi;
+        t2 = t1 < hi ? lo + k + kCtrPerXcd * (2 * nwk + take_visit(sched, k)) : hi;
         const int64_t ds = start[c], de = start[c + 1];
         if (ds == de) continue;
         const int cx = static_cast<int>(c % p.dim[0]);
@@ -772,7 +782,7 @@ Ws carve(Carve &c, int64_t n, int64_t cells_per_point = 1) {
     w.perm_b = c.take<int32_t>(n);
     w.start = c.take<int64_t>(w.max_cells + 1);
     w.order = c.take<int32_t>(w.max_cells);
-    w.sched = c.take<uint32_t>(kXcds * kSchedStride);
+    w.sched = c.take<uint32_t>(kXcds * kCtrPerXcd * kSchedStride);
     w.rec = c.take<float4>(n);
     w.sort = c.take<char>(csr::sort_keys_ws_bytes(n));
     w.scan = c.take<char>(scan_ws_bytes(n + 1));
