@@ -203,21 +203,22 @@ __device__ __forceinline__ void lds_fence() {
 // Visit order: the cell grid is cut into bricks of 8 x 8 x 8 cells (thinner at
 // the far faces), walked brick by brick (x-, then y-, then z-major; cells within
 // a brick the same way); order[t] is the t-th cell.  Each XCD (blockIdx.x % 8)
-// owns one contiguous eighth of that order, dealt out by 4 counters of its own
-// (one 256-byte line each): counter k serves the XCD's waves w = k (mod 4) with
-// the cells k (mod 4) of the share.  Each such wave takes its class's cells w'
-// and W' + w' (w' = w / 4, W' waves in the class), then the next one from the
-// counter as it finishes one: cell costs vary (Poisson occupancy), and a fixed
-// cells-to-waves split leaves the last waves running long after the rest.
-// Increments of one counter are serialized where it lives, so a single counter
-// per XCD capped the rate at which cells could be handed out; four spread the
-// increments while the cells in flight stay one compact run of the order.  A
-// wave always knows its next cell one cell ahead (the counter is read, and the
-// next cell's id loaded, while the current one runs), so neither latency is
-// exposed.  The cells in flight on
-// an XCD at any time thus form a compact block whose neighbour rows stay in
-// that XCD's L2; a run of whole x-rows of cells would instead touch three full
-// z-planes of rows per pass.  The grid is a multiple of 8 blocks.
+// owns one contiguous eighth of that order, so the cells in flight on an XCD
+// form a compact block whose neighbour rows stay in that XCD's L2 (a run of
+// whole x-rows of cells would touch three full z-planes of rows per pass).
+//
+// Dealing: cell costs vary (Poisson occupancy), and a fixed cells-to-waves
+// split leaves the last waves running long after the rest, so cells are taken
+// as waves finish.  An XCD has 4 counters (one 256-byte line each); counter k
+// serves its waves w = k (mod 4) with the cells k (mod 4) of its share.  Each
+// such wave takes its class's cells w' and W' + w' (w' = w / 4, W' waves in
+// the class, at least 1 since the grid has at least 8 blocks of 4 waves), then
+// the next one from the counter.  Increments of one counter are serialized
+// where it lives: a single counter per XCD capped the rate at which cells were
+// handed out, four spread the increments while the cells in flight stay one
+// compact run of the order.  A wave knows its next cell one cell ahead (the
+// counter is read, and the next cell's id loaded, while the current one runs),
+// so neither latency is exposed.
 constexpr float kLog2e = 1.44269504088896341f;
 constexpr int kBrickLog = 3;
 constexpr int kBrick = 1 << kBrickLog;
