@@ -234,7 +234,9 @@ size_t tiga_mp_radius_workspace(int64_t n, int32_t feat);
  *   count: int32 [n] or NULL.  reducer must be TIGA_REDUCE_SUM.
  *   feat == 0 computes the counts only (x and y may be NULL; count required):
  *   the first phase of tiga_radius_neighbors.
- * Requires n < 2^31, radius > 0, sigma > 0, finite positions. */
+ * Requires n < 2^31, radius finite and > 0, sigma > 0 with 2 / sigma^2 finite
+ * in fp32 (sigma >= 7.7e-20; TIGA_EINVAL otherwise).  A point with a non-finite
+ * coordinate has no neighbours (every d2 involving it compares false). */
 int tiga_mp_radius_fwd(int64_t n, int32_t feat, const float *pos, const float *x,
                        float radius, float sigma, int reducer, float *y, int32_t *count,
                        void *ws, size_t ws_bytes, void *stream);
@@ -244,7 +246,8 @@ int tiga_mp_radius_fwd(int64_t n, int32_t feat, const float *pos, const float *x
  *   dx_i = sum_{j in N(i)} k_ij dy_j
  *   dpos_i = sum_{j in N(i)} (2 k_ij / sigma^2) (p_j - p_i) (<dy_i, x_j> + <dy_j, x_i>)
  * with k_ij = exp(-|p_i - p_j|^2 / sigma^2).  dx: fp32 [n, feat] or NULL;
- * dpos: fp32 [n, 3] or NULL (x is only read when dpos is requested). */
+ * dpos: fp32 [n, 3] or NULL (x is only read when dpos is requested).
+ * The same requirements as tiga_mp_radius_fwd. */
 int tiga_mp_radius_bwd(int64_t n, int32_t feat, const float *pos, const float *x,
                        float radius, float sigma, const float *dy, float *dx, float *dpos,
                        void *ws, size_t ws_bytes, void *stream);

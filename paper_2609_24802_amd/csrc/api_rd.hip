@@ -26,6 +26,12 @@ int check_points(int64_t n, const float *pos) {
 int check_radius(float radius, float sigma) {
     if (!(radius > 0.0f) || !(radius < 3.0e38f)) return fail(TIGA_EINVAL, "radius must be finite and > 0");
     if (!(sigma > 0.0f) || !(sigma < 3.0e38f)) return fail(TIGA_EINVAL, "sigma must be finite and > 0");
+    // the kernels scale by -log2(e) / sigma^2 and 2 / sigma^2 in fp32: both must be finite, or a
+    // coincident pair (d2 = 0) would get weight exp2(0 * -inf) = NaN
+    const float two_inv_s2 = 2.0f / (sigma * sigma);
+    if (!(two_inv_s2 <= 3.4028234e38f))
+        return fail(TIGA_EINVAL, "sigma %g is too small: 2 / sigma^2 overflows fp32 (sigma must be >= 7.7e-20)",
+                    (double)sigma);
     return TIGA_OK;
 }
 

@@ -136,6 +136,11 @@ def test_radius_dense_errors(clib):
     assert rc == b.TIGA_EWORKSPACE
     rc = clib.tiga_mp_radius_bwd(100, 8, fake, None, 0.1, 0.05, fake, fake, fake, fake, 1 << 40, None)
     assert rc == b.TIGA_EINVAL  # dpos needs x
+    # 2 / sigma^2 must be finite in fp32 (else a coincident pair's weight would be NaN)
+    rc = clib.tiga_mp_radius_fwd(100, 8, fake, fake, 0.1, 1e-20, b.REDUCE_SUM, fake, None, fake, 1 << 40, None)
+    assert rc == b.TIGA_EINVAL and b"sigma" in clib.tiga_last_error()
+    rc = clib.tiga_mp_radius_bwd(100, 8, fake, fake, 0.1, 1e-20, fake, fake, fake, fake, 1 << 40, None)
+    assert rc == b.TIGA_EINVAL and b"sigma" in clib.tiga_last_error()
     rc = clib.tiga_mp_dense_fwd(100, fake, fake, 0.0, b.REDUCE_SUM, fake, fake, 1 << 40, None)
     assert rc == b.TIGA_EINVAL
     rc = clib.tiga_mp_dense_fwd(100, fake, fake, 0.01, b.REDUCE_MAX, fake, fake, 1 << 40, None)
