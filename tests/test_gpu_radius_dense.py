@@ -161,9 +161,10 @@ def test_radius_rejects_max(lib):
     assert e.value.code == lib.TIGA_EUNSUPPORTED
 
 
-def test_config3_full_size_sampled(lib):
+def test_config3_full_size(lib):
     """The measured workload (1M points, F = 32): every count of the fused forward and every
-    neighbour list bit-exact against the oracle's relation; values and gradients on 4,000 points."""
+    neighbour list bit-exact against the oracle's relation, and every value and gradient within
+    1e-5 * sum|terms| (the oracle needs a few seconds of the host's cores for each pass)."""
     g = synth.config3()
     pos, x, dy, r, s = g["pos"], g["x"], g["dy"], g["radius"], g["sigma"]
     n = pos.shape[0]
@@ -177,14 +178,16 @@ def test_config3_full_size_sampled(lib):
     assert np.array_equal(host(ptr), rptr)
     assert np.array_equal(host(idx), ridx)
     del c2, ptr, idx
-    pts = np.unique(np.random.default_rng(4).integers(0, n, 4000))
-    ry, rya, rcnt = oracle.radius_fwd(pos, x, r, s, pts=pts)
-    assert np.array_equal(host(cnt)[pts], rcnt)
-    assert_terms_close(host(y)[pts], ry, rya, what="config 3 y")
+    print("config 3: values", flush=True)
+    ry, rya, rcnt = oracle.radius_fwd(pos, x, r, s)
+    assert np.array_equal(host(cnt), rcnt)
+    assert_terms_close(host(y), ry, rya, what="config 3 y")
+    del ry, rya
+    print("config 3: gradients", flush=True)
     dx, dp = lib.tiga_mp_radius_bwd(pd, xd, dyd, r, s)
-    rdx, rdxa, rdp, rdpa = oracle.radius_bwd(pos, x, dy, r, s, pts=pts)
-    assert_terms_close(host(dx)[pts], rdx, rdxa, what="config 3 dx")
-    assert_terms_close(host(dp)[pts], rdp, rdpa, what="config 3 dpos")
+    rdx, rdxa, rdp, rdpa = oracle.radius_bwd(pos, x, dy, r, s)
+    assert_terms_close(host(dx), rdx, rdxa, what="config 3 dx")
+    assert_terms_close(host(dp), rdp, rdpa, what="config 3 dpos")
     # symmetric relation: the directed pair count is even; mean degree near 32
     total = int(rptr[-1])
     assert total % 2 == 0 and abs(total / n - 31.3) < 0.3
@@ -230,12 +233,13 @@ def test_dense_same_sign_adversarial(lib):
     assert_terms_close(host(y)[[0, 1, n - 1]], ry, rya, what="dense same-sign")
 
 
-def test_config4_full_size_sampled(lib):
+def test_config4_full_size(lib):
+    """Every one of the 65,536 outputs of the measured workload (4.3e9 ordered pairs: a few seconds
+    of the oracle on the host's cores)."""
     g = synth.config4()
     y = lib.tiga_mp_dense_fwd(dev(g["pos"]), dev(g["q"]), g["eps"])
-    pts = np.unique(np.random.default_rng(6).integers(0, 65536, 1500))
-    ry, rya = oracle.dense_fwd(g["pos"], g["q"], g["eps"], pts=pts)
-    assert_terms_close(host(y)[pts], ry, rya, what="config 4 y")
+    ry, rya = oracle.dense_fwd(g["pos"], g["q"], g["eps"])
+    assert_terms_close(host(y), ry, rya, what="config 4 y")
 
 
 def test_radius_autograd_wrapper(lib):
